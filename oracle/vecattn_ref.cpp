@@ -1,0 +1,524 @@
+// Oracle for vertical-vector sparse attention (VecAttention, arXiv 2603.29494).
+//
+// TEST INFRASTRUCTURE ONLY.  This file is the plain, slow, obviously-correct CPU
+// reference that the GPU library is checked against.  It shares no code, header,
+// table or helper with the HIP path under paper_2603_29494_amd/csrc, and the
+// product never links, loads or calls it.  Only tests/, the smoke check and the
+// CPU-baseline leg of the benchmark use it.
+//
+// Every quantity is computed in IEEE double from bf16 inputs (upcast exactly).
+// Loops are written in the order of the paper's definitions; there is no
+// blocking, fusion or reordering.  OpenMP only splits independent rows.
+//
+// Paper passages followed:
+//   * Eq. 1 (Sec. 2.1): S = Q K^T / sqrt(D), A = softmax(S), O = A V.
+//   * Eq. 2 (Sec. 3.1.1): pooled query Q_p[i] = mean of the P_q query rows of
+//     block i.
+//   * Sec. 3.1.1, estimated attention map A_p = softmax(Q_p K^T / sqrt(D)); the
+//     entry A_p[i, j] scores the vertical vector A[i*P_q:(i+1)*P_q, j].
+//   * Sec. 3.1.2: row-wise topK (keep exactly the k largest entries) and topP
+//     (keep entries until their cumulative attention mass reaches p).
+//   * Eq. 3 (Sec. 3.1.2): minS, Idx(i) = { j : s_ij >= rowmax_i - alpha }.
+//   * Eq. 4 (Sec. 3.2): O[I_B(i)] = softmax(Q[I_B(i)] K[Idx(i)]^T / sqrt(D)) V[Idx(i)].
+//   * Algorithm 2 (appendix, Vector-Sparse Computation): the tiled online-softmax
+//     recurrence, used here only as a second route to Eq. 4 for self-checks.
+//
+// Readings where the paper is silent (each is listed in the design doc):
+//   ragged last block pools only its existing rows; Q_p is rounded once from the
+//   exact double mean to bf16 (round to nearest, ties to even); causal selection
+//   ranges over keys up to the block's last row; ties are broken by lower key
+//   index; topP keeps the shortest prefix (score desc, index asc) whose mass is
+//   >= p; rows with no visible key produce O = 0 and LSE = -inf; GQA maps query
+//   head h to key/value head h / (Hq / Hkv).
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <limits>
+#include <utility>
+#include <vector>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+namespace {
+
+enum { ORA_OK = 0, ORA_ERR_ARG = 1, ORA_ERR_UNSUPPORTED = 2, ORA_ERR_CAPACITY = 3 };
+enum { SEL_TOPK = 0, SEL_TOPP = 1, SEL_MINS = 2 };
+
+double bf16_value(uint16_t bits) {
+  uint32_t u = static_cast<uint32_t>(bits) << 16;
+  float f;
+  std::memcpy(&f, &u, sizeof f);
+  return static_cast<double>(f);
+}
+
+// Round a double to the nearest bfloat16 value, ties to even, in one step.
+// bfloat16 keeps 8 significant bits and float32's exponent range; its smallest
+// subnormal is 2^-133 and its largest finite value is (2 - 2^-7) * 2^127.
+uint16_t bf16_round(double x) {
+  if (std::isnan(x)) return 0x7FC0;
+  const bool neg = std::signbit(x);
+  double a = std::fabs(x);
+  double y = 0.0;
+  if (a != 0.0 && !std::isinf(a)) {
+    int e;
+    std::frexp(a, &e);                      // a = f * 2^e with f in [0.5, 1)
+    int quantum = std::max(e - 8, -133);    // spacing of bf16 values near a
+    double units = std::ldexp(a, -quantum); // exact: power-of-two scaling
+    double r = std::nearbyint(units);       // default mode: nearest, ties to even
+    y = std::ldexp(r, quantum);
+  } else {
+    y = a;
+  }
+  const double max_bf16 = std::ldexp(255.0, 120);  // (2 - 2^-7) * 2^127
+  float f;
+  if (y > max_bf16) {
+    f = std::numeric_limits<float>::infinity();
+  } else {
+    f = static_cast<float>(y);  // exact: y is a bf16 value
+  }
+  if (neg) f = -f;
+  uint32_t u;
+  std::memcpy(&u, &f, sizeof u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+struct Shape {
+  int64_t B, Hq, Hkv, N, D;
+};
+
+// Element offset of row n of head h, batch b in a contiguous [B, H, N, D] tensor.
+inline int64_t row_off(int64_t b, int64_t h, int64_t n, int64_t H, int64_t N, int64_t D) {
+  return ((b * H + h) * N + n) * D;
+}
+
+inline int64_t num_blocks(int64_t N, int64_t P) { return (N + P - 1) / P; }
+
+// Number of keys a block may select from.  Non-causal: all N keys.  Causal:
+// keys 0 .. (last row of the block), so that every selected key is visible to
+// at least the block's last query row.
+inline int64_t eligible_keys(int64_t N, int64_t P, int64_t i, int causal) {
+  if (!causal) return N;
+  return std::min<int64_t>(N, (i + 1) * P);
+}
+
+// Eq. 2 for one block: exact double mean of the block's existing rows, then one
+// rounding to bf16.  Returns the pooled vector as doubles (the bf16 values).
+void pooled_query(const uint16_t* q, const Shape& s, int64_t P, int64_t b, int64_t h, int64_t i,
+                  std::vector<double>& out, uint16_t* bits_out) {
+  const int64_t r0 = i * P;
+  const int64_t r1 = std::min<int64_t>(s.N, r0 + P);
+  const int64_t n = r1 - r0;
+  out.assign(s.D, 0.0);
+  for (int64_t d = 0; d < s.D; ++d) {
+    double sum = 0.0;
+    for (int64_t r = r0; r < r1; ++r) sum += bf16_value(q[row_off(b, h, r, s.Hq, s.N, s.D) + d]);
+    const uint16_t rb = bf16_round(sum / static_cast<double>(n));
+    if (bits_out) bits_out[d] = rb;
+    out[d] = bf16_value(rb);
+  }
+}
+
+// Scores of the estimated map (Sec. 3.1.1): s_ij = <Q_p[i], k_j> / sqrt(D) for
+// every eligible key j, in key order.
+void pooled_scores(const uint16_t* q, const uint16_t* k, const Shape& s, int64_t P, int causal,
+                   int64_t b, int64_t h, int64_t i, std::vector<double>& scores) {
+  std::vector<double> qp;
+  pooled_query(q, s, P, b, h, i, qp, nullptr);
+  const int64_t g = s.Hq / s.Hkv;
+  const int64_t hk = h / g;
+  const int64_t L = eligible_keys(s.N, P, i, causal);
+  const double tau = 1.0 / std::sqrt(static_cast<double>(s.D));
+  scores.assign(L, 0.0);
+  for (int64_t j = 0; j < L; ++j) {
+    const uint16_t* kr = k + row_off(b, hk, j, s.Hkv, s.N, s.D);
+    double dot = 0.0;
+    for (int64_t d = 0; d < s.D; ++d) dot += qp[d] * bf16_value(kr[d]);
+    scores[j] = tau * dot;
+  }
+}
+
+// k_i for a keep ratio r: ceil(r * L) with a 1e-9 guard so that products such
+// as 0.1 * 640 that land a hair above an integer do not round up; at least one
+// key and at most L keys.
+int64_t topk_count(double ratio, int64_t L) {
+  double x = std::ceil(ratio * static_cast<double>(L) - 1e-9);
+  int64_t kk = static_cast<int64_t>(x);
+  kk = std::max<int64_t>(kk, 1);
+  kk = std::min<int64_t>(kk, L);
+  return kk;
+}
+
+// Keys of one row ordered by score descending, then by key index ascending
+// (the total order used to break ties).
+std::vector<int64_t> order_desc(const std::vector<double>& sc) {
+  std::vector<int64_t> ord(sc.size());
+  for (size_t j = 0; j < sc.size(); ++j) ord[j] = static_cast<int64_t>(j);
+  std::sort(ord.begin(), ord.end(), [&](int64_t a, int64_t b2) {
+    if (sc[a] != sc[b2]) return sc[a] > sc[b2];
+    return a < b2;
+  });
+  return ord;
+}
+
+// Number of leading keys (in score order) that topP keeps: the shortest prefix
+// whose softmax mass reaches p.  Masses use the row max for stability and are
+// accumulated in the same order.
+int64_t topp_count(const std::vector<double>& sc, const std::vector<int64_t>& ord, double p) {
+  const int64_t L = static_cast<int64_t>(sc.size());
+  if (p >= 1.0) return L;
+  const double m = sc[ord[0]];
+  double Z = 0.0;
+  for (int64_t t = 0; t < L; ++t) Z += std::exp(sc[ord[t]] - m);
+  double cum = 0.0;
+  for (int64_t t = 0; t < L; ++t) {
+    cum += std::exp(sc[ord[t]] - m);
+    if (cum >= p * Z) return t + 1;
+  }
+  return L;
+}
+
+// Eq. 3 with the global row max: every eligible key whose score is at least
+// rowmax - alpha.
+std::vector<int64_t> mins_global(const std::vector<double>& sc, double alpha) {
+  double m = -std::numeric_limits<double>::infinity();
+  for (double x : sc) m = std::max(m, x);
+  std::vector<int64_t> out;
+  for (size_t j = 0; j < sc.size(); ++j)
+    if (sc[j] >= m - alpha) out.push_back(static_cast<int64_t>(j));
+  return out;
+}
+
+// Eq. 3 applied the way Algorithm 1 applies it inside a thread block: keys are
+// split into groups of bk * gk; inside a group, tiles of bk keys are visited in
+// order and each tile keeps the keys whose score is at least (running max over
+// the tiles visited so far in this group) - alpha.  Comparator >= as in Eq. 3.
+std::vector<int64_t> mins_progressive(const std::vector<double>& sc, double alpha, int64_t bk,
+                                      int64_t gk) {
+  std::vector<int64_t> out;
+  const int64_t L = static_cast<int64_t>(sc.size());
+  const int64_t group = bk * gk;
+  for (int64_t g0 = 0; g0 < L; g0 += group) {
+    double run_max = -std::numeric_limits<double>::infinity();
+    for (int64_t t0 = g0; t0 < std::min(L, g0 + group); t0 += bk) {
+      const int64_t t1 = std::min(L, t0 + bk);
+      for (int64_t j = t0; j < t1; ++j) run_max = std::max(run_max, sc[j]);
+      for (int64_t j = t0; j < t1; ++j)
+        if (sc[j] >= run_max - alpha) out.push_back(j);
+    }
+  }
+  return out;
+}
+
+bool shape_ok(const Shape& s) {
+  return s.B > 0 && s.Hq > 0 && s.Hkv > 0 && s.N > 0 && s.D > 0 && s.Hq % s.Hkv == 0;
+}
+
+void set_threads(int32_t nthreads) {
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+  (void)nthreads;
+#endif
+}
+
+// Attention output for one query row over an explicit list of visible keys:
+// materialised softmax, Eq. 4 restricted to one row.
+void attend_row(const uint16_t* q, const uint16_t* k, const uint16_t* v, const Shape& s,
+                int64_t b, int64_t h, int64_t r, const std::vector<int64_t>& keys, double scale,
+                double* o_row, double* lse_out) {
+  const int64_t hk = h / (s.Hq / s.Hkv);
+  const uint16_t* qr = q + row_off(b, h, r, s.Hq, s.N, s.D);
+  for (int64_t d = 0; d < s.D; ++d) o_row[d] = 0.0;
+  if (keys.empty()) {
+    *lse_out = -std::numeric_limits<double>::infinity();
+    return;
+  }
+  std::vector<double> x(keys.size());
+  double m = -std::numeric_limits<double>::infinity();
+  for (size_t t = 0; t < keys.size(); ++t) {
+    const uint16_t* kr = k + row_off(b, hk, keys[t], s.Hkv, s.N, s.D);
+    double dot = 0.0;
+    for (int64_t d = 0; d < s.D; ++d) dot += bf16_value(qr[d]) * bf16_value(kr[d]);
+    x[t] = scale * dot;
+    m = std::max(m, x[t]);
+  }
+  double denom = 0.0;
+  for (size_t t = 0; t < keys.size(); ++t) denom += std::exp(x[t] - m);
+  for (size_t t = 0; t < keys.size(); ++t) {
+    const double w = std::exp(x[t] - m) / denom;
+    const uint16_t* vr = v + row_off(b, hk, keys[t], s.Hkv, s.N, s.D);
+    for (int64_t d = 0; d < s.D; ++d) o_row[d] += w * bf16_value(vr[d]);
+  }
+  *lse_out = m + std::log(denom);
+}
+
+}  // namespace
+
+extern "C" {
+
+int ora_bf16_round(const double* x, int64_t n, uint16_t* out) {
+  for (int64_t t = 0; t < n; ++t) out[t] = bf16_round(x[t]);
+  return ORA_OK;
+}
+
+// Eq. 2: pooled queries, bf16 bits, [B, Hq, ceil(N/P), D].
+int ora_pool(const uint16_t* q, int64_t B, int64_t H, int64_t N, int64_t D, int32_t block,
+             uint16_t* qp_out, int32_t nthreads) {
+  if (!q || !qp_out || block < 1 || B < 1 || H < 1 || N < 1 || D < 1) return ORA_ERR_ARG;
+  Shape s{B, H, H, N, D};
+  const int64_t Np = num_blocks(N, block);
+  set_threads(nthreads);
+#pragma omp parallel for schedule(dynamic)
+  for (int64_t w = 0; w < B * H * Np; ++w) {
+    const int64_t i = w % Np, h = (w / Np) % H, b = w / (Np * H);
+    std::vector<double> tmp;
+    pooled_query(q, s, block, b, h, i, tmp, qp_out + w * D);
+  }
+  return ORA_OK;
+}
+
+// Scores of one row of the estimated map (Sec. 3.1.1); writes L_i doubles.
+int ora_pooled_scores(const uint16_t* q, const uint16_t* k, int64_t B, int64_t Hq, int64_t Hkv,
+                      int64_t N, int64_t D, int32_t block, int32_t causal, int64_t b, int64_t h,
+                      int64_t i, double* scores_out, int64_t* L_out) {
+  Shape s{B, Hq, Hkv, N, D};
+  if (!q || !k || !scores_out || block < 1 || !shape_ok(s)) return ORA_ERR_ARG;
+  if (b < 0 || b >= B || h < 0 || h >= Hq || i < 0 || i >= num_blocks(N, block)) return ORA_ERR_ARG;
+  std::vector<double> sc;
+  pooled_scores(q, k, s, block, causal, b, h, i, sc);
+  for (size_t j = 0; j < sc.size(); ++j) scores_out[j] = sc[j];
+  if (L_out) *L_out = static_cast<int64_t>(sc.size());
+  return ORA_OK;
+}
+
+int64_t ora_topk_count(double ratio, int64_t L) { return topk_count(ratio, L); }
+
+// Selection (Sec. 3.1): for every block (or for the listed flat rows
+// w = (b * Hq + h) * Np + i), the selected key indices in ascending order in
+// idx[w * cap ...], padded with -1, and their number in counts[w].
+// mode 0 topK (param = keep ratio), 1 topP (param = mass p), 2 minS with the
+// global row max (param = alpha).  Threshold modes that select more than cap
+// keys keep the first cap keys in (score desc, index asc) order and add one to
+// *n_clamped.  topK with k_i > cap is a capacity error.
+int ora_select(const uint16_t* q, const uint16_t* k, int64_t B, int64_t Hq, int64_t Hkv, int64_t N,
+               int64_t D, int32_t block, int32_t causal, int32_t mode, double param, int64_t cap,
+               int32_t* idx, int32_t* counts, int64_t* n_clamped, const int64_t* rows,
+               int64_t n_rows, int32_t nthreads) {
+  Shape s{B, Hq, Hkv, N, D};
+  if (!q || !k || !idx || !counts || block < 1 || cap < 1 || !shape_ok(s)) return ORA_ERR_ARG;
+  if (mode == SEL_TOPK && !(param > 0.0 && param <= 1.0)) return ORA_ERR_ARG;
+  if (mode == SEL_TOPP && !(param > 0.0 && param <= 1.0)) return ORA_ERR_ARG;
+  if (mode == SEL_MINS && !(param >= 0.0)) return ORA_ERR_ARG;
+  if (mode < 0 || mode > 2) return ORA_ERR_ARG;
+  const int64_t Np = num_blocks(N, block);
+  if (mode == SEL_TOPK) {
+    for (int64_t i = 0; i < Np; ++i)
+      if (topk_count(param, eligible_keys(N, block, i, causal)) > cap) return ORA_ERR_CAPACITY;
+  }
+  const int64_t total = rows ? n_rows : B * Hq * Np;
+  int64_t clamped = 0;
+  set_threads(nthreads);
+#pragma omp parallel for schedule(dynamic) reduction(+ : clamped)
+  for (int64_t t = 0; t < total; ++t) {
+    const int64_t w = rows ? rows[t] : t;
+    const int64_t i = w % Np, h = (w / Np) % Hq, b = w / (Np * Hq);
+    std::vector<double> sc;
+    pooled_scores(q, k, s, block, causal, b, h, i, sc);
+    std::vector<int64_t> chosen;
+    if (mode == SEL_MINS) {
+      chosen = mins_global(sc, param);
+      if (static_cast<int64_t>(chosen.size()) > cap) {
+        std::vector<int64_t> ord = order_desc(sc);
+        std::vector<int64_t> keep;
+        for (int64_t j : ord)
+          if (sc[j] >= sc[ord[0]] - param && static_cast<int64_t>(keep.size()) < cap) keep.push_back(j);
+        chosen = keep;
+        clamped += 1;
+      }
+    } else {
+      std::vector<int64_t> ord = order_desc(sc);
+      const int64_t L = static_cast<int64_t>(sc.size());
+      int64_t n = (mode == SEL_TOPK) ? topk_count(param, L) : topp_count(sc, ord, param);
+      if (n > cap) {
+        n = cap;
+        clamped += 1;
+      }
+      chosen.assign(ord.begin(), ord.begin() + n);
+    }
+    std::sort(chosen.begin(), chosen.end());
+    int32_t* row = idx + w * cap;
+    for (int64_t c = 0; c < cap; ++c)
+      row[c] = c < static_cast<int64_t>(chosen.size()) ? static_cast<int32_t>(chosen[c]) : -1;
+    counts[w] = static_cast<int32_t>(chosen.size());
+  }
+  if (n_clamped) *n_clamped = clamped;
+  return ORA_OK;
+}
+
+// Progressive minS of one row as Algorithm 1 applies it (running max inside
+// each group of bk*gk keys); writes the kept indices ascending.
+int ora_mins_progressive_row(const double* scores, int64_t L, double alpha, int64_t bk, int64_t gk,
+                             int32_t* out, int64_t* n_out) {
+  if (!scores || !out || !n_out || L < 0 || bk < 1 || gk < 1) return ORA_ERR_ARG;
+  std::vector<double> sc(scores, scores + L);
+  std::vector<int64_t> kept = mins_progressive(sc, alpha, bk, gk);
+  for (size_t t = 0; t < kept.size(); ++t) out[t] = static_cast<int32_t>(kept[t]);
+  *n_out = static_cast<int64_t>(kept.size());
+  return ORA_OK;
+}
+
+// Eq. 4 (materialised softmax) for every query row of the listed blocks (all
+// blocks when blocks == NULL).  Query row r of block i sees the keys of
+// Idx(i) = idx[w*cap .. w*cap + counts[w]) that are <= r when causal.
+// o is [B, Hq, N, D] doubles, lse is [B, Hq, N] (may be NULL).
+int ora_sparse_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t B, int64_t Hq,
+                    int64_t Hkv, int64_t N, int64_t D, int32_t block, int32_t causal, double scale,
+                    const int32_t* idx, int64_t cap, const int32_t* counts, double* o, double* lse,
+                    const int64_t* blocks, int64_t n_blocks, int32_t nthreads) {
+  Shape s{B, Hq, Hkv, N, D};
+  if (!q || !k || !v || !idx || !counts || !o || block < 1 || cap < 0 || !shape_ok(s))
+    return ORA_ERR_ARG;
+  if (scale == 0.0) scale = 1.0 / std::sqrt(static_cast<double>(D));
+  const int64_t Np = num_blocks(N, block);
+  const int64_t total = blocks ? n_blocks : B * Hq * Np;
+  int bad = 0;
+  set_threads(nthreads);
+#pragma omp parallel for schedule(dynamic) reduction(| : bad)
+  for (int64_t t = 0; t < total; ++t) {
+    const int64_t w = blocks ? blocks[t] : t;
+    const int64_t i = w % Np, h = (w / Np) % Hq, b = w / (Np * Hq);
+    const int32_t c = counts[w];
+    if (c < 0 || c > cap) {
+      bad = 1;
+      continue;
+    }
+    const int32_t* list = idx + w * cap;
+    const int64_t r0 = i * block, r1 = std::min<int64_t>(N, r0 + block);
+    std::vector<int64_t> keys;
+    for (int64_t r = r0; r < r1; ++r) {
+      keys.clear();
+      for (int32_t t2 = 0; t2 < c; ++t2) {
+        const int64_t j = list[t2];
+        if (j < 0 || j >= N) {
+          bad = 1;
+          continue;
+        }
+        if (!causal || j <= r) keys.push_back(j);
+      }
+      double lse_r;
+      attend_row(q, k, v, s, b, h, r, keys, scale, o + row_off(b, h, r, Hq, N, D), &lse_r);
+      if (lse) lse[(b * Hq + h) * N + r] = lse_r;
+    }
+  }
+  return bad ? ORA_ERR_ARG : ORA_OK;
+}
+
+// Eq. 1, textbook dense attention (causal: row r sees keys 0..r).  Written
+// without any index list so that it can pin Eq. 4 at 100% keep.
+int ora_dense_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t B, int64_t Hq,
+                   int64_t Hkv, int64_t N, int64_t D, int32_t causal, double scale, double* o,
+                   double* lse, int32_t nthreads) {
+  Shape s{B, Hq, Hkv, N, D};
+  if (!q || !k || !v || !o || !shape_ok(s)) return ORA_ERR_ARG;
+  if (scale == 0.0) scale = 1.0 / std::sqrt(static_cast<double>(D));
+  const int64_t g = Hq / Hkv;
+  set_threads(nthreads);
+#pragma omp parallel for schedule(dynamic)
+  for (int64_t w = 0; w < B * Hq * N; ++w) {
+    const int64_t r = w % N, h = (w / N) % Hq, b = w / (N * Hq);
+    const int64_t hk = h / g;
+    const int64_t nk = causal ? r + 1 : N;
+    const uint16_t* qr = q + row_off(b, h, r, Hq, N, D);
+    std::vector<double> srow(nk);
+    double m = -std::numeric_limits<double>::infinity();
+    for (int64_t j = 0; j < nk; ++j) {
+      const uint16_t* kr = k + row_off(b, hk, j, Hkv, N, D);
+      double dot = 0.0;
+      for (int64_t d = 0; d < D; ++d) dot += bf16_value(qr[d]) * bf16_value(kr[d]);
+      srow[j] = scale * dot;
+      m = std::max(m, srow[j]);
+    }
+    double Z = 0.0;
+    for (int64_t j = 0; j < nk; ++j) Z += std::exp(srow[j] - m);
+    double* orow = o + row_off(b, h, r, Hq, N, D);
+    for (int64_t d = 0; d < D; ++d) {
+      double acc = 0.0;
+      for (int64_t j = 0; j < nk; ++j)
+        acc += std::exp(srow[j] - m) / Z * bf16_value(v[row_off(b, hk, j, Hkv, N, D) + d]);
+      orow[d] = acc;
+    }
+    if (lse) lse[w] = m + std::log(Z);
+  }
+  return ORA_OK;
+}
+
+// Algorithm 2 (Vector-Sparse Computation) for the listed blocks: the index list
+// of each block is consumed bk entries at a time; each tile is masked (causal:
+// key <= row; entries past counts[w]: excluded), and the running max m, running
+// normaliser l and accumulator O follow the online-softmax recurrence; the
+// output is O / l.  A row that has seen no visible key keeps m = -inf and ends
+// with O = 0, LSE = -inf instead of dividing by zero.
+int ora_sparse_attn_online(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t B,
+                           int64_t Hq, int64_t Hkv, int64_t N, int64_t D, int32_t block,
+                           int32_t causal, double scale, const int32_t* idx, int64_t cap,
+                           const int32_t* counts, int32_t bk, double* o, double* lse,
+                           int32_t nthreads) {
+  Shape s{B, Hq, Hkv, N, D};
+  if (!q || !k || !v || !idx || !counts || !o || block < 1 || bk < 1 || !shape_ok(s))
+    return ORA_ERR_ARG;
+  if (scale == 0.0) scale = 1.0 / std::sqrt(static_cast<double>(D));
+  const double NEG_INF = -std::numeric_limits<double>::infinity();
+  const int64_t Np = num_blocks(N, block);
+  const int64_t g = Hq / Hkv;
+  set_threads(nthreads);
+#pragma omp parallel for schedule(dynamic)
+  for (int64_t w = 0; w < B * Hq * Np; ++w) {
+    const int64_t i = w % Np, h = (w / Np) % Hq, b = w / (Np * Hq);
+    const int64_t hk = h / g;
+    const int32_t* list = idx + w * cap;
+    const int32_t c = counts[w];
+    const int64_t r0 = i * block, r1 = std::min<int64_t>(N, r0 + block);
+    for (int64_t r = r0; r < r1; ++r) {
+      const uint16_t* qr = q + row_off(b, h, r, Hq, N, D);
+      double m = NEG_INF, l = 0.0;
+      std::vector<double> acc(D, 0.0);
+      for (int32_t j0 = 0; j0 < c; j0 += bk) {
+        std::vector<double> st(bk, NEG_INF);
+        for (int32_t t = 0; t < bk; ++t) {
+          if (j0 + t >= c) continue;
+          const int64_t j = list[j0 + t];
+          if (causal && j > r) continue;
+          const uint16_t* kr = k + row_off(b, hk, j, Hkv, N, D);
+          double dot = 0.0;
+          for (int64_t d = 0; d < D; ++d) dot += bf16_value(qr[d]) * bf16_value(kr[d]);
+          st[t] = scale * dot;
+        }
+        double m_new = m;
+        for (int32_t t = 0; t < bk; ++t) m_new = std::max(m_new, st[t]);
+        if (m_new == NEG_INF) continue;  // nothing visible yet
+        const double alpha = (m == NEG_INF) ? 0.0 : std::exp(m - m_new);
+        double l_new = 0.0;
+        for (int64_t d = 0; d < D; ++d) acc[d] *= alpha;
+        for (int32_t t = 0; t < bk; ++t) {
+          if (st[t] == NEG_INF) continue;
+          const double p = std::exp(st[t] - m_new);
+          l_new += p;
+          const uint16_t* vr = v + row_off(b, hk, list[j0 + t], Hkv, N, D);
+          for (int64_t d = 0; d < D; ++d) acc[d] += p * bf16_value(vr[d]);
+        }
+        l = alpha * l + l_new;
+        m = m_new;
+      }
+      double* orow = o + row_off(b, h, r, Hq, N, D);
+      for (int64_t d = 0; d < D; ++d) orow[d] = (l > 0.0) ? acc[d] / l : 0.0;
+      if (lse) lse[(b * Hq + h) * N + r] = (l > 0.0) ? m + std::log(l) : NEG_INF;
+    }
+  }
+  return ORA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,376 @@
+"""Pins of the CPU oracle against facts fixed by the paper's definitions and by
+mathematics: brute force on tiny inputs, library routines, closed forms and
+invariants.  None of these re-types the oracle's own arithmetic.
+
+Passages: Eq. 1 and Eq. 2, the estimated map and topK/topP of Sec. 3.1,
+Eq. 3 (minS) and Algorithm 1's per-group running max, Eq. 4 and Algorithm 2.
+"""
+import itertools
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2603_29494_amd import synth
+
+
+def _bf16_nearest_by_search(x: float) -> int:
+    """Nearest bf16 to x by searching neighbouring bit patterns (ties: even)."""
+    if x == 0.0:
+        return 0x8000 if math.copysign(1.0, x) < 0 else 0
+    f32 = np.array([x], dtype=np.float32)
+    base = int(f32.view(np.uint32)[0] >> 16)
+    best = None
+    for cand in range(base - 3, base + 4):
+        if not 0 <= cand <= 0xFFFF:
+            continue
+        val = float(oracle.bf16_to_f64(np.array([cand], dtype=np.uint16))[0])
+        if not math.isfinite(val):
+            continue
+        err = abs(val - x)
+        key = (err, cand & 1)
+        if best is None or key < best[0]:
+            best = (key, cand)
+    return best[1]
+
+
+def test_bf16_round_is_nearest_even():
+    r = np.random.Generator(np.random.PCG64(1))
+    xs = list(r.standard_normal(400) * 10.0 ** r.uniform(-40, 30, 400))
+    # exact midpoints between neighbouring bf16 values, both parities
+    for bits in (0x3F80, 0x3F81, 0x4049, 0x404A, 0xC123, 0x0001, 0x0080, 0x7F7E):
+        lo = float(oracle.bf16_to_f64(np.array([bits], dtype=np.uint16))[0])
+        hi = float(oracle.bf16_to_f64(np.array([bits + 1], dtype=np.uint16))[0])
+        xs += [(lo + hi) / 2, lo + (hi - lo) * 0.4999, lo + (hi - lo) * 0.5001]
+    xs += [1e-45, -3e-41, 2.0 ** -133, 1.5 * 2.0 ** -133]
+    got = oracle.bf16_round(np.array(xs))
+    for x, g in zip(xs, got):
+        assert int(g) == _bf16_nearest_by_search(x), (x, hex(int(g)))
+
+
+def test_bf16_round_agrees_with_torch_on_fp32_values():
+    # torch rounds fp32 -> bf16 to nearest even; on fp32 inputs one rounding step
+    # is the same as ours.
+    r = np.random.Generator(np.random.PCG64(2))
+    x = (r.standard_normal(20000) * 3).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(oracle.bf16_round(x.astype(np.float64)), ref)
+
+
+@pytest.mark.parametrize("N,P", [(64, 16), (70, 16), (5, 1), (33, 64), (130, 128)])
+def test_pool_is_rounded_block_mean(N, P):
+    q = synth.random_bits(10 + N, (1, 2, N, 8))
+    qp = oracle.pool(q, P)
+    qf = oracle.bf16_to_f64(q)
+    Np = (N + P - 1) // P
+    assert qp.shape == (1, 2, Np, 8)
+    for i in range(Np):
+        mean = qf[:, :, i * P:min(N, (i + 1) * P), :].mean(axis=2)   # numpy mean (library)
+        expect = np.array([_bf16_nearest_by_search(float(m)) for m in mean.ravel()], dtype=np.uint16)
+        assert np.array_equal(qp[:, :, i, :].ravel(), expect)
+
+
+def test_pool_special_cases():
+    q = synth.random_bits(3, (1, 1, 40, 16))
+    assert np.array_equal(oracle.pool(q, 1), q)                      # P = 1: Q_p = Q
+    same = np.repeat(q[:, :, :1, :], 40, axis=2)
+    assert np.array_equal(oracle.pool(same, 16)[0, 0], np.repeat(q[0, 0, :1], 3, axis=0))
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_scores_match_numpy(causal):
+    q = synth.random_bits(4, (1, 4, 100, 32))
+    k = synth.random_bits(5, (1, 2, 100, 32))
+    P = 16
+    qp = oracle.bf16_to_f64(oracle.pool(q, P))
+    kf = oracle.bf16_to_f64(k)
+    for h in range(4):
+        for i in range(7):
+            s = oracle.pooled_scores(q, k, P, causal, 0, h, i)
+            L = min(100, (i + 1) * P) if causal else 100
+            ref = (kf[0, h // 2, :L] @ qp[0, h, i]) / math.sqrt(32)    # numpy matmul
+            assert s.shape == (L,)
+            np.testing.assert_allclose(s, ref, rtol=1e-12, atol=1e-14)
+
+
+def test_topk_count_values():
+    assert oracle.topk_count(0.15, 75600) == 11340
+    assert oracle.topk_count(0.125, 1024) == 128
+    assert oracle.topk_count(0.10, 64) == 7
+    assert oracle.topk_count(0.10, 32768) == 3277
+    assert oracle.topk_count(0.1, 640) == 64
+    assert 0.07 * 100 > 7.0 and oracle.topk_count(0.07, 100) == 7   # rounding guard
+    assert oracle.topk_count(1e-9, 50) == 1
+    assert oracle.topk_count(1.0, 50) == 50
+
+
+def _tiny_layer(seed, N, D=16, dup=False):
+    q = synth.random_bits(seed, (1, 1, N, D))
+    k = synth.random_bits(seed + 1, (1, 1, N, D))
+    if dup:  # identical key rows create exact score ties
+        k[0, 0, 5] = k[0, 0, 2]
+        k[0, 0, 9] = k[0, 0, 2]
+        k[0, 0, 11] = k[0, 0, 7]
+    return q, k
+
+
+def _brute_topk(s, kk):
+    best = None
+    for sub in itertools.combinations(range(len(s)), kk):
+        key = (-sum(s[j] for j in sub), sub)     # max sum, then lexicographically smallest
+        if best is None or key < best:
+            best = key
+    return list(best[1])
+
+
+@pytest.mark.parametrize("seed,N,ratio,dup", [(11, 12, 0.25, False), (12, 12, 0.5, True),
+                                              (13, 14, 0.3, True), (14, 9, 0.6, False)])
+def test_topk_matches_brute_force(seed, N, ratio, dup):
+    q, k = _tiny_layer(seed, N, dup=dup)
+    idx, cnt, _ = oracle.select(q, k, N, oracle.TOPK, ratio, False, N)
+    s = oracle.pooled_scores(q, k, N, False, 0, 0, 0)
+    kk = oracle.topk_count(ratio, N)
+    assert cnt[0, 0, 0] == kk
+    assert list(idx[0, 0, 0, :kk]) == _brute_topk(list(s), kk)
+    assert np.all(idx[0, 0, 0, kk:] == -1)
+
+
+def test_topk_invariants_and_scale():
+    q, k = _tiny_layer(21, 200, D=32)
+    P = 50
+    idx, cnt, _ = oracle.select(q, k, P, oracle.TOPK, 0.2, True, 200)
+    for i in range(4):
+        s = oracle.pooled_scores(q, k, P, True, 0, 0, i)
+        L = len(s)
+        c = cnt[0, 0, i]
+        assert c == oracle.topk_count(0.2, L)
+        sel = idx[0, 0, i, :c]
+        assert np.all(np.diff(sel) > 0) and sel.min() >= 0 and sel.max() < L
+        rest = np.setdiff1d(np.arange(L), sel)
+        assert s[sel].min() >= s[rest].max()
+    k2 = oracle.bf16_round(oracle.bf16_to_f64(k) * 2.0)    # exact rescale of every score
+    idx2, cnt2, _ = oracle.select(q, k2, P, oracle.TOPK, 0.2, True, 200)
+    assert np.array_equal(idx, idx2) and np.array_equal(cnt, cnt2)
+    idx3, cnt3, _ = oracle.select(q, k, P, oracle.TOPK, 1.0, True, 200)
+    for i in range(4):
+        L = min(200, (i + 1) * P)
+        assert list(idx3[0, 0, i, :cnt3[0, 0, i]]) == list(range(L))
+
+
+def _brute_topp(s, p):
+    s = np.asarray(s)
+    e = np.exp(s - s.max())
+    Z = e.sum()
+    best = None
+    for n in range(1, len(s) + 1):
+        for sub in itertools.combinations(range(len(s)), n):
+            m = e[list(sub)].sum() / Z
+            if m >= p:
+                key = (n, -m, sub)
+                if best is None or key < best:
+                    best = key
+        if best is not None:
+            return list(best[2])
+    return list(range(len(s)))
+
+
+@pytest.mark.parametrize("seed,N,p", [(31, 10, 0.5), (32, 12, 0.8), (33, 11, 0.95), (34, 12, 0.3)])
+def test_topp_matches_brute_force(seed, N, p):
+    q, k = _tiny_layer(seed, N, D=16)
+    k = oracle.bf16_round(oracle.bf16_to_f64(k) * 3.0)   # spread the scores
+    idx, cnt, _ = oracle.select(q, k, N, oracle.TOPP, p, False, N)
+    s = oracle.pooled_scores(q, k, N, False, 0, 0, 0)
+    assert list(idx[0, 0, 0, :cnt[0, 0, 0]]) == sorted(_brute_topp(s, p))
+
+
+@pytest.mark.parametrize("L,p", [(100, 0.333), (640, 0.9512), (77, 0.5)])
+def test_topp_uniform_scores(L, p):
+    # Q = 0 makes every score 0: the mass is uniform and topP keeps ceil(p L)
+    # keys, the lowest indices first.
+    q = np.zeros((1, 1, L, 16), dtype=np.uint16)
+    k = synth.random_bits(41, (1, 1, L, 16))
+    idx, cnt, _ = oracle.select(q, k, L, oracle.TOPP, p, False, L)
+    t = math.ceil(p * L)
+    assert abs(p * L - round(p * L)) > 1e-6
+    assert cnt[0, 0, 0] == t and list(idx[0, 0, 0, :t]) == list(range(t))
+
+
+def test_topp_mass_reaching_p_exactly_stops():
+    # uniform scores, p * L an integer: the cumulative mass equals p exactly
+    # after p * L keys, and "reaches p" means >= p, so no further key is taken
+    L, p = 100, 0.25
+    q = np.zeros((1, 1, L, 16), dtype=np.uint16)
+    k = synth.random_bits(42, (1, 1, L, 16))
+    idx, cnt, _ = oracle.select(q, k, L, oracle.TOPP, p, False, L)
+    assert cnt[0, 0, 0] == 25 and list(idx[0, 0, 0, :25]) == list(range(25))
+
+
+def test_topp_mass_invariants():
+    q, k = _tiny_layer(51, 300, D=32)
+    k = oracle.bf16_round(oracle.bf16_to_f64(k) * 4.0)
+    for p in (0.5, 0.9, 0.99):
+        idx, cnt, _ = oracle.select(q, k, 100, oracle.TOPP, p, False, 300)
+        for i in range(3):
+            s = oracle.pooled_scores(q, k, 100, False, 0, 0, i)
+            e = np.exp(s - s.max())
+            sel = idx[0, 0, i, :cnt[0, 0, i]]
+            mass = e[sel].sum() / e.sum()
+            assert mass >= p - 1e-12
+            weakest = sel[np.argmin(s[sel])]
+            assert (e[sel].sum() - e[weakest]) / e.sum() < p
+            rest = np.setdiff1d(np.arange(300), sel)
+            assert s[sel].min() >= s[rest].max()
+
+
+def test_threshold_cap_keeps_best():
+    q, k = _tiny_layer(52, 256, D=32)
+    idx, cnt, ncl = oracle.select(q, k, 64, oracle.TOPP, 0.99, False, 20)
+    assert ncl == 4 and np.all(cnt == 20)
+    for i in range(4):
+        s = oracle.pooled_scores(q, k, 64, False, 0, 0, i)
+        top = np.argsort(-s, kind="stable")[:20]
+        assert set(idx[0, 0, i]) == set(top)
+    with pytest.raises(ValueError):
+        oracle.select(q, k, 64, oracle.TOPK, 0.5, False, 20)
+
+
+def test_mins_special_cases():
+    r = np.random.Generator(np.random.PCG64(61))
+    s = r.standard_normal(1000)
+    s[[17, 400]] = s.max() + 1.0
+    q, k = _tiny_layer(62, 64)
+    assert list(oracle.mins_progressive(s, 0.0, 1000, 1)) == [17, 400]     # alpha = 0: argmax ties
+    assert list(oracle.mins_progressive(s, np.inf, 16, 16)) == list(range(1000))
+    for alpha in (0.1, 0.5, 2.0):
+        glob = set(np.nonzero(s >= s.max() - alpha)[0])
+        prog = set(oracle.mins_progressive(s, alpha, 16, 16))
+        assert glob <= prog            # a running max never exceeds the global max
+    # when each group's max sits in its first tile the running max is the group max
+    s2 = r.standard_normal(512)
+    for g0 in range(0, 512, 64):
+        s2[g0] = s2[g0:g0 + 64].max() + 0.5
+    prog = oracle.mins_progressive(s2, 0.7, 16, 4)
+    expect = [j for j in range(512) if s2[j] >= s2[(j // 64) * 64:(j // 64) * 64 + 64].max() - 0.7]
+    assert list(prog) == expect
+    # global minS through select(): alpha = 0 keeps the argmax
+    idx, cnt, _ = oracle.select(q, k, 64, oracle.MINS, 0.0, False, 64)
+    sc = oracle.pooled_scores(q, k, 64, False, 0, 0, 0)
+    assert list(idx[0, 0, 0, :cnt[0, 0, 0]]) == [int(np.argmax(sc))]
+
+
+def _all_keys(N, P, causal, Np, B=1, H=1):
+    cap = N
+    idx = np.full((B, H, Np, cap), -1, dtype=np.int32)
+    cnt = np.zeros((B, H, Np), dtype=np.int32)
+    for i in range(Np):
+        L = min(N, (i + 1) * P) if causal else N
+        idx[:, :, i, :L] = np.arange(L)
+        cnt[:, :, i] = L
+    return idx, cnt
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_full_keep_equals_dense_and_sdpa(causal):
+    B, Hq, Hkv, N, D, P = 1, 4, 2, 70, 16, 16
+    q = synth.random_bits(71, (B, Hq, N, D))
+    k = synth.random_bits(72, (B, Hkv, N, D))
+    v = synth.random_bits(73, (B, Hkv, N, D))
+    Np = (N + P - 1) // P
+    idx, cnt = _all_keys(N, P, causal, Np, B, Hq)
+    o, lse = oracle.sparse_attn(q, k, v, idx, cnt, P, causal)
+    od, lsed = oracle.dense_attn(q, k, v, causal)
+    np.testing.assert_allclose(o, od, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse, lsed, rtol=0, atol=1e-12)
+    tq, tk, tv = (torch.from_numpy(oracle.bf16_to_f64(x)) for x in (q, k, v))
+    ref = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, is_causal=causal,
+                                                           enable_gqa=True)
+    np.testing.assert_allclose(o, ref.numpy(), rtol=0, atol=1e-12)
+
+
+def test_single_key_and_zero_query():
+    B, H, N, D, P = 1, 1, 48, 16, 16
+    q = synth.random_bits(81, (B, H, N, D))
+    k = synth.random_bits(82, (B, H, N, D))
+    v = synth.random_bits(83, (B, H, N, D))
+    idx = np.full((1, 1, 3, 4), -1, dtype=np.int32)
+    cnt = np.array([[[1, 1, 1]]], dtype=np.int32)
+    idx[0, 0, :, 0] = [5, 30, 40]
+    o, _ = oracle.sparse_attn(q, k, v, idx, cnt, P, False)
+    vf = oracle.bf16_to_f64(v)
+    for i, j in enumerate([5, 30, 40]):
+        assert np.array_equal(o[0, 0, i * P:(i + 1) * P], np.repeat(vf[0, 0, j:j + 1], P, 0))
+    z = np.zeros_like(q)
+    idx2 = np.array([[[[1, 4, 9, 20]] * 3]], dtype=np.int32).reshape(1, 1, 3, 4)
+    cnt2 = np.full((1, 1, 3), 4, dtype=np.int32)
+    o2, _ = oracle.sparse_attn(z, k, v, idx2, cnt2, P, False)
+    np.testing.assert_allclose(o2[0, 0], np.repeat(vf[0, 0, [1, 4, 9, 20]].mean(0)[None], N, 0),
+                               rtol=0, atol=1e-14)
+
+
+def test_empty_causal_rows():
+    B, H, N, D, P = 1, 1, 32, 16, 16
+    q, k, v = (synth.random_bits(s, (B, H, N, D)) for s in (91, 92, 93))
+    idx = np.array([[[[10, 12, -1], [3, 20, 31]]]], dtype=np.int32)
+    cnt = np.array([[[2, 3]]], dtype=np.int32)
+    o, lse = oracle.sparse_attn(q, k, v, idx, cnt, P, True)
+    assert np.all(o[0, 0, :10] == 0) and np.all(np.isneginf(lse[0, 0, :10]))
+    assert np.all(np.isfinite(lse[0, 0, 10:]))
+    oo, lo = oracle.sparse_attn_online(q, k, v, idx, cnt, P, True, 2)
+    np.testing.assert_array_equal(oo[0, 0, :10], 0.0)
+    assert np.all(np.isneginf(lo[0, 0, :10]))
+
+
+@pytest.mark.parametrize("bk", [1, 3, 16, 64])
+@pytest.mark.parametrize("causal", [False, True])
+def test_online_recurrence_equals_materialised(bk, causal):
+    B, Hq, Hkv, N, D, P = 1, 2, 1, 150, 16, 32
+    q, k, v = (synth.random_bits(s, (B, h, N, D)) for s, h in ((101, Hq), (102, Hkv), (103, Hkv)))
+    r = np.random.Generator(np.random.PCG64(104))
+    Np = (N + P - 1) // P
+    cap = 90
+    idx = np.full((B, Hq, Np, cap), -1, dtype=np.int32)
+    cnt = np.zeros((B, Hq, Np), dtype=np.int32)
+    for h in range(Hq):
+        for i in range(Np):
+            c = int(r.integers(0, cap + 1))
+            idx[0, h, i, :c] = np.sort(r.choice(N, size=c, replace=False))
+            cnt[0, h, i] = c
+    o, lse = oracle.sparse_attn(q, k, v, idx, cnt, P, causal)
+    o2, lse2 = oracle.sparse_attn_online(q, k, v, idx, cnt, P, causal, bk)
+    np.testing.assert_allclose(o2, o, rtol=0, atol=1e-12)
+    fin = np.isfinite(lse)
+    assert np.array_equal(fin, np.isfinite(lse2))
+    np.testing.assert_allclose(lse2[fin], lse[fin], rtol=0, atol=1e-12)
+
+
+def test_gqa_equals_replicated_kv():
+    B, Hq, Hkv, N, D, P = 1, 6, 2, 64, 16, 16
+    q = synth.random_bits(111, (B, Hq, N, D))
+    k = synth.random_bits(112, (B, Hkv, N, D))
+    v = synth.random_bits(113, (B, Hkv, N, D))
+    kr, vr = np.repeat(k, 3, axis=1), np.repeat(v, 3, axis=1)   # contiguous grouping
+    for mode, par in ((oracle.TOPK, 0.3), (oracle.TOPP, 0.7)):
+        a = oracle.select(q, k, P, mode, par, True, N)
+        b = oracle.select(q, kr, P, mode, par, True, N)
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    idx, cnt, _ = oracle.select(q, k, P, oracle.TOPK, 0.3, False, N)
+    o1, _ = oracle.sparse_attn(q, k, v, idx, cnt, P, False)
+    o2, _ = oracle.sparse_attn(q, kr, vr, idx, cnt, P, False)
+    np.testing.assert_array_equal(o1, o2)
+
+
+def test_plumbing_workload_recovers_planted_columns():
+    layer = synth.make_layer(1)
+    w = layer.w
+    idx, cnt, _ = oracle.select(layer.q, layer.k, w.block, oracle.TOPK, w.param, w.causal, 128)
+    assert np.all(cnt == 128)
+    recall = []
+    for h in range(w.Hq):
+        planted = set(layer.planted[h].tolist())
+        for i in range(w.num_blocks):
+            recall.append(len(planted & set(idx[0, h, i].tolist())) / len(planted))
+    # the planted boost is 0.5 logit against a score spread of ~0.2, so most
+    # (not all) planted columns land in every block's top 12.5%
+    assert np.mean(recall) > 0.85

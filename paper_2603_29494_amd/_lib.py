@@ -1,0 +1,192 @@
+"""ctypes binding of libvecattn.so (include/vecattn.h).
+
+Argument marshalling only: torch tensors become device pointers, tensor
+descriptors and the current HIP stream; every step of the computation runs in
+the library's HIP kernels.  There is no fallback: if the library is missing or
+cannot be loaded, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libvecattn.so")
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_CAPACITY, ERR_DEVICE = range(5)
+SEL_TOPK, SEL_TOPP, SEL_MINS = 0, 1, 2
+_MODES = {"topk": SEL_TOPK, "topp": SEL_TOPP, "mins": SEL_MINS}
+
+
+class VecattnError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} (status {status})")
+
+
+class TDesc(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int64), ("H", ctypes.c_int64), ("N", ctypes.c_int64),
+                ("D", ctypes.c_int64), ("sB", ctypes.c_int64), ("sH", ctypes.c_int64),
+                ("sN", ctypes.c_int64)]
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libvecattn.so from the package directory (raises if not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                          "(or python paper_2603_29494_amd/build.py) first")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, i32, i64, f64, f32 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double,
+                            ctypes.c_float)
+    D = ctypes.POINTER(TDesc)
+    lib.vecattn_version.restype = i32
+    lib.vecattn_status_string.argtypes = [ctypes.c_int]
+    lib.vecattn_status_string.restype = ctypes.c_char_p
+    lib.vecattn_pool.argtypes = [P, D, i32, P, D, P]
+    lib.vecattn_select_max_count.argtypes = [i64, i32, i32, i32, f64, ctypes.POINTER(i64)]
+    lib.vecattn_select_workspace_size.argtypes = [D, D, i32, i32, i32, i64,
+                                                  ctypes.POINTER(ctypes.c_size_t)]
+    lib.vecattn_select.argtypes = [P, D, P, D, i32, i32, i32, f64, P, i64, P, P, P,
+                                   ctypes.c_size_t, P]
+    lib.vecattn_sparse_attn.argtypes = [P, D, P, D, P, D, P, i64, P, i32, i32, f32, P, D, P, P]
+    for name in ("vecattn_pool", "vecattn_select_max_count", "vecattn_select_workspace_size",
+                 "vecattn_select", "vecattn_sparse_attn"):
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    try:
+        return load().vecattn_status_string(int(status)).decode()
+    except ImportError:
+        return "unknown"
+
+
+def _check(status: int, what: str):
+    if status != OK:
+        raise VecattnError(status, what)
+
+
+def desc(t: torch.Tensor) -> TDesc:
+    if t.dim() != 4:
+        raise ValueError("expected a [B, H, N, D] tensor")
+    B, H, N, Dd = t.shape
+    sB, sH, sN, sD = t.stride()
+    if sD != 1:
+        raise ValueError("the D dimension must be contiguous")
+    return TDesc(B, H, N, Dd, sB, sH, sN)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(t: torch.Tensor):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _bf16_cuda(t: torch.Tensor, name: str):
+    if not t.is_cuda or t.dtype != torch.bfloat16:
+        raise TypeError(f"{name} must be a bfloat16 CUDA tensor")
+
+
+def mode_id(mode) -> int:
+    return _MODES[mode] if isinstance(mode, str) else int(mode)
+
+
+def max_count(N: int, block: int, causal: bool, mode, param: float) -> int:
+    out = ctypes.c_int64(0)
+    _check(load().vecattn_select_max_count(int(N), int(block), int(bool(causal)), mode_id(mode),
+                                           float(param), ctypes.byref(out)), "select_max_count")
+    return int(out.value)
+
+
+def pool(q: torch.Tensor, block: int, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Pooled queries, Eq. 2: bf16 [B, H, ceil(N/block), D]."""
+    _bf16_cuda(q, "q")
+    B, H, N, Dd = q.shape
+    Np = (N + block - 1) // block
+    if out is None:
+        out = torch.empty((B, H, Np, Dd), dtype=torch.bfloat16, device=q.device)
+    qd, od = desc(q), desc(out)
+    _check(load().vecattn_pool(_ptr(q), ctypes.byref(qd), int(block), _ptr(out), ctypes.byref(od),
+                               _stream(q)), "pool")
+    return out
+
+
+def workspace_bytes(q: torch.Tensor, k: torch.Tensor, block: int, causal: bool, mode,
+                    cap: int) -> int:
+    n = ctypes.c_size_t(0)
+    qd, kd = desc(q), desc(k)
+    _check(load().vecattn_select_workspace_size(ctypes.byref(qd), ctypes.byref(kd), int(block),
+                                                int(bool(causal)), mode_id(mode), int(cap),
+                                                ctypes.byref(n)), "select_workspace_size")
+    return int(n.value)
+
+
+def select(q: torch.Tensor, k: torch.Tensor, block: int, mode, param: float,
+           causal: bool = False, cap: Optional[int] = None,
+           idx: Optional[torch.Tensor] = None, counts: Optional[torch.Tensor] = None,
+           workspace: Optional[torch.Tensor] = None,
+           n_clamped: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Per-block key-index lists (I, C) of Algorithm 1 for topK / topP selection."""
+    _bf16_cuda(q, "q")
+    _bf16_cuda(k, "k")
+    B, Hq, N, Dd = q.shape
+    Np = (N + block - 1) // block
+    if cap is None:
+        cap = max_count(N, block, causal, mode, param)
+    dev = q.device
+    if idx is None:
+        idx = torch.empty((B, Hq, Np, cap), dtype=torch.int32, device=dev)
+    if counts is None:
+        counts = torch.empty((B, Hq, Np), dtype=torch.int32, device=dev)
+    if idx.shape != (B, Hq, Np, cap) or not idx.is_contiguous() or idx.dtype != torch.int32:
+        raise ValueError("idx must be contiguous int32 [B, Hq, N_p, cap]")
+    if counts.shape != (B, Hq, Np) or not counts.is_contiguous() or counts.dtype != torch.int32:
+        raise ValueError("counts must be contiguous int32 [B, Hq, N_p]")
+    need = workspace_bytes(q, k, block, causal, mode, cap)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    qd, kd = desc(q), desc(k)
+    _check(load().vecattn_select(_ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd), int(block),
+                                 int(bool(causal)), mode_id(mode), float(param), _ptr(idx),
+                                 int(cap), _ptr(counts), _ptr(n_clamped), _ptr(workspace),
+                                 0 if workspace is None else workspace.numel(), _stream(q)),
+           "select")
+    return idx, counts
+
+
+def sparse_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: torch.Tensor,
+                counts: torch.Tensor, block: int, causal: bool = False, scale: float = 0.0,
+                out: Optional[torch.Tensor] = None, return_lse: bool = False):
+    """Vector-sparse attention, Eq. 4: O (bf16, like q) and optionally LSE (fp32 [B,Hq,N])."""
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _bf16_cuda(t, n)
+    if idx.dtype != torch.int32 or counts.dtype != torch.int32 or not idx.is_contiguous() \
+            or not counts.is_contiguous():
+        raise ValueError("idx and counts must be contiguous int32")
+    B, Hq, N, Dd = q.shape
+    Np = (N + block - 1) // block
+    if idx.dim() != 4 or tuple(idx.shape[:3]) != (B, Hq, Np) or tuple(counts.shape) != (B, Hq, Np):
+        raise ValueError("idx must be [B, Hq, N_p, cap] and counts [B, Hq, N_p]")
+    if out is None:
+        out = torch.empty_like(q, memory_format=torch.contiguous_format)
+    lse = torch.empty((B, Hq, N), dtype=torch.float32, device=q.device) if return_lse else None
+    qd, kd, vd, od = desc(q), desc(k), desc(v), desc(out)
+    _check(load().vecattn_sparse_attn(_ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd), _ptr(v),
+                                      ctypes.byref(vd), _ptr(idx), int(idx.shape[-1]),
+                                      _ptr(counts), int(block), int(bool(causal)), float(scale),
+                                      _ptr(out), ctypes.byref(od), _ptr(lse), _stream(q)),
+           "sparse_attn")
+    return (out, lse) if return_lse else out

@@ -1,0 +1,53 @@
+// Internal launch interface between the C ABI (vecattn_api.cpp) and the HIP
+// kernels.  Arguments are already validated by the caller.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace vecattn {
+
+struct Tensor4 {
+  const void* ptr;
+  int64_t B, H, N, D;
+  int64_t sB, sH, sN;
+};
+
+hipError_t launch_pool(const Tensor4& q, int32_t block, void* qp, int64_t qp_sB, int64_t qp_sH,
+                       int64_t qp_sN, hipStream_t stream);
+
+struct SparseAttnArgs {
+  Tensor4 q, k, v;
+  void* o;
+  int64_t o_sB, o_sH, o_sN;
+  float* lse;
+  const int32_t* idx;
+  const int32_t* counts;
+  int64_t cap;
+  int32_t block;
+  int32_t causal;
+  float scale;
+};
+
+hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream);
+
+struct SelectArgs {
+  Tensor4 q, k;
+  int32_t block;
+  int32_t causal;
+  int32_t mode;
+  double param;
+  int32_t* idx;
+  int64_t cap;
+  int32_t* counts;
+  int32_t* n_clamped;
+  void* workspace;
+  size_t workspace_bytes;
+};
+
+size_t select_workspace_bytes(int64_t B, int64_t Hq, int64_t N, int64_t D, int32_t block,
+                              int32_t mode, int64_t cap);
+hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
+
+}  // namespace vecattn

@@ -1,0 +1,865 @@
+// Important-vector selection (paper Sec. 3.1; the outputs I and C of
+// Algorithm 1) for gfx950: row-wise topK (a budget) and topP (a cumulative
+// softmax-mass threshold) over the estimated map Q_p K^T / sqrt(D), without
+// ever writing that map to memory (the TilingSelect principle, Sec. 3.1.3).
+//
+// Exact selection needs the score of the k-th key (topK) or of the key where
+// the mass reaches p (topP).  Every row therefore narrows a score interval
+// that must contain its cut, one pass over the keys at a time:
+//   HIST     score tiles stay on chip; each key of the row is classified
+//            against the interval (above / inside / below); keys inside land
+//            in a 256-bin LDS histogram, keys above are counted (and their
+//            softmax mass summed for topP).  A resolve kernel picks the bin
+//            range that must hold the cut, which becomes the next interval.
+//   COLLECT  once the interval holds at most kCand keys, their (score, index)
+//            pairs are gathered; a resolve kernel sorts them and fixes the cut
+//            score t* and how many keys tied at t* are kept (lowest indices).
+//   EMIT     one more pass sets a bit per kept key (score > t*), and one per
+//            key tied at t* when only some ties are kept.
+//   COMPACT  bitmasks -> ascending index lists and counts.
+// All passes compute every score with the same MFMA sequence, so a key's
+// score is bit-identical in every pass.
+//
+// Work decomposition of a pass: a workgroup owns 64 pooled rows (query
+// blocks) of one head and one split of up to `split` keys; its 4 waves take
+// the split's 32-key blocks in turn.  S^T = K_blk Q_p^T uses
+// v_mfma_f32_32x32x16_bf16 with the pooled queries held in registers.
+#include <float.h>
+
+#include "device_common.h"
+#include "launch.h"
+
+namespace vecattn {
+namespace {
+
+constexpr int kRowsWG = 64;     // pooled rows per workgroup
+constexpr int kThreads = 256;
+constexpr int kBins = 256;
+constexpr int kLevels = 4;      // histogram refinements per round
+constexpr int kCand = 1024;     // candidate capacity per row
+constexpr int kRounds = 2;      // a topP row whose count exceeds cap reruns as topK(cap)
+
+enum Phase : int { PH_IDLE = 0, PH_HIST = 1, PH_COLLECT = 2, PH_DONE = 3 };
+enum Mode : int { MODE_HIST = 0, MODE_COLLECT = 1, MODE_EMIT = 2 };
+
+struct RowState {
+  int phase;
+  int level;        // histogram level the next HIST pass runs (interval = levels < level)
+  int topp;         // 1: cut by mass, 0: cut by rank
+  int k_target;     // topK: number of keys to keep
+  int k_rem;        // topK: rank of the cut inside the interval (1 = highest)
+  int L;            // eligible keys
+  int tie_partial;  // 1: only the first k_eq keys tied at t* are kept
+  int k_eq;         // keys tied at t* that are kept
+  int count;        // final count
+  int clamped;      // 1 if the threshold selection was clamped to cap
+  int pad0, pad1;
+  float lo[kLevels];
+  float inv[kLevels];
+  int ba[kLevels];
+  int bb[kLevels];
+  float tstar;
+  float pad2;
+  double ref;       // softmax reference (an upper bound of the row's scores)
+  double Z;         // total mass (topP)
+  double pZ;        // p * Z
+};
+
+struct SelParams {
+  const uint16_t* qp;     // pooled queries, [rows][D] contiguous, rows = bh * Np + i
+  const uint16_t* k;
+  int64_t k_sB, k_sH, k_sN;
+  RowState* st;
+  uint32_t* hist;         // [rows][kBins]
+  uint32_t* n_above;      // [rows][nsplit]
+  double* m_above;        // [rows][nsplit]
+  double* zpart;          // [rows][nsplit]
+  uint32_t* cand_n;       // [rows]
+  uint32_t* cand_lohi;    // [rows][2] ordered-score min / max of collected candidates
+  uint64_t* cand;         // [rows][kCand]
+  uint32_t* bsel;         // [rows][W]
+  uint32_t* btie;         // [rows][W]
+  float* qnorm;           // [rows]
+  float* kmax;            // [B * Hkv]
+  int32_t* idx;
+  int32_t* counts;
+  int32_t* n_clamped;
+  int64_t cap;
+  int64_t rows;
+  int B, Hq, Hkv, group, N, P, Np, D, causal, split, nsplit, W, nrb;  // nrb: row blocks per head
+  int mode_topp;
+  double param;
+  float tau;
+};
+
+__device__ __forceinline__ uint32_t ord_key(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float ord_val(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
+
+__device__ __forceinline__ int eligible(int i, int P, int N, int causal) {
+  return causal ? min(N, (i + 1) * P) : N;
+}
+
+__device__ __forceinline__ int topk_count(double r, int L) {
+  int k = static_cast<int>(ceil(r * static_cast<double>(L) - 1e-9));
+  return min(max(k, 1), L);
+}
+
+// exp(s - ref) for topP masses: exp2 in fp32 while the exponent is in range
+// (relative error ~1e-7), with an exact power-of-two rescale below it.
+__device__ __forceinline__ double mass_term(float s, double ref) {
+  const double y = (static_cast<double>(s) - ref) * 1.4426950408889634;
+  if (y > -120.0) return static_cast<double>(__builtin_amdgcn_exp2f(static_cast<float>(y)));
+  const double n = floor(y);
+  return ldexp(static_cast<double>(__builtin_amdgcn_exp2f(static_cast<float>(y - n))), static_cast<int>(n));
+}
+
+// Bin of s at one level (must be evaluated identically everywhere).
+__device__ __forceinline__ int bin_of(float s, float lo, float inv) {
+  const float x = (s - lo) * inv;
+  int b = static_cast<int>(floorf(x));
+  return min(max(b, 0), kBins - 1);
+}
+
+// Position of score s relative to the interval of `nlev` levels:
+// +1 above, -1 below, 0 inside; *bin = its bin at level nlev when inside.
+struct RowInterval {
+  float lo[kLevels], inv[kLevels];
+  int ba[kLevels], bb[kLevels];
+  int nlev;
+};
+__device__ __forceinline__ int classify(float s, const RowInterval& I) {
+  for (int l = 0; l < I.nlev; ++l) {
+    const int b = bin_of(s, I.lo[l], I.inv[l]);
+    if (b > I.bb[l]) return 1;
+    if (b < I.ba[l]) return -1;
+  }
+  return 0;
+}
+
+// ---------------------------------------------------------------------------
+// Per-row setup: eligible keys, targets, first interval [-c, c] with
+// c >= tau * |q_p| * max |k| (Cauchy-Schwarz, padded for fp32 rounding).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
+  const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (r >= p.rows) return;
+  RowState& s = p.st[r];
+  const int i = static_cast<int>(r % p.Np);
+  const int64_t bh = r / p.Np;
+  const int b = static_cast<int>(bh / p.Hq), h = static_cast<int>(bh % p.Hq);
+  if (round > 0) {
+    if (s.phase != PH_IDLE) return;   // only rows sent back for a second round
+  } else {
+    s.L = eligible(i, p.P, p.N, p.causal);
+    s.clamped = 0;
+    s.topp = p.mode_topp;
+    if (!p.mode_topp) s.k_target = topk_count(p.param, s.L);
+  }
+  const float c = p.tau * p.qnorm[r] * p.kmax[b * p.Hkv + h / p.group];
+  const float cc = c * 1.0009765625f + 1e-30f;
+  s.level = 0;
+  s.phase = PH_HIST;
+  s.lo[0] = -cc;
+  s.inv[0] = static_cast<float>(kBins) / (2.0f * cc);
+  s.ba[0] = 0;
+  s.bb[0] = kBins - 1;
+  s.k_rem = s.k_target;
+  s.ref = static_cast<double>(cc);
+  s.tie_partial = 0;
+  s.k_eq = 0;
+  p.cand_n[r] = 0;
+  p.cand_lohi[2 * r] = 0xFFFFFFFFu;
+  p.cand_lohi[2 * r + 1] = 0u;
+}
+
+// ---------------------------------------------------------------------------
+// Norms for the bound: |q_p| per pooled row (from its bf16 values) and the
+// largest |k_j| per key/value head.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_qnorm(const uint16_t* __restrict__ qp, int64_t rows, int D,
+                                               float* __restrict__ out) {
+  const int64_t r = static_cast<int64_t>(blockIdx.x) * (blockDim.x / 64) + threadIdx.x / 64;
+  const int lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  float acc = 0.0f;
+  for (int d = lane; d < D; d += 64) {
+    const float x = bf16_bits_to_f32(qp[r * D + d]);
+    acc = __builtin_fmaf(x, x, acc);
+  }
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+  if (lane == 0) out[r] = sqrtf(acc);
+}
+
+__global__ __launch_bounds__(256) void k_kmax_init(float* kmax, int n) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < n) kmax[t] = 0.0f;
+}
+
+__global__ __launch_bounds__(256) void k_kmax(const uint16_t* __restrict__ k, int64_t sB, int64_t sH,
+                                              int64_t sN, int Hkv, int N, int D,
+                                              float* __restrict__ kmax) {
+  // one wave per 64 key rows; lane = row
+  const int bh = blockIdx.y;
+  const int b = bh / Hkv, h = bh % Hkv;
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  float nrm = 0.0f;
+  if (j < N) {
+    const uint16_t* row = k + b * sB + h * sH + static_cast<int64_t>(j) * sN;
+    float acc = 0.0f;
+    for (int d = 0; d < D; d += 8) {
+      const u32x4 w = *reinterpret_cast<const u32x4*>(row + d);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float a = bf16_bits_to_f32(w[e] & 0xFFFFu), c = bf16_bits_to_f32(w[e] >> 16);
+        acc = __builtin_fmaf(a, a, acc);
+        acc = __builtin_fmaf(c, c, acc);
+      }
+    }
+    nrm = sqrtf(acc);
+  }
+  for (int o = 32; o > 0; o >>= 1) nrm = fmaxf(nrm, __shfl_xor(nrm, o));
+  if ((threadIdx.x & 63) == 0) atomicMax(reinterpret_cast<unsigned int*>(kmax + bh), __float_as_uint(nrm));
+}
+
+// ---------------------------------------------------------------------------
+// The scoring pass.
+// ---------------------------------------------------------------------------
+template <int D, int MODE>
+__global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
+  constexpr int DS = D / 16;
+  constexpr int HS = kBins + 1;  // odd row stride: rows hitting the same bin use different banks
+  __shared__ uint32_t s_hist[(MODE == MODE_HIST) ? kRowsWG * HS : 1];
+  __shared__ int s_part[kRowsWG];
+  __shared__ RowInterval s_iv[kRowsWG];
+  __shared__ float s_tstar[kRowsWG];
+  __shared__ int s_L[kRowsWG];
+  __shared__ int s_tie[kRowsWG];
+  __shared__ double s_ref[kRowsWG];
+  __shared__ int s_lev0[kRowsWG];
+  __shared__ double s_zred[4][kRowsWG];
+  __shared__ double s_mred[4][kRowsWG];
+  __shared__ uint32_t s_nred[4][kRowsWG];
+  __shared__ int s_any;
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63, g = lane >> 5, ln = lane & 31;
+  // grid: x = split, y = row block, z = bh
+  const int sp = blockIdx.x;
+  const int rb = blockIdx.y;
+  const int64_t bh = blockIdx.z;
+  const int b = static_cast<int>(bh / p.Hq), h = static_cast<int>(bh % p.Hq);
+  const int hk = h / p.group;
+  const int i0 = rb * kRowsWG;
+  const int nrows = min(kRowsWG, p.Np - i0);
+  const int Ltile = eligible(i0 + nrows - 1, p.P, p.N, p.causal);
+  const int key0 = sp * p.split;
+  if (key0 >= Ltile) return;
+  const int key1 = min(key0 + p.split, Ltile);
+  const int64_t row0 = bh * p.Np + i0;
+
+  if (tid == 0) s_any = 0;
+  __syncthreads();
+  if (tid < kRowsWG) {
+    int part = 0;
+    if (tid < nrows) {
+      const RowState& s = p.st[row0 + tid];
+      if (MODE == MODE_HIST) part = (s.phase == PH_HIST);
+      else if (MODE == MODE_COLLECT) part = (s.phase == PH_COLLECT);
+      else part = (s.phase == PH_DONE);
+      if (part) {
+        RowInterval iv;
+        iv.nlev = (MODE == MODE_EMIT) ? 0 : s.level;
+        for (int l = 0; l < kLevels; ++l) {
+          iv.lo[l] = s.lo[l];
+          iv.inv[l] = s.inv[l];
+          iv.ba[l] = s.ba[l];
+          iv.bb[l] = s.bb[l];
+        }
+        s_iv[tid] = iv;
+        s_tstar[tid] = s.tstar;
+        s_L[tid] = s.L;
+        s_tie[tid] = s.tie_partial;
+        s_ref[tid] = s.topp ? s.ref : 0.0;
+        s_lev0[tid] = (s.level == 0);
+        if (!s.topp) s_ref[tid] = -1.0;  // marker: no masses needed
+      }
+    }
+    s_part[tid] = part;
+    if (part) atomicOr(&s_any, 1);
+  }
+  if (MODE == MODE_HIST)
+    for (int t = tid; t < kRowsWG * HS; t += kThreads) s_hist[t] = 0u;
+  __syncthreads();
+  if (!s_any) return;
+
+  // Pooled queries as the B operand: lane -> row ln of row block rb2, head-dim
+  // slots 16s + 8g .. +7.
+  bf16x8 qf[2][DS];
+#pragma unroll
+  for (int rb2 = 0; rb2 < 2; ++rb2) {
+    const int rr = rb2 * 32 + ln;
+    const bool have = rr < nrows;
+    const u32x4* src = reinterpret_cast<const u32x4*>(p.qp + (row0 + (have ? rr : 0)) * D);
+#pragma unroll
+    for (int s2 = 0; s2 < DS; ++s2) {
+      const u32x4 t = have ? src[2 * s2 + g] : u32x4{0, 0, 0, 0};
+      qf[rb2][s2] = __builtin_bit_cast(bf16x8, t);
+    }
+  }
+
+  // Per-lane row state for the two rows this lane owns (rb2 = 0, 1).
+  double zacc[2] = {0.0, 0.0}, macc[2] = {0.0, 0.0};
+  uint32_t nacc[2] = {0u, 0u};
+
+  const uint16_t* kh = p.k + b * p.k_sB + hk * p.k_sH;
+  const int nblk = (key1 - key0 + 31) / 32;
+  for (int blk = wave; blk < nblk; blk += 4) {
+    const int kb = key0 + blk * 32;
+    const int kr = min(kb + ln, p.N - 1);
+    const u32x4* ksrc = reinterpret_cast<const u32x4*>(kh + static_cast<int64_t>(kr) * p.k_sN);
+    u32x4 ka[DS];
+#pragma unroll
+    for (int s2 = 0; s2 < DS; ++s2) ka[s2] = ksrc[2 * s2 + g];
+#pragma unroll
+    for (int rb2 = 0; rb2 < 2; ++rb2) {
+      const int rl = rb2 * 32 + ln;  // local row
+      f32x16 acc = f32x16{};
+#pragma unroll
+      for (int s2 = 0; s2 < DS; ++s2)
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ka[s2]),
+                                                      qf[rb2][s2], acc, 0, 0, 0);
+      const bool part = rl < nrows && s_part[rl];
+      if (!part) continue;
+      const int L = s_L[rl];
+      if (MODE == MODE_EMIT) {
+        const float ts = s_tstar[rl];
+        const bool tiep = s_tie[rl];
+        uint32_t wsel = 0u, wtie = 0u;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+          const float sc = acc[e] * p.tau;
+          const bool ok = kb + kl < L;
+          if (ok && sc > ts) wsel |= 1u << kl;
+          if (ok && sc == ts) wtie |= 1u << kl;
+        }
+        wsel |= __shfl_xor(wsel, 32);
+        wtie |= __shfl_xor(wtie, 32);
+        if (!tiep) wsel |= wtie;
+        if (g == 0) {
+          const int64_t row = row0 + rl;
+          p.bsel[row * p.W + kb / 32] = wsel;
+          if (tiep) p.btie[row * p.W + kb / 32] = wtie;
+        }
+        continue;
+      }
+      const RowInterval& iv = s_iv[rl];
+      const double ref = s_ref[rl];
+      const bool lev0 = s_lev0[rl];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int key = kb + 8 * (e >> 2) + 4 * g + (e & 3);
+        if (key >= L) continue;
+        const float sc = acc[e] * p.tau;
+        const int cls = classify(sc, iv);
+        if (ref >= 0.0) {
+          const double mt = mass_term(sc, ref);
+          if (MODE == MODE_HIST && lev0) zacc[rb2] += mt;
+          if (cls > 0) macc[rb2] += mt;
+        }
+        if (cls > 0) {
+          nacc[rb2] += 1u;
+        } else if (cls == 0) {
+          if (MODE == MODE_HIST) {
+            const int bn = bin_of(sc, iv.lo[iv.nlev], iv.inv[iv.nlev]);
+            atomicAdd(&s_hist[rl * HS + bn], 1u);
+          } else {  // collect
+            const int64_t row = row0 + rl;
+            const uint32_t pos = atomicAdd(&p.cand_n[row], 1u);
+            const uint32_t ok = ord_key(sc);
+            if (pos < kCand)
+              p.cand[row * kCand + pos] = (static_cast<uint64_t>(ok) << 32) | (~static_cast<uint32_t>(key));
+            atomicMin(&p.cand_lohi[2 * row], ok);
+            atomicMax(&p.cand_lohi[2 * row + 1], ok);
+          }
+        }
+      }
+    }
+  }
+  if (MODE == MODE_EMIT) return;
+
+  // Reduce per-row partials: lanes (ln, g=0/1) of each wave, then the 4 waves
+  // in a fixed order (deterministic sums).
+#pragma unroll
+  for (int rb2 = 0; rb2 < 2; ++rb2) {
+    double z = zacc[rb2] + __shfl_xor(zacc[rb2], 32);
+    double m = macc[rb2] + __shfl_xor(macc[rb2], 32);
+    uint32_t n = nacc[rb2] + __shfl_xor(nacc[rb2], 32);
+    if (g == 0) {
+      s_zred[wave][rb2 * 32 + ln] = z;
+      s_mred[wave][rb2 * 32 + ln] = m;
+      s_nred[wave][rb2 * 32 + ln] = n;
+    }
+  }
+  __syncthreads();
+  if (tid < nrows && s_part[tid]) {
+    const int64_t row = row0 + tid;
+    const double z = ((s_zred[0][tid] + s_zred[1][tid]) + s_zred[2][tid]) + s_zred[3][tid];
+    const double m = ((s_mred[0][tid] + s_mred[1][tid]) + s_mred[2][tid]) + s_mred[3][tid];
+    const uint32_t n = s_nred[0][tid] + s_nred[1][tid] + s_nred[2][tid] + s_nred[3][tid];
+    p.n_above[row * p.nsplit + sp] = n;
+    p.m_above[row * p.nsplit + sp] = m;
+    if (MODE == MODE_HIST && s_lev0[tid]) p.zpart[row * p.nsplit + sp] = z;
+  }
+  if (MODE == MODE_HIST) {
+    for (int t = tid; t < nrows * kBins; t += kThreads) {
+      const int rl = t / kBins, bn = t % kBins;
+      const uint32_t c = s_hist[rl * HS + bn];
+      if (c && s_part[rl]) atomicAdd(&p.hist[(row0 + rl) * kBins + bn], c);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Resolve after a HIST pass: one wave per row.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
+  const int64_t r = blockIdx.x;
+  RowState& s = p.st[r];
+  if (s.phase != PH_HIST || s.level != level) return;
+  __shared__ uint32_t hs[kBins];
+  const int lane = threadIdx.x;
+  for (int t = lane; t < kBins; t += 64) {
+    hs[t] = p.hist[r * kBins + t];
+    p.hist[r * kBins + t] = 0u;  // ready for the next level
+  }
+  __syncthreads();
+  if (lane != 0) return;
+  // Sum the per-split statistics in split order.
+  const int64_t bh = r / p.Np;
+  const int i = static_cast<int>(r % p.Np);
+  const int rb = i / kRowsWG;
+  const int i_last = min(p.Np, (rb + 1) * kRowsWG) - 1;
+  const int Ltile = eligible(i_last, p.P, p.N, p.causal);
+  const int ns = (Ltile + p.split - 1) / p.split;
+  uint32_t nab = 0;
+  double mab = 0.0, z = 0.0;
+  for (int q = 0; q < ns; ++q) {
+    nab += p.n_above[r * p.nsplit + q];
+    mab += p.m_above[r * p.nsplit + q];
+    if (level == 0) z += p.zpart[r * p.nsplit + q];
+  }
+  (void)bh;
+  if (level == 0 && s.topp) {
+    s.Z = z;
+    s.pZ = p.param * z;
+  }
+  const float lo = s.lo[level], inv = s.inv[level];
+  int ba = -1, bb = -1;
+  uint32_t above_bins = 0;  // keys in bins above bb (inside the interval)
+  if (!s.topp) {
+    const int k_rem = s.k_target - static_cast<int>(nab);  // rank of the cut inside the interval
+    uint32_t cum = 0;
+    for (int bn = kBins - 1; bn >= 0; --bn) {
+      if (hs[bn] == 0) continue;
+      if (cum + hs[bn] >= static_cast<uint32_t>(max(k_rem, 1))) {
+        ba = bb = bn;
+        break;
+      }
+      cum += hs[bn];
+    }
+    if (ba < 0) {  // cannot happen unless the counts disagree; keep the lowest non-empty bin
+      for (int bn = 0; bn < kBins; ++bn)
+        if (hs[bn]) { ba = bb = bn; break; }
+      cum = 0;
+      for (int bn = kBins - 1; bn > ba; --bn) cum += hs[bn];
+    }
+    above_bins = cum;
+    s.k_rem = k_rem - static_cast<int>(above_bins);
+  } else {
+    // Mass bounds per bin from its score range; the cut bin range is every bin
+    // the true cut may lie in.
+    const double T = s.pZ - mab;
+    const float w = 1.0f / inv;
+    const float slop = fabsf(w) * 1e-3f + fabsf(lo) * 1e-6f;
+    double before_lo = 0.0, before_hi = 0.0;
+    int top_nonempty = -1;
+    for (int bn = kBins - 1; bn >= 0; --bn) {
+      if (hs[bn] == 0) continue;
+      if (top_nonempty < 0) top_nonempty = bn;
+      float e_lo = lo + static_cast<float>(bn) * w - slop;
+      float e_hi = lo + static_cast<float>(bn + 1) * w + slop;
+      if (level == 0 && bn == 0) e_lo = -FLT_MAX;
+      if (level == 0 && bn == kBins - 1) e_hi = static_cast<float>(s.ref);
+      const double mlo = hs[bn] * mass_term(e_lo, s.ref);
+      const double mhi = hs[bn] * mass_term(fminf(e_hi, static_cast<float>(s.ref)), s.ref);
+      const bool may_before_lt = before_lo < T;          // true mass before bn may be < T
+      const bool may_through_ge = before_hi + mhi >= T;  // true mass through bn may be >= T
+      if (may_before_lt && may_through_ge) {
+        if (bb < 0) bb = bn;
+        ba = bn;
+      }
+      before_lo += mlo;
+      before_hi += mhi;
+      if (!may_before_lt) break;
+    }
+    if (bb < 0) {  // T <= 0 or rounding: the cut is at the top of the interval
+      bb = ba = top_nonempty >= 0 ? top_nonempty : 0;
+    }
+  }
+  uint32_t inside = 0;
+  for (int bn = ba; bn <= bb; ++bn) inside += hs[bn];
+  s.ba[level] = ba;
+  s.bb[level] = bb;
+  const int nl = level + 1;
+  if (inside <= static_cast<uint32_t>(kCand) || nl >= kLevels) {
+    s.level = nl;
+    s.phase = PH_COLLECT;
+  } else {
+    const float nlo = lo + static_cast<float>(ba) / inv;
+    const float nhi = lo + static_cast<float>(bb + 1) / inv;
+    s.lo[nl] = nlo;
+    s.inv[nl] = static_cast<float>(kBins) / fmaxf(nhi - nlo, FLT_MIN);
+    s.ba[nl] = 0;
+    s.bb[nl] = kBins - 1;
+    s.level = nl;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Resolve after COLLECT: sort the candidates (score desc, index asc) and fix
+// the cut.  One workgroup of 256 threads per row.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_resolve_cand(SelParams p) {
+  const int64_t r = blockIdx.x;
+  RowState& s = p.st[r];
+  if (s.phase != PH_COLLECT) return;
+  __shared__ uint64_t key[kCand];
+  __shared__ int res[4];
+  const int tid = threadIdx.x;
+  const uint32_t nc_raw = p.cand_n[r];
+  const int nc = static_cast<int>(min(nc_raw, static_cast<uint32_t>(kCand)));
+  int np2 = 1;
+  while (np2 < nc) np2 <<= 1;
+  for (int t = tid; t < np2; t += 256) key[t] = t < nc ? p.cand[r * kCand + t] : 0ull;
+  __syncthreads();
+  // bitonic sort, descending
+  for (int k2 = 2; k2 <= np2; k2 <<= 1) {
+    for (int j = k2 >> 1; j > 0; j >>= 1) {
+      for (int t = tid; t < np2; t += 256) {
+        const int x = t ^ j;
+        if (x > t) {
+          const bool desc = (t & k2) == 0;
+          const uint64_t a = key[t], c = key[x];
+          if (desc ? (a < c) : (a > c)) {
+            key[t] = c;
+            key[x] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // statistics of the final interval
+  const int64_t bh = r / p.Np;
+  (void)bh;
+  const int i = static_cast<int>(r % p.Np);
+  const int rb = i / kRowsWG;
+  const int i_last = min(p.Np, (rb + 1) * kRowsWG) - 1;
+  const int Ltile = eligible(i_last, p.P, p.N, p.causal);
+  const int ns = (Ltile + p.split - 1) / p.split;
+  if (tid == 0) {
+    uint32_t nab = 0;
+    double mab = 0.0;
+    for (int q = 0; q < ns; ++q) {
+      nab += p.n_above[r * p.nsplit + q];
+      mab += p.m_above[r * p.nsplit + q];
+    }
+    const bool overflow = nc_raw > static_cast<uint32_t>(kCand);
+    const bool all_tied = p.cand_lohi[2 * r] == p.cand_lohi[2 * r + 1];
+    int n_sel = 0;      // keys kept from the interval (the first n_sel in sorted order)
+    int count = 0;
+    if (!s.topp) {
+      n_sel = s.k_target - static_cast<int>(nab);
+    } else {
+      const double T = s.pZ - mab;
+      if (overflow && all_tied) {
+        const double term = mass_term(ord_val(p.cand_lohi[2 * r]), s.ref);
+        double need = T > 0.0 ? ceil(T / term) : 1.0;
+        n_sel = static_cast<int>(fmin(fmax(need, 1.0), static_cast<double>(nc_raw)));
+      } else {
+        double c = 0.0;
+        n_sel = nc;
+        for (int t = 0; t < nc; ++t) {
+          c += mass_term(ord_val(static_cast<uint32_t>(key[t] >> 32)), s.ref);
+          if (c >= T) { n_sel = t + 1; break; }
+        }
+        if (T <= 0.0) n_sel = 1;
+      }
+    }
+    count = static_cast<int>(nab) + n_sel;
+    // threshold modes: clamp to cap (keep the cap best)
+    if (s.topp && count > p.cap) {
+      if (p.cap <= static_cast<int64_t>(nab)) {
+        // the cap cut lies above this interval: rerun this row as topK(cap)
+        s.topp = 0;
+        s.k_target = static_cast<int>(p.cap);
+        s.clamped = 1;
+        s.phase = PH_IDLE;
+        res[0] = -1;
+      } else {
+        n_sel = static_cast<int>(p.cap - nab);
+        count = static_cast<int>(p.cap);
+        s.clamped = 1;
+      }
+    }
+    if (s.phase == PH_COLLECT) {
+      n_sel = max(n_sel, 0);
+      if (overflow && all_tied) {
+        s.tstar = ord_val(p.cand_lohi[2 * r]);
+        s.tie_partial = n_sel < static_cast<int>(nc_raw);
+        s.k_eq = n_sel;
+      } else if (n_sel == 0) {
+        // nothing kept from the interval: cut just above it
+        s.tstar = nc > 0 ? ord_val(static_cast<uint32_t>(key[0] >> 32)) : FLT_MAX;
+        s.tie_partial = 1;
+        s.k_eq = 0;
+      } else {
+        const int m = min(n_sel, max(nc, 1)) - 1;
+        const uint32_t tk = static_cast<uint32_t>(key[m] >> 32);
+        s.tstar = ord_val(tk);
+        // ties at t*: kept ones are sorted first by index
+        int kept_ties = 0, all_ties = 0;
+        for (int t = 0; t < nc; ++t) {
+          const uint32_t kk = static_cast<uint32_t>(key[t] >> 32);
+          if (kk == tk) {
+            ++all_ties;
+            if (t <= m) ++kept_ties;
+          }
+        }
+        s.tie_partial = kept_ties < all_ties;
+        s.k_eq = kept_ties;
+      }
+      s.count = count;
+      s.phase = PH_DONE;
+      if (s.clamped && p.n_clamped) atomicAdd(p.n_clamped, 1);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Bitmasks -> ascending index lists.  One wave per row; each lane expands one
+// 32-key word per step into LDS at its prefix position, then the wave copies
+// the staged indices out contiguously.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void k_compact(SelParams p) {
+  const int64_t r = blockIdx.x;
+  const RowState& s = p.st[r];
+  __shared__ int32_t stage[64 * 32];
+  const int lane = threadIdx.x;
+  const int L = s.L;
+  const int nw = (L + 31) / 32;
+  const bool tiep = s.tie_partial;
+  const int k_eq = s.k_eq;
+  int base = 0;      // entries written so far
+  int ties_seen = 0; // tied keys met so far (ascending index)
+  int32_t* out = p.idx + r * p.cap;
+  for (int w0 = 0; w0 < nw; w0 += 64) {
+    const int wd = w0 + lane;
+    const bool valid = wd < nw;
+    uint32_t m = valid ? p.bsel[r * p.W + wd] : 0u;
+    if (tiep) {  // uniform per row: keep only the first k_eq tied keys
+      const uint32_t tw = valid ? p.btie[r * p.W + wd] : 0u;
+      const int nt = __builtin_popcount(tw);
+      int incl = nt;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o);
+        if (lane >= o) incl += y;
+      }
+      int room = k_eq - (ties_seen + incl - nt);  // ties this lane may still keep
+      uint32_t t2 = tw;
+      while (t2 && room > 0) {
+        const uint32_t bit = t2 & (~t2 + 1u);
+        m |= bit;
+        t2 ^= bit;
+        --room;
+      }
+      ties_seen += __shfl(incl, 63);
+    }
+    if (valid && L - 32 * wd < 32) m &= (1u << (L - 32 * wd)) - 1u;
+    const int nb = __builtin_popcount(m);
+    int pre = nb;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(pre, o);
+      if (lane >= o) pre += y;
+    }
+    const int total = __shfl(pre, 63);
+    int pos = pre - nb;
+    uint32_t mm = m;
+    while (mm) {
+      const int bit = __builtin_ctz(mm);
+      mm &= mm - 1;
+      stage[pos++] = 32 * wd + bit;
+    }
+    __syncthreads();
+    for (int t = lane; t < total; t += 64)
+      if (base + t < p.cap) out[base + t] = stage[t];
+    __syncthreads();
+    base += total;
+  }
+  const int n = min(base, static_cast<int>(p.cap));
+  for (int t = n + lane; t < p.cap; t += 64) out[t] = -1;
+  if (lane == 0) p.counts[r] = n;
+}
+
+__global__ __launch_bounds__(256) void k_zero_u32(uint32_t* p, int64_t n) {
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t < n) p[t] = 0u;
+}
+
+// ---------------------------------------------------------------------------
+// Workspace layout.
+// ---------------------------------------------------------------------------
+struct Layout {
+  size_t qp, state, hist, nab, mab, zp, cand_n, cand_lohi, cand, bsel, btie, qnorm, kmax, total;
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+Layout layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t D, int32_t P, int split) {
+  const int64_t Np = (N + P - 1) / P;
+  const int64_t rows = B * Hq * Np;
+  const int64_t nsplit = (N + split - 1) / split;
+  const int64_t W = (N + 31) / 32;
+  Layout l{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) { size_t at = o; o = align256(o + bytes); return at; };
+  l.qp = take(rows * D * 2);
+  l.state = take(rows * sizeof(RowState));
+  l.hist = take(rows * kBins * 4);
+  l.nab = take(rows * nsplit * 4);
+  l.mab = take(rows * nsplit * 8);
+  l.zp = take(rows * nsplit * 8);
+  l.cand_n = take(rows * 4);
+  l.cand_lohi = take(rows * 8);
+  l.cand = take(rows * kCand * 8);
+  l.bsel = take(rows * W * 4);
+  l.btie = take(rows * W * 4);
+  l.qnorm = take(rows * 4);
+  l.kmax = take(B * Hkv * 4);
+  l.total = o;
+  return l;
+}
+
+int choose_split(int64_t B, int64_t Hq, int64_t N, int32_t P) {
+  // Enough workgroups to fill the chip a few times over, splits of at least
+  // 2048 keys (multiples of 128).
+  const int64_t Np = (N + P - 1) / P;
+  const int64_t tiles = B * Hq * ((Np + kRowsWG - 1) / kRowsWG);
+  int64_t want = (tiles * N) / 4096;  // target ~4096 workgroups
+  if (want < 2048) want = 2048;
+  int64_t s = 2048;
+  while (s < want && s < 65536) s <<= 1;
+  if (s > N) s = ((N + 127) / 128) * 128;
+  return static_cast<int>(s);
+}
+
+}  // namespace
+
+size_t select_workspace_bytes(int64_t B, int64_t Hq, int64_t N, int64_t D, int32_t block,
+                              int32_t mode, int64_t cap) {
+  (void)mode;
+  (void)cap;
+  // Hkv is not known here; reserve one bound per query head (>= per kv head).
+  return layout(B, Hq, Hq, N, D, block, choose_split(B, Hq, N, block)).total;
+}
+
+hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
+  const int64_t B = a.q.B, Hq = a.q.H, Hkv = a.k.H, N = a.q.N, D = a.q.D;
+  const int32_t P = a.block;
+  const int64_t Np = (N + P - 1) / P;
+  const int64_t rows = B * Hq * Np;
+  const int split = choose_split(B, Hq, N, P);
+  const Layout l = layout(B, Hq, Hq, N, D, P, split);
+  if (a.workspace_bytes < l.total) return hipErrorInvalidValue;
+  char* ws = static_cast<char*>(a.workspace);
+  SelParams p{};
+  p.qp = reinterpret_cast<const uint16_t*>(ws + l.qp);
+  p.k = static_cast<const uint16_t*>(a.k.ptr);
+  p.k_sB = a.k.sB;
+  p.k_sH = a.k.sH;
+  p.k_sN = a.k.sN;
+  p.st = reinterpret_cast<RowState*>(ws + l.state);
+  p.hist = reinterpret_cast<uint32_t*>(ws + l.hist);
+  p.n_above = reinterpret_cast<uint32_t*>(ws + l.nab);
+  p.m_above = reinterpret_cast<double*>(ws + l.mab);
+  p.zpart = reinterpret_cast<double*>(ws + l.zp);
+  p.cand_n = reinterpret_cast<uint32_t*>(ws + l.cand_n);
+  p.cand_lohi = reinterpret_cast<uint32_t*>(ws + l.cand_lohi);
+  p.cand = reinterpret_cast<uint64_t*>(ws + l.cand);
+  p.bsel = reinterpret_cast<uint32_t*>(ws + l.bsel);
+  p.btie = reinterpret_cast<uint32_t*>(ws + l.btie);
+  p.qnorm = reinterpret_cast<float*>(ws + l.qnorm);
+  p.kmax = reinterpret_cast<float*>(ws + l.kmax);
+  p.idx = a.idx;
+  p.counts = a.counts;
+  p.n_clamped = a.n_clamped;
+  p.cap = a.cap;
+  p.rows = rows;
+  p.B = static_cast<int>(B);
+  p.Hq = static_cast<int>(Hq);
+  p.Hkv = static_cast<int>(Hkv);
+  p.group = static_cast<int>(Hq / Hkv);
+  p.N = static_cast<int>(N);
+  p.P = P;
+  p.Np = static_cast<int>(Np);
+  p.D = static_cast<int>(D);
+  p.causal = a.causal;
+  p.split = split;
+  p.nsplit = static_cast<int>((N + split - 1) / split);
+  p.W = static_cast<int>((N + 31) / 32);
+  p.nrb = static_cast<int>((Np + kRowsWG - 1) / kRowsWG);
+  p.mode_topp = a.mode == 1;
+  p.param = a.param;
+  p.tau = 1.0f / sqrtf(static_cast<float>(D));
+
+  // Pooled queries (Eq. 2) into the workspace, contiguous [rows][D].
+  hipError_t e = launch_pool(a.q, P, const_cast<uint16_t*>(p.qp), Hq * Np * D, Np * D, D, stream);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_qnorm, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream,
+                     p.qp, rows, static_cast<int>(D), p.qnorm);
+  hipLaunchKernelGGL(k_kmax_init, dim3(static_cast<unsigned>((B * Hkv + 255) / 256)), dim3(256), 0,
+                     stream, p.kmax, static_cast<int>(B * Hkv));
+  hipLaunchKernelGGL(k_kmax, dim3(static_cast<unsigned>((N + 255) / 256), static_cast<unsigned>(B * Hkv)),
+                     dim3(256), 0, stream, p.k, a.k.sB, a.k.sH, a.k.sN, static_cast<int>(Hkv),
+                     static_cast<int>(N), static_cast<int>(D), p.kmax);
+  const int64_t nh = rows * kBins;
+  hipLaunchKernelGGL(k_zero_u32, dim3(static_cast<unsigned>((nh + 255) / 256)), dim3(256), 0, stream,
+                     p.hist, nh);
+  const dim3 pgrid(static_cast<unsigned>(p.nsplit), static_cast<unsigned>(p.nrb),
+                   static_cast<unsigned>(B * Hq));
+  const dim3 rgrid(static_cast<unsigned>(rows));
+  const dim3 igrid(static_cast<unsigned>((rows + 255) / 256));
+  for (int round = 0; round < kRounds; ++round) {
+    hipLaunchKernelGGL(k_sel_init, igrid, dim3(256), 0, stream, p, round);
+    for (int lv = 0; lv < kLevels; ++lv) {
+      if (D == 128) hipLaunchKernelGGL((k_score_pass<128, MODE_HIST>), pgrid, dim3(kThreads), 0, stream, p);
+      else hipLaunchKernelGGL((k_score_pass<64, MODE_HIST>), pgrid, dim3(kThreads), 0, stream, p);
+      hipLaunchKernelGGL(k_resolve_hist, rgrid, dim3(64), 0, stream, p, lv);
+    }
+    if (D == 128) hipLaunchKernelGGL((k_score_pass<128, MODE_COLLECT>), pgrid, dim3(kThreads), 0, stream, p);
+    else hipLaunchKernelGGL((k_score_pass<64, MODE_COLLECT>), pgrid, dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL(k_resolve_cand, rgrid, dim3(256), 0, stream, p);
+  }
+  if (D == 128) hipLaunchKernelGGL((k_score_pass<128, MODE_EMIT>), pgrid, dim3(kThreads), 0, stream, p);
+  else hipLaunchKernelGGL((k_score_pass<64, MODE_EMIT>), pgrid, dim3(kThreads), 0, stream, p);
+  hipLaunchKernelGGL(k_compact, rgrid, dim3(64), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace vecattn

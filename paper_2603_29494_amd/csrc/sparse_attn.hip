@@ -1,0 +1,365 @@
+// Vector-sparse attention (paper Eq. 4, Sec. 3.2; appendix Algorithm 2) for gfx950.
+//
+// One workgroup (4 waves) owns up to 64 query rows of one query block of one
+// head and walks the block's index list I[b,h,i,0:C) in tiles of 64 keys.
+// The K and V rows of a tile are gathered straight from global memory into
+// LDS (global_load_lds, 16 B per lane, no register staging) two tiles deep,
+// stored row-major with an XOR swizzle of their 16-byte chunks so that both
+// the row reads of K and the transposing reads of V (ds_read_b64_tr_b16) are
+// free of bank conflicts.  The waves compute S^T = K_tile Q^T and
+// O^T += V_tile^T P^T with v_mfma_f32_32x32x16_bf16 and keep the
+// online-softmax state in registers.  Wave w = (rw, kw): rw picks 32 of the
+// 64 query rows, kw picks 32 of the 64 keys of each tile; the two key halves
+// are merged at the end.
+//
+// MFMA 32x32x16 lane layout (lane l, g = l / 32):
+//   A (M x K): lane holds row l % 32, K-slots 8g .. 8g + 7
+//   B (K x N): lane holds column l % 32, K-slots 8g .. 8g + 7
+//   C (M x N): lane holds column l % 32, rows 8 * (v / 4) + 4g + v % 4, v < 16
+// Only the pairing of K-slots between A and B matters for the product, so the
+// keys of a K-step are ordered to match C's row order.
+//
+// ds_read_b64_tr_b16, per group of 16 lanes: lane 4p + c receives as element q
+// the c-th 16-bit value at the address supplied by lane 4q + p.
+#include "device_common.h"
+#include "launch.h"
+
+namespace vecattn {
+namespace {
+
+constexpr int kRows = 64;     // query rows per workgroup
+constexpr int kTile = 64;     // keys per gathered tile
+constexpr int kThreads = 256;
+constexpr int kStages = 2;
+
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
+#define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
+
+
+// Chunk swizzle: 16-byte chunk c of row r lives at chunk c ^ swz(r).  swz is
+// a bijection on the row's low bits, so 16 consecutive rows reading the same
+// chunk hit 16 different chunks; r % 4 drives output bits 1-2, so 4
+// consecutive rows x 2 adjacent chunks land on 8 distinct chunks.
+template <int D>
+__host__ __device__ __forceinline__ constexpr int swz(int r) {
+  if constexpr (D == 128) return ((r & 3) << 1) | ((r >> 2) & 1) | (r & 8);
+  else return ((r & 3) << 1) | ((r >> 2) & 1);
+}
+
+// 16-byte global -> LDS copy per lane (LDS destination: wave-uniform base +
+// 16 * lane).  The 16-byte form exists only on gfx950; the host pass of the
+// compiler rejects it, so the call is compiled for the device side only.
+__device__ __forceinline__ void gather16_to_lds(const void* src, void* lds_base) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_global_load_lds(src, LDS_PTR(void, lds_base), 16, 0, 0);
+#endif
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void k_sparse_attn(
+    const uint16_t* __restrict__ q, int64_t q_sB, int64_t q_sH, int64_t q_sN,
+    const uint16_t* __restrict__ k, int64_t k_sB, int64_t k_sH, int64_t k_sN,
+    const uint16_t* __restrict__ v, int64_t v_sB, int64_t v_sH, int64_t v_sN,
+    uint16_t* __restrict__ o, int64_t o_sB, int64_t o_sH, int64_t o_sN, float* __restrict__ lse,
+    const int32_t* __restrict__ idx, const int32_t* __restrict__ counts, int64_t cap, int32_t Hq,
+    int32_t group, int32_t N, int32_t P, int32_t Np, int32_t chunks, int32_t causal,
+    float scale_log2, int64_t total, int64_t per_xcd) {
+  constexpr int CH = D / 8;                 // 16-byte chunks per row
+  constexpr int U = kTile * CH / kThreads;  // direct-load instructions per wave per matrix
+  constexpr int DS = D / 16;                // MFMA K-steps over the head dimension
+  constexpr int DB = D / 32;                // 32-wide blocks of the head dimension
+  constexpr int RB = 2 * D;                 // bytes per LDS row
+  // Each pipeline stage is its own LDS object, so that the compiler can tell
+  // that reads of one stage do not depend on the gathers in flight into the
+  // other and does not make them wait for those.
+  __shared__ __align__(16) uint16_t k_s0[kTile * D];
+  __shared__ __align__(16) uint16_t k_s1[kTile * D];
+  __shared__ __align__(16) uint16_t v_s0[kTile * D];
+  __shared__ __align__(16) uint16_t v_s1[kTile * D];
+  __shared__ __align__(16) int32_t id_s0[kTile];
+  __shared__ __align__(16) int32_t id_s1[kTile];
+  // Stage selectors; always called with a constant stage, so they fold to a
+  // direct reference to one LDS object.
+  auto kbuf = [&](int st) __attribute__((always_inline)) { return st ? k_s1 : k_s0; };
+  auto vbuf = [&](int st) __attribute__((always_inline)) { return st ? v_s1 : v_s0; };
+  auto ibuf = [&](int st) __attribute__((always_inline)) { return st ? id_s1 : id_s0; };
+
+  const int64_t w = xcd_work_item(per_xcd);
+  if (w >= total) return;
+  const int chunk = static_cast<int>(w % chunks);
+  const int64_t rest = w / chunks;
+  const int i = static_cast<int>(rest % Np);
+  const int64_t bh = rest / Np;
+  const int b = static_cast<int>(bh / Hq);
+  const int h = static_cast<int>(bh % Hq);
+  const int hk = h / group;
+
+  const int row0 = i * P + chunk * kRows;
+  const int row_end = min(N, min(i * P + P, row0 + kRows));
+  const int count = static_cast<int>(min<int64_t>(max(counts[bh * Np + i], 0), cap));
+  const int32_t* list = idx + (bh * Np + i) * cap;
+  const int ntiles = (count + kTile - 1) / kTile;
+  // Reads of the list past `count` return 0 (buffer range check).
+  const __amdgpu_buffer_rsrc_t lrs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(list), 0, count * 4, 0x00020000);
+
+  const uint16_t* kh = k + b * k_sB + hk * k_sH;
+  const uint16_t* vh = v + b * v_sB + hk * v_sH;
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  const int lane = tid & 63;
+  const int g = lane >> 5;
+  const int ln = lane & 31;
+  const int rw = wave & 1;
+  const int kw = wave >> 1;
+
+  // Q^T operand: this lane's query row, head-dim slots 16s + 8g .. +7.
+  const int my_row = row0 + 32 * rw + ln;
+  bf16x8 qf[DS];
+  {
+    const bool have = my_row < row_end;
+    const u32x4* qr = reinterpret_cast<const u32x4*>(
+        q + b * q_sB + h * q_sH + static_cast<int64_t>(have ? my_row : row0) * q_sN);
+#pragma unroll
+    for (int s = 0; s < DS; ++s) {
+      const u32x4 t = have ? qr[2 * s + g] : u32x4{0, 0, 0, 0};
+      qf[s] = __builtin_bit_cast(bf16x8, t);
+    }
+    // Retire the Q loads here, so that the compiler's wait analysis does not
+    // make the first MFMA of every tile wait for the gathers in flight.
+    wait_vmcnt<0>();
+  }
+
+  // Gather mapping: direct-load instruction u of this wave covers LDS chunks
+  // [(wave*U + u)*64, +64) of a tile; lane -> (row r, physical chunk x), and
+  // it fetches logical chunk x ^ swz(r) of key row ids[r].
+  auto grow = [&](int u) __attribute__((always_inline)) { return ((wave * U + u) * 64 + lane) / CH; };
+  auto gcol = [&](int u) __attribute__((always_inline)) {
+    const int L = (wave * U + u) * 64 + lane;
+    return (L % CH) ^ swz<D>(L / CH);
+  };
+  int nid[U];  // key ids of the next tile to issue (raw; clamped when used)
+
+  auto load_ids = [&](int t) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      nid[u] = __builtin_amdgcn_raw_buffer_load_b32(lrs, (t * kTile + grow(u)) * 4, 0, 0);
+  };
+  auto issue_tile = [&](int t, int st) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t r = min(max(nid[u], 0), N - 1);  // memory safety only
+      uint16_t* kd = kbuf(st) + (wave * U + u) * 64 * 8;
+      uint16_t* vd = vbuf(st) + (wave * U + u) * 64 * 8;
+      gather16_to_lds(kh + r * k_sN + 8 * gcol(u), kd);
+      gather16_to_lds(vh + r * v_sN + 8 * gcol(u), vd);
+    }
+    if (wave == 0)  // the tile's key ids (clamped to the list; entries past count are masked)
+      __builtin_amdgcn_global_load_lds(list + min(t * kTile + lane, count - 1),
+                                       LDS_PTR(void, ibuf(st)), 4, 0, 0);
+  };
+
+  f32x16 oacc[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) oacc[db] = f32x16{};
+  float m_run = kNegInf;  // reference max (log2 units) this lane's row is scaled against
+  float l_run = 0.0f;     // this lane's partial normaliser
+
+  if (ntiles > 0) {
+    load_ids(0);
+    issue_tile(0, 0);
+    load_ids(1);
+  }
+
+  // Per-lane constants of the LDS reads.
+  const int krow = 32 * kw + ln;
+  const int ksw = swz<D>(krow);
+  const int j16 = lane & 15;
+  const int tq = j16 >> 2, tp = j16 & 3;
+  const int vhalf = (lane >> 4) & 1;
+
+  auto step = [&](const int t, const int st) __attribute__((always_inline)) {
+    // Tile t has landed, and the ids of tile t+1 (issued right after it) too;
+    // the barrier (no fence: all LDS traffic here is waited for explicitly)
+    // also guarantees every wave is done reading the other stage.
+    wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    if (t + 1 < ntiles) issue_tile(t + 1, st ^ 1);
+    load_ids(t + 2);  // past the list these read 0
+
+    // S^T = K_tile Q^T for this wave's 32 keys x 32 rows.
+    f32x16 sacc = f32x16{};
+    const char* kb = reinterpret_cast<const char*>(kbuf(st)) + krow * RB;
+#pragma unroll
+    for (int s2 = 0; s2 < DS; ++s2) {
+      const u32x4 a = *reinterpret_cast<const u32x4*>(kb + 16 * ((2 * s2 + g) ^ ksw));
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), qf[s2], sacc,
+                                                     0, 0, 0);
+    }
+
+    // Masks are needed only on the list's last tile and, when causal, on tiles
+    // reaching past this wave's first row (lists are ascending).
+    const int tbase = t * kTile;
+    const int nvalid = min(kTile, count - tbase);
+    const int32_t* ids = ibuf(st);
+    const bool need_mask = nvalid < kTile || (causal && ids[nvalid - 1] > row0 + 32 * rw);
+    if (need_mask) {
+#pragma unroll
+      for (int m4 = 0; m4 < 4; ++m4) {
+        const int kl = 32 * kw + 8 * m4 + 4 * g;
+        const int lim = nvalid - kl;  // entries e < lim of this group are in the list
+        const int4 jj = *reinterpret_cast<const int4*>(ids + kl);
+        const int js[4] = {jj.x, jj.y, jj.z, jj.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const bool ok = (e < lim) && (!causal || js[e] <= my_row);
+          sacc[4 * m4 + e] = ok ? sacc[4 * m4 + e] : kNegInf;
+        }
+      }
+    }
+    float tmax = kNegInf;
+#pragma unroll
+    for (int e = 0; e < 16; e += 2) tmax = fmaxf(tmax, fmaxf(sacc[e], sacc[e + 1]));
+    tmax = wave_max_xor32(tmax);
+
+    // Lazy rescaling: the reference max moves only when a row's max exceeds it
+    // by more than 8 (log2 units; P stays <= 256, harmless in bf16/fp32); O and
+    // l are rescaled only when some row of the wave moved.
+    const float m_new = fmaxf(m_run, tmax * scale_log2);
+    const bool move = m_new > m_run + 8.0f;
+    if (__any(move)) {
+      const float m_ref = move ? m_new : m_run;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - (m_ref == kNegInf ? 0.0f : m_ref));
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
+      m_run = m_ref;
+    }
+    const float m_sub = m_run == kNegInf ? 0.0f : m_run;
+    float psum = 0.0f;
+    f32x8 pf[2];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[e], scale_log2, -m_sub));
+      psum += p;
+      pf[e >> 3][e & 7] = p;
+    }
+    l_run += psum;
+    const bf16x8 pb0 = __builtin_convertvector(pf[0], bf16x8);
+    const bf16x8 pb1 = __builtin_convertvector(pf[1], bf16x8);
+
+    // O^T += V_tile^T P^T; the V^T operand comes from transposing LDS reads.
+    const char* vb = reinterpret_cast<const char*>(vbuf(st));
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int d = 32 * db + 16 * vhalf + 4 * tp;  // first of the 4 head-dim values addressed
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const int k0 = 32 * kw + 16 * ks + 4 * g + tq;  // key row this lane addresses
+        const int k1 = k0 + 8;
+        const char* a0 = vb + k0 * RB + 16 * ((d >> 3) ^ swz<D>(k0)) + 8 * ((d >> 2) & 1);
+        const char* a1 = vb + k1 * RB + 16 * ((d >> 3) ^ swz<D>(k1)) + 8 * ((d >> 2) & 1);
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(i16x4, a0));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(i16x4, a1));
+        const i16x8 av = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av),
+                                                           ks ? pb1 : pb0, oacc[db], 0, 0, 0);
+      }
+    }
+  };
+  for (int t = 0; t < ntiles; t += 2) {
+    step(t, 0);
+    if (t + 1 < ntiles) step(t + 1, 1);
+  }
+
+  // Merge the two key halves (kw = 1 hands its state to kw = 0 through LDS).
+  l_run += __shfl_xor(l_run, 32);
+  wait_vmcnt<0>();  // no gather may still be landing in the buffers reused below
+  __syncthreads();
+  // Reuse the tile buffers: O of row half rw in k_s0 / v_s0, (m, l) in k_s1.
+  float* red_o = reinterpret_cast<float*>(rw ? v_s0 : k_s0);
+  float* red_ml = reinterpret_cast<float*>(k_s1) + rw * 128;
+  if (kw == 1) {
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) red_o[(db * 16 + e) * 64 + lane] = oacc[db][e];
+    red_ml[lane] = m_run;
+    red_ml[64 + lane] = l_run;
+  }
+  __syncthreads();
+  if (kw == 1) return;
+
+  const float m1 = red_ml[lane];
+  const float l1 = red_ml[64 + lane];
+  const float m = fmaxf(m_run, m1);
+  float a0 = 0.0f, a1 = 0.0f, inv = 0.0f, l = 0.0f;
+  if (m != kNegInf) {
+    a0 = __builtin_amdgcn_exp2f(m_run - m);
+    a1 = __builtin_amdgcn_exp2f(m1 - m);
+    l = a0 * l_run + a1 * l1;
+    inv = l > 0.0f ? 1.0f / l : 0.0f;
+  }
+  if (my_row >= row_end) return;
+  if (lse && g == 0)
+    lse[bh * N + my_row] = l > 0.0f ? (m + __builtin_log2f(l)) * 0.69314718055994531f : kNegInf;
+  uint16_t* orow = o + b * o_sB + h * o_sH + static_cast<int64_t>(my_row) * o_sN;
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+#pragma unroll
+    for (int vq = 0; vq < 4; ++vq) {
+      f32x4 r;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int ee = 4 * vq + e;
+        r[e] = (a0 * oacc[db][ee] + a1 * red_o[(db * 16 + ee) * 64 + lane]) * inv;
+      }
+      *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * vq + 4 * g) = __builtin_convertvector(r, bf16x4);
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream) {
+  const int64_t B = a.q.B, Hq = a.q.H, N = a.q.N, D = a.q.D;
+  const int32_t P = a.block;
+  const int32_t Np = static_cast<int32_t>((N + P - 1) / P);
+  const int32_t chunks = (P + kRows - 1) / kRows;
+  const int64_t total = B * Hq * static_cast<int64_t>(Np) * chunks;
+  if (total == 0) return hipSuccess;
+  const int64_t per_xcd = (total + 7) / 8;
+  const dim3 grid(static_cast<unsigned>(per_xcd * 8));
+  const float scale = a.scale != 0.0f ? a.scale : 1.0f / sqrtf(static_cast<float>(D));
+  const float scale_log2 = scale * 1.4426950408889634f;
+  const int32_t group = static_cast<int32_t>(Hq / a.k.H);
+  const uint16_t* q = static_cast<const uint16_t*>(a.q.ptr);
+  const uint16_t* k = static_cast<const uint16_t*>(a.k.ptr);
+  const uint16_t* v = static_cast<const uint16_t*>(a.v.ptr);
+  uint16_t* o = static_cast<uint16_t*>(a.o);
+  if (D == 128) {
+    hipLaunchKernelGGL(k_sparse_attn<128>, grid, dim3(kThreads), 0, stream, q, a.q.sB, a.q.sH,
+                       a.q.sN, k, a.k.sB, a.k.sH, a.k.sN, v, a.v.sB, a.v.sH, a.v.sN, o, a.o_sB,
+                       a.o_sH, a.o_sN, a.lse, a.idx, a.counts, a.cap, static_cast<int32_t>(Hq),
+                       group, static_cast<int32_t>(N), P, Np, chunks, a.causal, scale_log2, total,
+                       per_xcd);
+  } else {
+    hipLaunchKernelGGL(k_sparse_attn<64>, grid, dim3(kThreads), 0, stream, q, a.q.sB, a.q.sH,
+                       a.q.sN, k, a.k.sB, a.k.sH, a.k.sN, v, a.v.sB, a.v.sH, a.v.sN, o, a.o_sB,
+                       a.o_sH, a.o_sN, a.lse, a.idx, a.counts, a.cap, static_cast<int32_t>(Hq),
+                       group, static_cast<int32_t>(N), P, Np, chunks, a.causal, scale_log2, total,
+                       per_xcd);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace vecattn

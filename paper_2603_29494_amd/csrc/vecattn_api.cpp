@@ -1,0 +1,160 @@
+// C ABI of libvecattn: argument validation and dispatch to the HIP kernels.
+// Every check happens on the host before any launch; see include/vecattn.h for
+// the contract of each entry point.
+#include "vecattn.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "launch.h"
+
+namespace {
+
+using vecattn::Tensor4;
+
+constexpr int64_t kMaxN = int64_t(1) << 30;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Sizes positive, D contiguous, rows 16-byte aligned.
+vecattn_status check_desc(const void* ptr, const vecattn_tdesc* d) {
+  if (!ptr || !d) return VECATTN_ERR_INVALID_ARG;
+  if (d->B < 1 || d->H < 1 || d->N < 1 || d->D < 1 || d->N > kMaxN) return VECATTN_ERR_INVALID_ARG;
+  if (d->sB < 0 || d->sH < 0 || d->sN < d->D) return VECATTN_ERR_INVALID_ARG;
+  if ((d->sB % 8) || (d->sH % 8) || (d->sN % 8) || !aligned16(ptr)) return VECATTN_ERR_INVALID_ARG;
+  if (d->D != 64 && d->D != 128) return VECATTN_ERR_UNSUPPORTED;
+  return VECATTN_OK;
+}
+
+Tensor4 to_tensor(const void* p, const vecattn_tdesc* d) {
+  return Tensor4{p, d->B, d->H, d->N, d->D, d->sB, d->sH, d->sN};
+}
+
+int64_t num_blocks(int64_t N, int32_t P) { return (N + P - 1) / P; }
+
+int64_t topk_count(double ratio, int64_t L) {
+  int64_t k = static_cast<int64_t>(std::ceil(ratio * static_cast<double>(L) - 1e-9));
+  if (k < 1) k = 1;
+  if (k > L) k = L;
+  return k;
+}
+
+bool param_ok(int32_t mode, double param) {
+  if (mode == VECATTN_SEL_TOPK || mode == VECATTN_SEL_TOPP) return param > 0.0 && param <= 1.0;
+  if (mode == VECATTN_SEL_MINS) return param >= 0.0;
+  return false;
+}
+
+// Largest count any block can produce (k_i is non-decreasing in L_i, so the
+// largest L_i decides).
+int64_t max_count(int64_t N, int32_t P, int32_t causal, int32_t mode, double param) {
+  const int64_t Np = num_blocks(N, P);
+  const int64_t Lmax = causal ? std::min<int64_t>(N, Np * static_cast<int64_t>(P)) : N;
+  return mode == VECATTN_SEL_TOPK ? topk_count(param, Lmax) : Lmax;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t vecattn_version(void) { return 100; }
+
+const char* vecattn_status_string(vecattn_status s) {
+  switch (s) {
+    case VECATTN_OK: return "ok";
+    case VECATTN_ERR_INVALID_ARG: return "invalid argument";
+    case VECATTN_ERR_UNSUPPORTED: return "unsupported";
+    case VECATTN_ERR_CAPACITY: return "capacity too small";
+    case VECATTN_ERR_DEVICE: return "device error";
+  }
+  return "unknown status";
+}
+
+vecattn_status vecattn_pool(const void* q, const vecattn_tdesc* qd, int32_t block, void* qp,
+                            const vecattn_tdesc* qpd, void* stream) {
+  vecattn_status st = check_desc(q, qd);
+  if (st != VECATTN_OK) return st;
+  if (block < 1) return VECATTN_ERR_INVALID_ARG;
+  st = check_desc(qp, qpd);
+  if (st != VECATTN_OK) return st;
+  if (qpd->B != qd->B || qpd->H != qd->H || qpd->D != qd->D || qpd->N != num_blocks(qd->N, block))
+    return VECATTN_ERR_INVALID_ARG;
+  hipError_t e = vecattn::launch_pool(to_tensor(q, qd), block, qp, qpd->sB, qpd->sH, qpd->sN,
+                                      static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
+}
+
+vecattn_status vecattn_select_max_count(int64_t N, int32_t block, int32_t causal, int32_t mode,
+                                        double param, int64_t* out) {
+  if (!out || N < 1 || N > kMaxN || block < 1 || !param_ok(mode, param))
+    return VECATTN_ERR_INVALID_ARG;
+  *out = max_count(N, block, causal, mode, param);
+  return VECATTN_OK;
+}
+
+vecattn_status vecattn_select_workspace_size(const vecattn_tdesc* qd, const vecattn_tdesc* kd,
+                                             int32_t block, int32_t causal, int32_t mode,
+                                             int64_t cap, size_t* bytes) {
+  (void)causal;
+  if (!qd || !kd || !bytes || block < 1 || cap < 1) return VECATTN_ERR_INVALID_ARG;
+  if (mode != VECATTN_SEL_TOPK && mode != VECATTN_SEL_TOPP && mode != VECATTN_SEL_MINS)
+    return VECATTN_ERR_INVALID_ARG;
+  *bytes = vecattn::select_workspace_bytes(qd->B, qd->H, qd->N, qd->D, block, mode, cap);
+  return VECATTN_OK;
+}
+
+vecattn_status vecattn_select(const void* q, const vecattn_tdesc* qd, const void* k,
+                              const vecattn_tdesc* kd, int32_t block, int32_t causal, int32_t mode,
+                              double param, int32_t* idx, int64_t cap, int32_t* counts,
+                              int32_t* n_clamped, void* workspace, size_t workspace_bytes,
+                              void* stream) {
+  vecattn_status st = check_desc(q, qd);
+  if (st != VECATTN_OK) return st;
+  st = check_desc(k, kd);
+  if (st != VECATTN_OK) return st;
+  if (kd->B != qd->B || kd->N != qd->N || kd->D != qd->D || qd->H % kd->H != 0)
+    return VECATTN_ERR_INVALID_ARG;
+  if (!idx || !counts || block < 1 || cap < 1 || cap > kMaxN) return VECATTN_ERR_INVALID_ARG;
+  if (mode != VECATTN_SEL_TOPK && mode != VECATTN_SEL_TOPP && mode != VECATTN_SEL_MINS)
+    return VECATTN_ERR_INVALID_ARG;
+  if (!param_ok(mode, param)) return VECATTN_ERR_INVALID_ARG;
+  if (mode == VECATTN_SEL_MINS) return VECATTN_ERR_UNSUPPORTED;
+  if (mode == VECATTN_SEL_TOPK && cap < max_count(qd->N, block, causal, mode, param))
+    return VECATTN_ERR_CAPACITY;
+  const size_t need = vecattn::select_workspace_bytes(qd->B, qd->H, qd->N, qd->D, block, mode, cap);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return VECATTN_ERR_CAPACITY;
+  if (workspace && !aligned16(workspace)) return VECATTN_ERR_INVALID_ARG;
+  vecattn::SelectArgs a{to_tensor(q, qd), to_tensor(k, kd), block, causal ? 1 : 0, mode, param,
+                        idx, cap, counts, n_clamped, workspace, workspace_bytes};
+  hipError_t e = vecattn::launch_select(a, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
+}
+
+vecattn_status vecattn_sparse_attn(const void* q, const vecattn_tdesc* qd, const void* k,
+                                   const vecattn_tdesc* kd, const void* v, const vecattn_tdesc* vd,
+                                   const int32_t* idx, int64_t cap, const int32_t* counts,
+                                   int32_t block, int32_t causal, float scale, void* o,
+                                   const vecattn_tdesc* od, float* lse, void* stream) {
+  vecattn_status st;
+  if ((st = check_desc(q, qd)) != VECATTN_OK) return st;
+  if ((st = check_desc(k, kd)) != VECATTN_OK) return st;
+  if ((st = check_desc(v, vd)) != VECATTN_OK) return st;
+  if ((st = check_desc(o, od)) != VECATTN_OK) return st;
+  if (kd->B != qd->B || kd->N != qd->N || kd->D != qd->D || qd->H % kd->H != 0)
+    return VECATTN_ERR_INVALID_ARG;
+  if (vd->B != kd->B || vd->H != kd->H || vd->N != kd->N || vd->D != kd->D)
+    return VECATTN_ERR_INVALID_ARG;
+  if (od->B != qd->B || od->H != qd->H || od->N != qd->N || od->D != qd->D)
+    return VECATTN_ERR_INVALID_ARG;
+  if (!idx || !counts || block < 1 || cap < 1 || cap > kMaxN) return VECATTN_ERR_INVALID_ARG;
+  if (!std::isfinite(scale) || scale < 0.0f) return VECATTN_ERR_INVALID_ARG;
+  vecattn::SparseAttnArgs a{to_tensor(q, qd), to_tensor(k, kd), to_tensor(v, vd),
+                            o, od->sB, od->sH, od->sN, lse, idx, counts, cap, block,
+                            causal ? 1 : 0, scale};
+  hipError_t e = vecattn::launch_sparse_attn(a, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
+}
+
+}  // extern "C"

@@ -1,0 +1,69 @@
+"""Parity rule for selected index sets (GPU vs oracle), shared by the GPU tests.
+
+Scores are the oracle's fp64 values of the estimated map (Sec. 3.1.1).  The
+GPU computes them from the same bf16 inputs with fp32 accumulation, so sets
+may differ only where two keys' scores are within 1e-5 * max|s| of the cut:
+  topK: equal counts; every key in the symmetric difference lies within the
+        tolerance of the oracle's k-th score.
+  topP: every key in the symmetric difference lies within the tolerance of
+        the oracle's cut score, or the oracle's cumulative mass at the cut is
+        within 1e-5 of p (then the counts differ by at most one); the GPU set's
+        oracle mass is >= p - 1e-5 unless the row was clamped to cap.
+Lists must be strictly ascending, in [0, L_i), and -1 padded.
+"""
+import numpy as np
+
+import oracle
+
+REL_TOL = 1e-5
+MASS_TOL = 1e-5
+
+
+def check_rows(q, k, block, mode, param, causal, cap, idx_gpu, cnt_gpu, rows):
+    """Returns the number of rows whose sets differ (all within the rule)."""
+    B, Hq, N, D = q.shape
+    Np = (N + block - 1) // block
+    idx_o, cnt_o, _ = oracle.select(q, k, block, mode, param, causal, cap, rows=rows)
+    idx_o = idx_o.reshape(-1, cap)
+    cnt_o = cnt_o.reshape(-1)
+    idx_gpu = idx_gpu.reshape(-1, idx_gpu.shape[-1])
+    cnt_gpu = cnt_gpu.reshape(-1)
+    mismatched = 0
+    for w in rows:
+        i, h, b = w % Np, (w // Np) % Hq, w // (Np * Hq)
+        s = oracle.pooled_scores(q, k, block, causal, b, h, i)
+        L = len(s)
+        tol = REL_TOL * np.abs(s).max()
+        cg, co = int(cnt_gpu[w]), int(cnt_o[w])
+        g = idx_gpu[w, :cg]
+        o = idx_o[w, :co]
+        assert 0 <= cg <= idx_gpu.shape[1], (w, cg)
+        assert np.all(np.diff(g) > 0), f"row {w}: not strictly ascending"
+        assert cg == 0 or (g[0] >= 0 and g[-1] < L), f"row {w}: index out of range"
+        assert np.all(idx_gpu[w, cg:] == -1), f"row {w}: padding"
+        diff = np.setxor1d(g, o)
+        if mode == oracle.TOPK or co == cap:   # topK, or a threshold row clamped to cap
+            assert cg == co, f"row {w}: count {cg} != {co}"
+            if diff.size:
+                vk = s[o].min()
+                assert np.all(np.abs(s[diff] - vk) <= tol), \
+                    f"row {w}: topK differs beyond near-tie: {np.abs(s[diff] - vk).max()}"
+                mismatched += 1
+        else:
+            if diff.size:
+                mismatched += 1
+                vcut = s[o].min()
+                e = np.exp(s - s.max())
+                Z = e.sum()
+                order = np.lexsort((np.arange(L), -s))
+                cum = np.cumsum(e[order]) / Z
+                mass_at_cut = cum[co - 1]
+                prev = cum[co - 2] if co >= 2 else 0.0
+                near_mass = abs(mass_at_cut - param) <= MASS_TOL or abs(prev - param) <= MASS_TOL
+                near_score = np.all(np.abs(s[diff] - vcut) <= tol)
+                assert near_score or (near_mass and abs(cg - co) <= 1), \
+                    f"row {w}: topP differs: counts {cg} vs {co}, gap {np.abs(s[diff] - vcut).max()}"
+            if cg < cap:
+                e = np.exp(s - s.max())
+                assert e[g].sum() / e.sum() >= param - MASS_TOL, f"row {w}: mass below p"
+    return mismatched

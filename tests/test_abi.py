@@ -1,0 +1,137 @@
+"""C-ABI contract of libvecattn on the host: the library loads, exports every
+entry point include/vecattn.h declares, and rejects bad arguments with the
+documented status before any launch (so no GPU is touched here: every call
+below fails validation).
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2603_29494_amd as va
+from paper_2603_29494_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "vecattn.h")
+
+OK, INVALID, UNSUPPORTED, CAPACITY = 0, 1, 2, 3
+FAKE = 0x100000   # 16-byte aligned address that validation rejects before any use
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(vecattn_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_entry_point():
+    lib = _lib.load()
+    names = declared_functions()
+    assert {"vecattn_select", "vecattn_sparse_attn", "vecattn_pool"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.vecattn_version() >= 100
+
+
+def test_status_strings():
+    for s, text in ((0, "ok"), (1, "invalid argument"), (2, "unsupported"), (3, "capacity"),
+                    (4, "device error")):
+        assert text in _lib.status_string(s)
+
+
+def test_max_count_matches_workloads():
+    assert va.max_count(1024, 64, False, "topk", 0.125) == 128
+    assert va.max_count(32768, 64, True, "topk", 0.10) == 3277
+    assert va.max_count(75600, 64, False, "topk", 0.15) == 11340
+    assert va.max_count(131072, 64, True, "topp", 0.95) == 131072
+    assert va.max_count(118800, 128, False, "topp", 0.9) == 118800
+    assert va.max_count(100, 64, True, "topp", 0.5) == 100        # last block ragged
+    with pytest.raises(va.VecattnError):
+        va.max_count(100, 64, False, "topk", 1.5)
+    with pytest.raises(va.VecattnError):
+        va.max_count(100, 0, False, "topk", 0.5)
+
+
+def desc(B, H, N, D, sN=None):
+    sN = D if sN is None else sN
+    return _lib.TDesc(B, H, N, D, H * N * sN, N * sN, sN)
+
+
+def attn(q=FAKE, qd=None, k=FAKE, kd=None, v=FAKE, vd=None, idx=FAKE, cap=16, cnt=FAKE, block=64,
+         causal=0, scale=0.0, o=FAKE, od=None):
+    lib = _lib.load()
+    qd = qd or desc(1, 4, 128, 128)
+    kd = kd or desc(1, 2, 128, 128)
+    vd = vd or desc(1, 2, 128, 128)
+    od = od or desc(1, 4, 128, 128)
+    return lib.vecattn_sparse_attn(q, ctypes.byref(qd), k, ctypes.byref(kd), v, ctypes.byref(vd),
+                                   idx, cap, cnt, block, causal, scale, o, ctypes.byref(od), None,
+                                   None)
+
+
+def test_sparse_attn_rejects_bad_arguments():
+    assert attn(q=None) == INVALID
+    assert attn(idx=None) == INVALID
+    assert attn(cnt=None) == INVALID
+    assert attn(block=0) == INVALID
+    assert attn(cap=0) == INVALID
+    assert attn(scale=-1.0) == INVALID
+    assert attn(scale=float("nan")) == INVALID
+    assert attn(q=FAKE + 2) == INVALID                                   # misaligned
+    assert attn(kd=desc(1, 3, 128, 128), vd=desc(1, 3, 128, 128)) == INVALID   # 4 % 3
+    assert attn(kd=desc(1, 2, 127, 128)) == INVALID                     # N mismatch
+    assert attn(vd=desc(1, 1, 128, 128)) == INVALID                     # v != k
+    assert attn(od=desc(1, 4, 128, 64)) == INVALID
+    assert attn(qd=desc(1, 4, 128, 128, sN=132)) == INVALID              # row not 16-B aligned
+    d96 = desc(1, 4, 128, 96)
+    assert attn(qd=d96, kd=desc(1, 2, 128, 96), vd=desc(1, 2, 128, 96), od=d96) == UNSUPPORTED
+
+
+def select(q=FAKE, qd=None, k=FAKE, kd=None, block=64, causal=0, mode=0, param=0.25, idx=FAKE,
+           cap=64, cnt=FAKE, ws=FAKE, ws_bytes=1 << 40):
+    lib = _lib.load()
+    qd = qd or desc(1, 4, 256, 128)
+    kd = kd or desc(1, 2, 256, 128)
+    return lib.vecattn_select(q, ctypes.byref(qd), k, ctypes.byref(kd), block, causal, mode, param,
+                              idx, cap, cnt, None, ws, ws_bytes, None)
+
+
+def test_select_rejects_bad_arguments():
+    assert select(q=None) == INVALID
+    assert select(k=None) == INVALID
+    assert select(idx=None) == INVALID
+    assert select(cnt=None) == INVALID
+    assert select(block=0) == INVALID
+    assert select(param=0.0) == INVALID
+    assert select(param=1.01) == INVALID
+    assert select(mode=1, param=-0.1) == INVALID
+    assert select(mode=7) == INVALID
+    assert select(kd=desc(1, 3, 256, 128)) == INVALID
+    assert select(kd=desc(1, 2, 255, 128)) == INVALID
+    assert select(mode=2, param=0.5) == UNSUPPORTED        # minS is not built
+    assert select(cap=63) == CAPACITY                      # topK 25% of 256 keys = 64
+    assert select(ws=None) == CAPACITY
+    assert select(ws_bytes=16) == CAPACITY
+    d64 = desc(1, 4, 256, 96)
+    assert select(qd=d64, kd=desc(1, 2, 256, 96)) == UNSUPPORTED
+
+
+def test_workspace_size_query():
+    qd, kd = desc(1, 40, 75600, 128), desc(1, 40, 75600, 128)
+    n = ctypes.c_size_t(0)
+    lib = _lib.load()
+    assert lib.vecattn_select_workspace_size(ctypes.byref(qd), ctypes.byref(kd), 64, 0, 0, 11340,
+                                             ctypes.byref(n)) == OK
+    assert n.value > 0
+    assert lib.vecattn_select_workspace_size(None, ctypes.byref(kd), 64, 0, 0, 11340,
+                                             ctypes.byref(n)) == INVALID
+
+
+def test_pool_rejects_bad_arguments():
+    lib = _lib.load()
+    qd, pd = desc(1, 2, 100, 64), desc(1, 2, 2, 64)
+    assert lib.vecattn_pool(None, ctypes.byref(qd), 64, FAKE, ctypes.byref(pd), None) == INVALID
+    assert lib.vecattn_pool(FAKE, ctypes.byref(qd), 0, FAKE, ctypes.byref(pd), None) == INVALID
+    bad = desc(1, 2, 3, 64)
+    assert lib.vecattn_pool(FAKE, ctypes.byref(qd), 64, FAKE, ctypes.byref(bad), None) == INVALID

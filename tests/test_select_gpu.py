@@ -1,0 +1,117 @@
+"""GPU parity of important-vector selection (Sec. 3.1: pooled-query scores,
+row-wise topK / topP) against the oracle, through the C ABI.  The index-set
+rule is in selection_parity.py."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2603_29494_amd as va
+from paper_2603_29494_amd import synth
+
+from selection_parity import check_rows
+
+pytestmark = pytest.mark.gpu
+
+
+def dev(bits):
+    return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def run(q, k, block, mode, param, causal, cap=None):
+    N = q.shape[2]
+    if cap is None:
+        cap = va.max_count(N, block, causal, "topk" if mode == oracle.TOPK else "topp", param)
+    ncl = torch.zeros(1, dtype=torch.int32, device="cuda")
+    idx, cnt = va.select(dev(q), dev(k), block, mode, param, causal, cap=cap, n_clamped=ncl)
+    torch.cuda.synchronize()
+    return idx.cpu().numpy(), cnt.cpu().numpy(), cap, int(ncl.item())
+
+
+def all_rows(q, block):
+    B, H, N, _ = q.shape
+    return list(range(B * H * ((N + block - 1) // block)))
+
+
+CASES = [
+    # B, Hq, Hkv, N, D, block, causal, mode, param
+    (1, 2, 2, 300, 128, 64, False, oracle.TOPK, 0.15),
+    (1, 4, 2, 333, 128, 64, True, oracle.TOPK, 0.1),
+    (2, 2, 1, 257, 64, 64, False, oracle.TOPK, 0.5),
+    (1, 3, 3, 520, 64, 16, True, oracle.TOPK, 0.3),
+    (1, 2, 2, 700, 128, 128, False, oracle.TOPP, 0.9),
+    (1, 4, 1, 450, 128, 64, True, oracle.TOPP, 0.95),
+    (1, 2, 2, 1000, 64, 48, False, oracle.TOPP, 0.5),
+    (1, 1, 1, 5000, 128, 64, False, oracle.TOPK, 0.15),
+    (1, 1, 1, 5000, 128, 64, True, oracle.TOPP, 0.9),
+]
+
+
+@pytest.mark.parametrize("case", CASES)
+def test_select_matches_oracle(gpu, case):
+    B, Hq, Hkv, N, D, block, causal, mode, param = case
+    q, k, _ = synth.planted_case(hash(case) % 10000, B, Hq, Hkv, N, D)
+    idx, cnt, cap, _ = run(q, k, block, mode, param, causal)
+    rows = all_rows(q, block)
+    mism = check_rows(q, k, block, mode, param, causal, cap, idx, cnt, rows)
+    assert mism <= max(1, len(rows) // 20)
+
+
+@pytest.mark.parametrize("mode,param", [(oracle.TOPK, 0.125), (oracle.TOPP, 0.9)])
+def test_plumbing_workload(gpu, mode, param):
+    layer = synth.make_layer(1)
+    w = layer.w
+    idx, cnt, cap, _ = run(layer.q, layer.k, w.block, mode, param, w.causal)
+    check_rows(layer.q, layer.k, w.block, mode, param, w.causal, cap, idx, cnt,
+               all_rows(layer.q, w.block))
+
+
+@pytest.mark.parametrize("mode,param", [(oracle.TOPK, 0.3), (oracle.TOPP, 0.5), (oracle.TOPP, 0.999)])
+def test_tie_storm_zero_queries(gpu, mode, param):
+    # Q = 0: every score is exactly 0; the kept keys are the lowest indices.
+    N, block = 3000, 64
+    q = np.zeros((1, 2, N, 128), dtype=np.uint16)
+    k = synth.random_bits(5, (1, 2, N, 128))
+    idx, cnt, cap, _ = run(q, k, block, mode, param, False)
+    idx_o, cnt_o, _ = oracle.select(q, k, block, mode, param, False, cap)
+    assert np.array_equal(cnt, cnt_o)
+    assert np.array_equal(idx, idx_o)
+
+
+def test_partial_ties_from_duplicate_keys(gpu):
+    # many identical key rows: ties at the cut, broken toward lower indices
+    N, block = 2048, 64
+    k = synth.random_bits(6, (1, 1, N, 128))
+    k[0, 0, 1::3] = k[0, 0, 0]
+    q = synth.random_bits(7, (1, 1, N, 128))
+    for mode, param in ((oracle.TOPK, 0.2), (oracle.TOPK, 0.4), (oracle.TOPP, 0.7)):
+        idx, cnt, cap, _ = run(q, k, block, mode, param, False)
+        check_rows(q, k, block, mode, param, False, cap, idx, cnt, all_rows(q, block))
+
+
+def test_threshold_clamped_to_cap(gpu):
+    q, k, _ = synth.planted_case(8, 1, 2, 2, 1500, 128, frac=0.02, logits=1.0)
+    cap = 200
+    idx, cnt, _, ncl = run(q, k, 64, oracle.TOPP, 0.95, False, cap=cap)
+    _, cnt_o, ncl_o = oracle.select(q, k, 64, oracle.TOPP, 0.95, False, cap)
+    assert ncl == ncl_o and ncl > 0
+    check_rows(q, k, 64, oracle.TOPP, 0.95, False, cap, idx, cnt, all_rows(q, 64))
+
+
+def test_full_keep(gpu):
+    q, k, _ = synth.planted_case(9, 1, 2, 1, 400, 64)
+    idx, cnt, cap, _ = run(q, k, 64, oracle.TOPK, 1.0, True)
+    for i in range(7):
+        L = min(400, (i + 1) * 64)
+        assert cnt[0, 0, i] == L and list(idx[0, 0, i, :L]) == list(range(L))
+
+
+def test_selection_then_attention_end_to_end(gpu):
+    q, k, v = synth.planted_case(10, 1, 4, 2, 640, 128)
+    idx, cnt, cap, _ = run(q, k, 64, oracle.TOPK, 0.2, True)
+    o = va.sparse_attn(dev(q), dev(k), dev(v), torch.from_numpy(idx).cuda(),
+                       torch.from_numpy(cnt).cuda(), 64, True)
+    torch.cuda.synchronize()
+    o_ref, _ = oracle.sparse_attn(q, k, v, idx, cnt, 64, True)
+    err = np.abs(o.float().cpu().numpy() - o_ref)
+    assert err.max() <= 2e-2 and err.mean() <= 2e-3

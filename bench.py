@@ -1,0 +1,196 @@
+"""Benchmark: one vertical-vector sparse attention layer (selection + sparse
+attention) on one MI355X at the 75k-token DiT shape.
+
+Workload (Wan-style 720p video DiT self-attention): latent grid 21x45x80 =
+75600 tokens, 40 heads, head_dim 128, bf16, non-causal, query block 64,
+topK keep ratio 15% (11340 keys per block).  Inputs are seeded synthetic
+tensors with planted vertical structure (paper_2603_29494_amd.synth, workload
+4); the paper's model activations are not available.
+
+A step = vecattn_select (pooling, scoring, topK) + vecattn_sparse_attn over all
+heads, inputs resident in HBM.  Prints one JSON line:
+  value  = dense-equivalent TFLOP/s = 4 * Hq * N^2 * D / (ms per layer)
+  ms_per_step = ms per layer
+  roofline   = the sparse-attention kernel (the dominant one): algorithmic
+               MFMA FLOPs on the gathered tiles per launch / its average
+               duration (HIP events on its stream) against 2516.6 TFLOP/s
+  cpu_baseline = the CPU oracle on a bounded sample of the same layer
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, HERE)
+
+PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 dense bf16 FLOP/clk/CU
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=4, help="synthetic workload id (1-5)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-blocks", type=int, default=0,
+                    help="query blocks in the CPU-oracle sample (0: sized for ~15 s)")
+    return ap.parse_args()
+
+
+def cpu_baseline(layer, sample_blocks):
+    """The oracle (selection + Eq. 4 attention, fp64) on a sample of query
+    blocks, all host threads.  Scaled to dense-equivalent TFLOP/s of the
+    sampled blocks."""
+    import oracle
+    w = layer.w
+    q, k, v = layer.q, layer.k, layer.v
+    B, Hq, N, D = q.shape
+    Np = w.num_blocks
+    nthreads = os.cpu_count() or 1
+    rng = np.random.Generator(np.random.PCG64(12345))
+    if sample_blocks <= 0:
+        sample_blocks = max(8, min(4 * nthreads, 256))
+    rows = np.sort(rng.choice(B * Hq * Np, size=sample_blocks, replace=False)).astype(np.int64)
+    mode = oracle.TOPK if w.mode == "topk" else oracle.TOPP
+    cap = oracle.topk_count(w.param, N) if w.mode == "topk" else N
+    t0 = time.perf_counter()
+    idx, cnt, _ = oracle.select(q, k, w.block, mode, w.param, w.causal, cap, rows=rows,
+                                nthreads=nthreads)
+    t1 = time.perf_counter()
+    oracle.sparse_attn(q, k, v, idx, cnt, w.block, w.causal, blocks=rows, nthreads=nthreads)
+    t2 = time.perf_counter()
+    nrows = 0
+    dense = 0.0
+    for r in rows:
+        i = int(r % Np)
+        n_i = min(N, (i + 1) * w.block) - i * w.block
+        keys = N if not w.causal else min(N, (i + 1) * w.block)
+        dense += 4.0 * n_i * keys * D
+        nrows += n_i
+    secs = t2 - t0
+    return {"value": dense / secs / 1e12, "unit": "TFLOP/s (dense-equivalent)", "cores": nthreads,
+            "kind": "oracle",
+            "sample": f"{sample_blocks} random query blocks of the same layer ({nrows} query rows); "
+                      f"select {t1 - t0:.2f} s + attention {t2 - t1:.2f} s",
+            "seconds": secs}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on exactly one GPU: the sparse-attention layer is sharded by head "
+              "across GPUs only by design (no multi-GPU path is built)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2603_29494_amd as va
+    from paper_2603_29494_amd import synth
+
+    va.load()  # fail loudly if the HIP library is missing
+    if not torch.cuda.is_available():
+        print("no GPU available", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    t_gen = time.perf_counter()
+    layer = synth.make_layer(args.workload)
+    w = layer.w
+    t_gen = time.perf_counter() - t_gen
+
+    def to_dev(bits):
+        return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(dev)
+
+    q, k, v = to_dev(layer.q), to_dev(layer.k), to_dev(layer.v)
+    B, Hq, N, D = q.shape
+    P = w.block
+    Np = (N + P - 1) // P
+    mode = w.mode
+    cap = va.max_count(N, P, w.causal, mode, w.param)
+    idx = torch.empty((B, Hq, Np, cap), dtype=torch.int32, device=dev)
+    counts = torch.empty((B, Hq, Np), dtype=torch.int32, device=dev)
+    ws = torch.empty(va.workspace_bytes(q, k, P, w.causal, mode, cap), dtype=torch.uint8, device=dev)
+    out = torch.empty_like(q)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        va.select(q, k, P, mode, w.param, w.causal, cap=cap, idx=idx, counts=counts, workspace=ws)
+        if ev is not None:
+            ev[1].record(stream)
+        va.sparse_attn(q, k, v, idx, counts, P, w.causal, out=out)
+        if ev is not None:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(events[s])
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    sel_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
+    attn_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
+    layer_ms = sel_ms + attn_ms
+
+    cnt = counts.cpu().numpy().astype(np.int64)
+    rows_per_block = np.minimum(N, (np.arange(Np) + 1) * P) - np.arange(Np) * P
+    pairs = float((cnt * rows_per_block[None, None, :]).sum())   # query rows x selected keys
+    f_alg = 4.0 * D * pairs                                        # QK^T + PV on gathered tiles
+    if w.causal:
+        f_dense = 2.0 * B * Hq * D * N * (N + 1)
+        L = np.minimum(N, (np.arange(Np) + 1) * P)
+    else:
+        f_dense = 4.0 * B * Hq * N * N * D
+        L = np.full(Np, N)
+    keep = float(cnt.sum()) / float(B * Hq * L.sum())
+    bytes_sel = 2.0 * B * N * D * (Hq + k.shape[1]) + 4.0 * cnt.sum() + 4.0 * B * Hq * Np
+    dense_tflops = f_dense / (layer_ms * 1e-3) / 1e12
+    attn_tflops = f_alg / (attn_ms * 1e-3) / 1e12
+
+    result = {
+        "metric": "ms/layer + dense-equiv TFLOP/s (MFMA-peak %) at 75k-token DiT shape",
+        "value": round(dense_tflops, 2),
+        "unit": "TFLOP/s (dense-equivalent)",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(layer_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": B, "q_heads": Hq, "kv_heads": int(k.shape[1]),
+                   "seq_len": N, "head_dim": D, "causal": bool(w.causal), "query_block": P,
+                   "selection": f"{mode} {w.param}"},
+        "ms_select": round(sel_ms, 4),
+        "ms_attention": round(attn_ms, 4),
+        "selection_pct": round(100.0 * sel_ms / layer_ms, 2),
+        "wall_ms_per_step": round(wall_ms, 4),
+        "attention_mfma_pct": round(100.0 * attn_tflops / PEAK_BF16_TFLOPS, 2),
+        "selection_hbm_pct": round(100.0 * bytes_sel / (sel_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 2),
+        "achieved_keep": round(keep, 6),
+        "roofline": {"bound": "mfma", "kernel": "k_sparse_attn<128>",
+                     "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None},
+        "input_generation_s": round(t_gen, 1),
+    }
+    if not args.no_cpu_baseline:
+        cb = cpu_baseline(layer, args.cpu_sample_blocks)
+        result["cpu_baseline"] = {k2: (round(v2, 6) if isinstance(v2, float) else v2)
+                                  for k2, v2 in cb.items()}
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

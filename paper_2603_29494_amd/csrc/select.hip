@@ -44,22 +44,19 @@ enum Mode : int { MODE_HIST = 0, MODE_COLLECT = 1, MODE_EMIT = 2 };
 
 struct RowState {
   int phase;
-  int level;        // histogram level the next HIST pass runs (interval = levels < level)
+  int level;        // histogram level the next HIST pass runs
   int topp;         // 1: cut by mass, 0: cut by rank
   int k_target;     // topK: number of keys to keep
-  int k_rem;        // topK: rank of the cut inside the interval (1 = highest)
   int L;            // eligible keys
   int tie_partial;  // 1: only the first k_eq keys tied at t* are kept
   int k_eq;         // keys tied at t* that are kept
   int count;        // final count
   int clamped;      // 1 if the threshold selection was clamped to cap
-  int pad0, pad1;
-  float lo[kLevels];
-  float inv[kLevels];
-  int ba[kLevels];
-  int bb[kLevels];
-  float tstar;
-  float pad2;
+  int pad0;
+  float s_lo, s_hi; // current interval: keys with s_lo <= s <= s_hi (exact float bounds)
+  float blo, binv;  // bin function of the current level: floor((s - blo) * binv)
+  float tstar;      // cut score
+  float pad1;
   double ref;       // softmax reference (an upper bound of the row's scores)
   double Z;         // total mass (topP)
   double pZ;        // p * Z
@@ -90,6 +87,8 @@ struct SelParams {
   int mode_topp;
   double param;
   float tau;
+  int64_t items;    // score-pass work items
+  int64_t per_xcd;  // work items per XCD
 };
 
 __device__ __forceinline__ uint32_t ord_key(float f) {
@@ -119,26 +118,37 @@ __device__ __forceinline__ double mass_term(float s, double ref) {
 }
 
 // Bin of s at one level (must be evaluated identically everywhere).
+// Clamped in float before the conversion (out-of-range conversions are
+// undefined); truncation equals floor on the clamped, non-negative value.
 __device__ __forceinline__ int bin_of(float s, float lo, float inv) {
-  const float x = (s - lo) * inv;
-  int b = static_cast<int>(floorf(x));
-  return min(max(b, 0), kBins - 1);
+  const float x = fminf(fmaxf((s - lo) * inv, 0.0f), static_cast<float>(kBins - 1));
+  return static_cast<int>(x);
 }
 
-// Position of score s relative to the interval of `nlev` levels:
-// +1 above, -1 below, 0 inside; *bin = its bin at level nlev when inside.
-struct RowInterval {
-  float lo[kLevels], inv[kLevels];
-  int ba[kLevels], bb[kLevels];
-  int nlev;
-};
-__device__ __forceinline__ int classify(float s, const RowInterval& I) {
-  for (int l = 0; l < I.nlev; ++l) {
-    const int b = bin_of(s, I.lo[l], I.inv[l]);
-    if (b > I.bb[l]) return 1;
-    if (b < I.ba[l]) return -1;
+// The interval after choosing bins [ba, bb] of the level with bin function
+// (lo, inv) inside [s_lo, s_hi]: the bin function is monotone in s, so the
+// chosen set is again a float interval; its exact ends are found by binary
+// search over ordered float keys with the same bin function the passes use.
+__device__ __forceinline__ void narrow(float& s_lo, float& s_hi, float lo, float inv, int ba, int bb) {
+  // smallest s with bin >= ba
+  uint32_t a = ord_key(-FLT_MAX), z = ord_key(FLT_MAX);
+  if (bin_of(ord_val(a), lo, inv) < ba) {
+    while (z - a > 1) {
+      const uint32_t m = a + (z - a) / 2;
+      if (bin_of(ord_val(m), lo, inv) >= ba) z = m; else a = m;
+    }
+    s_lo = fmaxf(s_lo, ord_val(z));
   }
-  return 0;
+  // largest s with bin <= bb
+  a = ord_key(-FLT_MAX);
+  z = ord_key(FLT_MAX);
+  if (bin_of(ord_val(z), lo, inv) > bb) {
+    while (z - a > 1) {
+      const uint32_t m = a + (z - a) / 2;
+      if (bin_of(ord_val(m), lo, inv) <= bb) a = m; else z = m;
+    }
+    s_hi = fminf(s_hi, ord_val(a));
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -164,11 +174,10 @@ __global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
   const float cc = c * 1.0009765625f + 1e-30f;
   s.level = 0;
   s.phase = PH_HIST;
-  s.lo[0] = -cc;
-  s.inv[0] = static_cast<float>(kBins) / (2.0f * cc);
-  s.ba[0] = 0;
-  s.bb[0] = kBins - 1;
-  s.k_rem = s.k_target;
+  s.s_lo = -FLT_MAX;
+  s.s_hi = FLT_MAX;
+  s.blo = -cc;
+  s.binv = static_cast<float>(kBins) / (2.0f * cc);
   s.ref = static_cast<double>(cc);
   s.tie_partial = 0;
   s.k_eq = 0;
@@ -203,55 +212,53 @@ __global__ __launch_bounds__(256) void k_kmax_init(float* kmax, int n) {
 __global__ __launch_bounds__(256) void k_kmax(const uint16_t* __restrict__ k, int64_t sB, int64_t sH,
                                               int64_t sN, int Hkv, int N, int D,
                                               float* __restrict__ kmax) {
-  // one wave per 64 key rows; lane = row
+  // 16 lanes read one key row (16 B each, D = 128; 8 lanes for D = 64), so a
+  // wave reads 4 (8) whole rows per instruction; 16 rows per thread group.
   const int bh = blockIdx.y;
   const int b = bh / Hkv, h = bh % Hkv;
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  float nrm = 0.0f;
-  if (j < N) {
-    const uint16_t* row = k + b * sB + h * sH + static_cast<int64_t>(j) * sN;
+  const int lpr = D / 8;                       // lanes per row
+  const int rpw = 256 / lpr;                   // rows per block pass
+  const int c = threadIdx.x % lpr;
+  float best = 0.0f;
+  for (int j = blockIdx.x * rpw * 16 + threadIdx.x / lpr; j < min(N, (blockIdx.x + 1) * rpw * 16);
+       j += rpw) {
+    const u32x4 w = *reinterpret_cast<const u32x4*>(k + b * sB + h * sH + static_cast<int64_t>(j) * sN + 8 * c);
     float acc = 0.0f;
-    for (int d = 0; d < D; d += 8) {
-      const u32x4 w = *reinterpret_cast<const u32x4*>(row + d);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float a = bf16_bits_to_f32(w[e] & 0xFFFFu), c = bf16_bits_to_f32(w[e] >> 16);
-        acc = __builtin_fmaf(a, a, acc);
-        acc = __builtin_fmaf(c, c, acc);
-      }
+    for (int e = 0; e < 4; ++e) {
+      const float x0 = bf16_bits_to_f32(w[e] & 0xFFFFu), x1 = bf16_bits_to_f32(w[e] >> 16);
+      acc = __builtin_fmaf(x0, x0, acc);
+      acc = __builtin_fmaf(x1, x1, acc);
     }
-    nrm = sqrtf(acc);
+    for (int o = 1; o < lpr; o <<= 1) acc += __shfl_xor(acc, o);
+    best = fmaxf(best, sqrtf(acc));
   }
-  for (int o = 32; o > 0; o >>= 1) nrm = fmaxf(nrm, __shfl_xor(nrm, o));
-  if ((threadIdx.x & 63) == 0) atomicMax(reinterpret_cast<unsigned int*>(kmax + bh), __float_as_uint(nrm));
+  for (int o = 32; o > 0; o >>= 1) best = fmaxf(best, __shfl_xor(best, o));
+  if ((threadIdx.x & 63) == 0) atomicMax(reinterpret_cast<unsigned int*>(kmax + bh), __float_as_uint(best));
 }
 
 // ---------------------------------------------------------------------------
-// The scoring pass.
+// The scoring pass.  Work items are ordered (head, split, row tile) with the
+// row tile fastest and handed out XCD by XCD, so the row tiles of one head
+// that read the same key split run together on one XCD and share its L2.
 // ---------------------------------------------------------------------------
 template <int D, int MODE>
 __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   constexpr int DS = D / 16;
   constexpr int HS = kBins + 1;  // odd row stride: rows hitting the same bin use different banks
   __shared__ uint32_t s_hist[(MODE == MODE_HIST) ? kRowsWG * HS : 1];
-  __shared__ int s_part[kRowsWG];
-  __shared__ RowInterval s_iv[kRowsWG];
-  __shared__ float s_tstar[kRowsWG];
-  __shared__ int s_L[kRowsWG];
-  __shared__ int s_tie[kRowsWG];
-  __shared__ double s_ref[kRowsWG];
-  __shared__ int s_lev0[kRowsWG];
   __shared__ double s_zred[4][kRowsWG];
   __shared__ double s_mred[4][kRowsWG];
   __shared__ uint32_t s_nred[4][kRowsWG];
+  __shared__ int s_part[kRowsWG];
   __shared__ int s_any;
 
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63, g = lane >> 5, ln = lane & 31;
-  // grid: x = split, y = row block, z = bh
-  const int sp = blockIdx.x;
-  const int rb = blockIdx.y;
-  const int64_t bh = blockIdx.z;
+  const int64_t item = xcd_work_item(p.per_xcd);
+  if (item >= p.items) return;
+  const int rb = static_cast<int>(item % p.nrb);
+  const int64_t rest = item / p.nrb;
+  const int sp = static_cast<int>(rest % p.nsplit);
+  const int64_t bh = rest / p.nsplit;
   const int b = static_cast<int>(bh / p.Hq), h = static_cast<int>(bh % p.Hq);
   const int hk = h / p.group;
   const int i0 = rb * kRowsWG;
@@ -262,32 +269,15 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   const int key1 = min(key0 + p.split, Ltile);
   const int64_t row0 = bh * p.Np + i0;
 
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63, g = lane >> 5, ln = lane & 31;
   if (tid == 0) s_any = 0;
   __syncthreads();
   if (tid < kRowsWG) {
     int part = 0;
     if (tid < nrows) {
-      const RowState& s = p.st[row0 + tid];
-      if (MODE == MODE_HIST) part = (s.phase == PH_HIST);
-      else if (MODE == MODE_COLLECT) part = (s.phase == PH_COLLECT);
-      else part = (s.phase == PH_DONE);
-      if (part) {
-        RowInterval iv;
-        iv.nlev = (MODE == MODE_EMIT) ? 0 : s.level;
-        for (int l = 0; l < kLevels; ++l) {
-          iv.lo[l] = s.lo[l];
-          iv.inv[l] = s.inv[l];
-          iv.ba[l] = s.ba[l];
-          iv.bb[l] = s.bb[l];
-        }
-        s_iv[tid] = iv;
-        s_tstar[tid] = s.tstar;
-        s_L[tid] = s.L;
-        s_tie[tid] = s.tie_partial;
-        s_ref[tid] = s.topp ? s.ref : 0.0;
-        s_lev0[tid] = (s.level == 0);
-        if (!s.topp) s_ref[tid] = -1.0;  // marker: no masses needed
-      }
+      const int ph = p.st[row0 + tid].phase;
+      part = (MODE == MODE_HIST) ? ph == PH_HIST : (MODE == MODE_COLLECT) ? ph == PH_COLLECT : ph == PH_DONE;
     }
     s_part[tid] = part;
     if (part) atomicOr(&s_any, 1);
@@ -297,22 +287,37 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   __syncthreads();
   if (!s_any) return;
 
-  // Pooled queries as the B operand: lane -> row ln of row block rb2, head-dim
-  // slots 16s + 8g .. +7.
+  // This lane's two rows (rl = 32 * rb2 + ln): pooled query as the B operand
+  // (head-dim slots 16s + 8g .. +7) and the row's interval in registers.
   bf16x8 qf[2][DS];
+  bool part[2];
+  int Lr[2];
+  float slo[2], shi[2], blo[2], binv[2], ts[2];
+  bool tiep[2], lev0[2];
+  double ref[2];  // < 0: no masses needed
 #pragma unroll
   for (int rb2 = 0; rb2 < 2; ++rb2) {
-    const int rr = rb2 * 32 + ln;
-    const bool have = rr < nrows;
-    const u32x4* src = reinterpret_cast<const u32x4*>(p.qp + (row0 + (have ? rr : 0)) * D);
+    const int rl = rb2 * 32 + ln;
+    part[rb2] = rl < nrows && s_part[rl];
+    const int64_t row = row0 + (rl < nrows ? rl : 0);
+    const RowState& s = p.st[row];
+    Lr[rb2] = s.L;
+    slo[rb2] = s.s_lo;
+    shi[rb2] = s.s_hi;
+    blo[rb2] = s.blo;
+    binv[rb2] = s.binv;
+    ts[rb2] = s.tstar;
+    tiep[rb2] = s.tie_partial;
+    lev0[rb2] = s.level == 0;
+    ref[rb2] = s.topp ? s.ref : -1.0;
+    const u32x4* src = reinterpret_cast<const u32x4*>(p.qp + row * D);
 #pragma unroll
     for (int s2 = 0; s2 < DS; ++s2) {
-      const u32x4 t = have ? src[2 * s2 + g] : u32x4{0, 0, 0, 0};
+      const u32x4 t = rl < nrows ? src[2 * s2 + g] : u32x4{0, 0, 0, 0};
       qf[rb2][s2] = __builtin_bit_cast(bf16x8, t);
     }
   }
 
-  // Per-lane row state for the two rows this lane owns (rb2 = 0, 1).
   double zacc[2] = {0.0, 0.0}, macc[2] = {0.0, 0.0};
   uint32_t nacc[2] = {0u, 0u};
 
@@ -327,63 +332,57 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     for (int s2 = 0; s2 < DS; ++s2) ka[s2] = ksrc[2 * s2 + g];
 #pragma unroll
     for (int rb2 = 0; rb2 < 2; ++rb2) {
-      const int rl = rb2 * 32 + ln;  // local row
       f32x16 acc = f32x16{};
 #pragma unroll
       for (int s2 = 0; s2 < DS; ++s2)
         acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ka[s2]),
                                                       qf[rb2][s2], acc, 0, 0, 0);
-      const bool part = rl < nrows && s_part[rl];
-      if (!part) continue;
-      const int L = s_L[rl];
+      if (!part[rb2]) continue;
+      const int lim = Lr[rb2] - kb;  // keys kl < lim are eligible
       if (MODE == MODE_EMIT) {
-        const float ts = s_tstar[rl];
-        const bool tiep = s_tie[rl];
         uint32_t wsel = 0u, wtie = 0u;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
           const float sc = acc[e] * p.tau;
-          const bool ok = kb + kl < L;
-          if (ok && sc > ts) wsel |= 1u << kl;
-          if (ok && sc == ts) wtie |= 1u << kl;
+          const bool ok = kl < lim;
+          wsel |= (ok && sc > ts[rb2]) ? 1u << kl : 0u;
+          wtie |= (ok && sc == ts[rb2]) ? 1u << kl : 0u;
         }
         wsel |= __shfl_xor(wsel, 32);
         wtie |= __shfl_xor(wtie, 32);
-        if (!tiep) wsel |= wtie;
+        if (!tiep[rb2]) wsel |= wtie;
         if (g == 0) {
-          const int64_t row = row0 + rl;
+          const int64_t row = row0 + rb2 * 32 + ln;
           p.bsel[row * p.W + kb / 32] = wsel;
-          if (tiep) p.btie[row * p.W + kb / 32] = wtie;
+          if (tiep[rb2]) p.btie[row * p.W + kb / 32] = wtie;
         }
         continue;
       }
-      const RowInterval& iv = s_iv[rl];
-      const double ref = s_ref[rl];
-      const bool lev0 = s_lev0[rl];
+      const int rl = rb2 * 32 + ln;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int key = kb + 8 * (e >> 2) + 4 * g + (e & 3);
-        if (key >= L) continue;
+        const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+        if (kl >= lim) continue;
         const float sc = acc[e] * p.tau;
-        const int cls = classify(sc, iv);
-        if (ref >= 0.0) {
-          const double mt = mass_term(sc, ref);
-          if (MODE == MODE_HIST && lev0) zacc[rb2] += mt;
-          if (cls > 0) macc[rb2] += mt;
+        const bool above = sc > shi[rb2];
+        const bool inside = !above && sc >= slo[rb2];
+        if (ref[rb2] >= 0.0) {
+          const double mt = mass_term(sc, ref[rb2]);
+          if (MODE == MODE_HIST && lev0[rb2]) zacc[rb2] += mt;
+          if (above) macc[rb2] += mt;
         }
-        if (cls > 0) {
-          nacc[rb2] += 1u;
-        } else if (cls == 0) {
+        nacc[rb2] += above ? 1u : 0u;
+        if (inside) {
           if (MODE == MODE_HIST) {
-            const int bn = bin_of(sc, iv.lo[iv.nlev], iv.inv[iv.nlev]);
-            atomicAdd(&s_hist[rl * HS + bn], 1u);
+            atomicAdd(&s_hist[rl * HS + bin_of(sc, blo[rb2], binv[rb2])], 1u);
           } else {  // collect
             const int64_t row = row0 + rl;
             const uint32_t pos = atomicAdd(&p.cand_n[row], 1u);
             const uint32_t ok = ord_key(sc);
             if (pos < kCand)
-              p.cand[row * kCand + pos] = (static_cast<uint64_t>(ok) << 32) | (~static_cast<uint32_t>(key));
+              p.cand[row * kCand + pos] =
+                  (static_cast<uint64_t>(ok) << 32) | (~static_cast<uint32_t>(kb + kl));
             atomicMin(&p.cand_lohi[2 * row], ok);
             atomicMax(&p.cand_lohi[2 * row + 1], ok);
           }
@@ -393,13 +392,13 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   }
   if (MODE == MODE_EMIT) return;
 
-  // Reduce per-row partials: lanes (ln, g=0/1) of each wave, then the 4 waves
-  // in a fixed order (deterministic sums).
+  // Reduce per-row partials: lanes (ln, g = 0 / 1) of each wave, then the 4
+  // waves in a fixed order (deterministic sums).
 #pragma unroll
   for (int rb2 = 0; rb2 < 2; ++rb2) {
-    double z = zacc[rb2] + __shfl_xor(zacc[rb2], 32);
-    double m = macc[rb2] + __shfl_xor(macc[rb2], 32);
-    uint32_t n = nacc[rb2] + __shfl_xor(nacc[rb2], 32);
+    const double z = zacc[rb2] + __shfl_xor(zacc[rb2], 32);
+    const double m = macc[rb2] + __shfl_xor(macc[rb2], 32);
+    const uint32_t n = nacc[rb2] + __shfl_xor(nacc[rb2], 32);
     if (g == 0) {
       s_zred[wave][rb2 * 32 + ln] = z;
       s_mred[wave][rb2 * 32 + ln] = m;
@@ -414,7 +413,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     const uint32_t n = s_nred[0][tid] + s_nred[1][tid] + s_nred[2][tid] + s_nred[3][tid];
     p.n_above[row * p.nsplit + sp] = n;
     p.m_above[row * p.nsplit + sp] = m;
-    if (MODE == MODE_HIST && s_lev0[tid]) p.zpart[row * p.nsplit + sp] = z;
+    if (MODE == MODE_HIST && p.st[row].level == 0) p.zpart[row * p.nsplit + sp] = z;
   }
   if (MODE == MODE_HIST) {
     for (int t = tid; t < nrows * kBins; t += kThreads) {
@@ -459,7 +458,7 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
     s.Z = z;
     s.pZ = p.param * z;
   }
-  const float lo = s.lo[level], inv = s.inv[level];
+  const float lo = s.blo, inv = s.binv;
   int ba = -1, bb = -1;
   uint32_t above_bins = 0;  // keys in bins above bb (inside the interval)
   if (!s.topp) {
@@ -480,7 +479,6 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
       for (int bn = kBins - 1; bn > ba; --bn) cum += hs[bn];
     }
     above_bins = cum;
-    s.k_rem = k_rem - static_cast<int>(above_bins);
   } else {
     // Mass bounds per bin from its score range; the cut bin range is every bin
     // the true cut may lie in.
@@ -514,20 +512,18 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
   }
   uint32_t inside = 0;
   for (int bn = ba; bn <= bb; ++bn) inside += hs[bn];
-  s.ba[level] = ba;
-  s.bb[level] = bb;
+  (void)above_bins;
+  // New interval: the chosen bins of this level, as exact float bounds.
+  narrow(s.s_lo, s.s_hi, lo, inv, ba, bb);
   const int nl = level + 1;
+  s.level = nl;
   if (inside <= static_cast<uint32_t>(kCand) || nl >= kLevels) {
-    s.level = nl;
     s.phase = PH_COLLECT;
   } else {
     const float nlo = lo + static_cast<float>(ba) / inv;
     const float nhi = lo + static_cast<float>(bb + 1) / inv;
-    s.lo[nl] = nlo;
-    s.inv[nl] = static_cast<float>(kBins) / fmaxf(nhi - nlo, FLT_MIN);
-    s.ba[nl] = 0;
-    s.bb[nl] = kBins - 1;
-    s.level = nl;
+    s.blo = nlo;
+    s.binv = static_cast<float>(kBins) / fmaxf(nhi - nlo, FLT_MIN);
   }
 }
 
@@ -757,16 +753,13 @@ Layout layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t D, int32_t 
 }
 
 int choose_split(int64_t B, int64_t Hq, int64_t N, int32_t P) {
-  // Enough workgroups to fill the chip a few times over, splits of at least
-  // 2048 keys (multiples of 128).
-  const int64_t Np = (N + P - 1) / P;
-  const int64_t tiles = B * Hq * ((Np + kRowsWG - 1) / kRowsWG);
-  int64_t want = (tiles * N) / 4096;  // target ~4096 workgroups
-  if (want < 2048) want = 2048;
-  int64_t s = 2048;
-  while (s < want && s < 65536) s <<= 1;
-  if (s > N) s = ((N + 127) / 128) * 128;
-  return static_cast<int>(s);
+  // 4096 keys (1 MB of K at D = 128): the ~64 workgroups resident on an XCD
+  // cover a few splits of one head, whose K then fits the XCD's 4 MB L2.
+  (void)B;
+  (void)Hq;
+  (void)P;
+  const int64_t s = 4096;
+  return static_cast<int>(N < s ? ((N + 127) / 128) * 128 : s);
 }
 
 }  // namespace
@@ -835,14 +828,16 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
                      p.qp, rows, static_cast<int>(D), p.qnorm);
   hipLaunchKernelGGL(k_kmax_init, dim3(static_cast<unsigned>((B * Hkv + 255) / 256)), dim3(256), 0,
                      stream, p.kmax, static_cast<int>(B * Hkv));
-  hipLaunchKernelGGL(k_kmax, dim3(static_cast<unsigned>((N + 255) / 256), static_cast<unsigned>(B * Hkv)),
+  const int kmax_rows = (256 / (static_cast<int>(D) / 8)) * 16;
+  hipLaunchKernelGGL(k_kmax, dim3(static_cast<unsigned>((N + kmax_rows - 1) / kmax_rows), static_cast<unsigned>(B * Hkv)),
                      dim3(256), 0, stream, p.k, a.k.sB, a.k.sH, a.k.sN, static_cast<int>(Hkv),
                      static_cast<int>(N), static_cast<int>(D), p.kmax);
   const int64_t nh = rows * kBins;
   hipLaunchKernelGGL(k_zero_u32, dim3(static_cast<unsigned>((nh + 255) / 256)), dim3(256), 0, stream,
                      p.hist, nh);
-  const dim3 pgrid(static_cast<unsigned>(p.nsplit), static_cast<unsigned>(p.nrb),
-                   static_cast<unsigned>(B * Hq));
+  p.items = B * Hq * static_cast<int64_t>(p.nsplit) * p.nrb;
+  p.per_xcd = (p.items + 7) / 8;
+  const dim3 pgrid(static_cast<unsigned>(p.per_xcd * 8));
   const dim3 rgrid(static_cast<unsigned>(rows));
   const dim3 igrid(static_cast<unsigned>((rows + 255) / 256));
   for (int round = 0; round < kRounds; ++round) {

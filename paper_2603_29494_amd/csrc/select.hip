@@ -39,7 +39,7 @@ constexpr int kLevels = 4;      // histogram refinements per round
 constexpr int kCand = 1024;     // candidate capacity per row
 constexpr int kRounds = 2;      // a topP row whose count exceeds cap reruns as topK(cap)
 
-enum Phase : int { PH_IDLE = 0, PH_HIST = 1, PH_COLLECT = 2, PH_DONE = 3 };
+enum Phase : int { PH_IDLE = 0, PH_HIST = 1, PH_COLLECT = 2, PH_DONE = 3, PH_EMIT = 4 };
 enum Mode : int { MODE_HIST = 0, MODE_COLLECT = 1, MODE_EMIT = 2 };
 
 struct RowState {
@@ -209,32 +209,49 @@ __global__ __launch_bounds__(256) void k_kmax_init(float* kmax, int n) {
   if (t < n) kmax[t] = 0.0f;
 }
 
+constexpr int kKmaxRows = 1024;  // key rows per workgroup of the key-norm kernel
+
 __global__ __launch_bounds__(256) void k_kmax(const uint16_t* __restrict__ k, int64_t sB, int64_t sH,
                                               int64_t sN, int Hkv, int N, int D,
                                               float* __restrict__ kmax) {
-  // 16 lanes read one key row (16 B each, D = 128; 8 lanes for D = 64), so a
-  // wave reads 4 (8) whole rows per instruction; 16 rows per thread group.
+  // D / 8 lanes read one key row (16 B each); the workgroup steps over
+  // kKmaxRows rows, four row groups per step, and issues one atomic.
+  __shared__ float s_red[4];
   const int bh = blockIdx.y;
   const int b = bh / Hkv, h = bh % Hkv;
-  const int lpr = D / 8;                       // lanes per row
-  const int rpw = 256 / lpr;                   // rows per block pass
-  const int c = threadIdx.x % lpr;
+  const int lpr = D / 8;
+  const int rpi = 256 / lpr;
+  const int j0 = blockIdx.x * kKmaxRows + threadIdx.x / lpr;
+  const int j1 = min(N, static_cast<int>(blockIdx.x + 1) * kKmaxRows);
+  const uint16_t* base = k + b * sB + h * sH + 8 * (threadIdx.x % lpr);
   float best = 0.0f;
-  for (int j = blockIdx.x * rpw * 16 + threadIdx.x / lpr; j < min(N, (blockIdx.x + 1) * rpw * 16);
-       j += rpw) {
-    const u32x4 w = *reinterpret_cast<const u32x4*>(k + b * sB + h * sH + static_cast<int64_t>(j) * sN + 8 * c);
-    float acc = 0.0f;
+  for (int j = j0; j < j1; j += 4 * rpi) {
+    u32x4 w[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float x0 = bf16_bits_to_f32(w[e] & 0xFFFFu), x1 = bf16_bits_to_f32(w[e] >> 16);
-      acc = __builtin_fmaf(x0, x0, acc);
-      acc = __builtin_fmaf(x1, x1, acc);
+    for (int u = 0; u < 4; ++u) {
+      const int jj = min(j + u * rpi, j1 - 1);
+      w[u] = *reinterpret_cast<const u32x4*>(base + static_cast<int64_t>(jj) * sN);
     }
-    for (int o = 1; o < lpr; o <<= 1) acc += __shfl_xor(acc, o);
-    best = fmaxf(best, sqrtf(acc));
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      float acc = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float x0 = bf16_bits_to_f32(w[u][e] & 0xFFFFu), x1 = bf16_bits_to_f32(w[u][e] >> 16);
+        acc = __builtin_fmaf(x0, x0, acc);
+        acc = __builtin_fmaf(x1, x1, acc);
+      }
+      for (int o = 1; o < lpr; o <<= 1) acc += __shfl_xor(acc, o);
+      best = fmaxf(best, acc);  // rows past j1 repeat row j1 - 1
+    }
   }
   for (int o = 32; o > 0; o >>= 1) best = fmaxf(best, __shfl_xor(best, o));
-  if ((threadIdx.x & 63) == 0) atomicMax(reinterpret_cast<unsigned int*>(kmax + bh), __float_as_uint(best));
+  if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = best;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const float m = sqrtf(fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3])));
+    atomicMax(reinterpret_cast<unsigned int*>(kmax + bh), __float_as_uint(m));
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -277,7 +294,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     int part = 0;
     if (tid < nrows) {
       const int ph = p.st[row0 + tid].phase;
-      part = (MODE == MODE_HIST) ? ph == PH_HIST : (MODE == MODE_COLLECT) ? ph == PH_COLLECT : ph == PH_DONE;
+      part = (MODE == MODE_HIST) ? ph == PH_HIST : (MODE == MODE_COLLECT) ? ph == PH_COLLECT : ph == PH_EMIT;
     }
     s_part[tid] = part;
     if (part) atomicOr(&s_any, 1);
@@ -323,13 +340,17 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
 
   const uint16_t* kh = p.k + b * p.k_sB + hk * p.k_sH;
   const int nblk = (key1 - key0 + 31) / 32;
-  for (int blk = wave; blk < nblk; blk += 4) {
-    const int kb = key0 + blk * 32;
-    const int kr = min(kb + ln, p.N - 1);
+  // K of a 32-key block as the A operand (lane -> key ln, head-dim slots
+  // 16s + 8g .. +7); the next block of this wave is loaded while the current
+  // one is processed (addresses are clamped, so loads past the end are safe).
+  auto kload = [&](u32x4 (&dst)[DS], int blk) __attribute__((always_inline)) {
+    const int kr = min(key0 + blk * 32 + ln, p.N - 1);
     const u32x4* ksrc = reinterpret_cast<const u32x4*>(kh + static_cast<int64_t>(kr) * p.k_sN);
-    u32x4 ka[DS];
 #pragma unroll
-    for (int s2 = 0; s2 < DS; ++s2) ka[s2] = ksrc[2 * s2 + g];
+    for (int s2 = 0; s2 < DS; ++s2) dst[s2] = ksrc[2 * s2 + g];
+  };
+  auto kproc = [&](const u32x4 (&ka)[DS], int blk) __attribute__((always_inline)) {
+    const int kb = key0 + blk * 32;
 #pragma unroll
     for (int rb2 = 0; rb2 < 2; ++rb2) {
       f32x16 acc = f32x16{};
@@ -339,6 +360,18 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
                                                       qf[rb2][s2], acc, 0, 0, 0);
       if (!part[rb2]) continue;
       const int lim = Lr[rb2] - kb;  // keys kl < lim are eligible
+      if (MODE == MODE_COLLECT) {
+        // Kept-key bitmask for this block: every key at or above the interval's
+        // lower bound; the resolve step clears the candidates it rejects.
+        uint32_t w = 0u;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+          w |= (kl < lim && acc[e] * p.tau >= slo[rb2]) ? 1u << kl : 0u;
+        }
+        w |= __shfl_xor(w, 32);
+        if (g == 0) p.bsel[(row0 + rb2 * 32 + ln) * p.W + kb / 32] = w;
+      }
       if (MODE == MODE_EMIT) {
         uint32_t wsel = 0u, wtie = 0u;
 #pragma unroll
@@ -389,6 +422,15 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
         }
       }
     }
+  };
+  u32x4 k0[DS], k1[DS];
+  kload(k0, wave);
+  for (int blk = wave; blk < nblk; blk += 8) {
+    kload(k1, blk + 4);
+    kproc(k0, blk);
+    if (blk + 4 >= nblk) break;
+    kload(k0, blk + 8);
+    kproc(k1, blk + 4);
   }
   if (MODE == MODE_EMIT) return;
 
@@ -614,7 +656,20 @@ __global__ __launch_bounds__(256) void k_resolve_cand(SelParams p) {
         s.clamped = 1;
       }
     }
-    if (s.phase == PH_COLLECT) {
+    res[1] = -1;  // no candidate bits to clear unless set below
+    if (s.phase == PH_COLLECT && !overflow) {
+      // The collect pass set a bit for every key at or above the interval;
+      // keep the first n_sel candidates (score desc, index asc), clear the rest.
+      n_sel = min(max(n_sel, 0), nc);
+      res[1] = n_sel;
+      s.tie_partial = 0;
+      s.k_eq = 0;
+      s.tstar = n_sel > 0 ? ord_val(static_cast<uint32_t>(key[n_sel - 1] >> 32)) : FLT_MAX;
+      s.count = count;
+      s.phase = PH_DONE;
+      if (s.clamped && p.n_clamped) atomicAdd(p.n_clamped, 1);
+    }
+    if (s.phase == PH_COLLECT) {  // too many candidates to store: the emit pass redoes the row
       n_sel = max(n_sel, 0);
       if (overflow && all_tied) {
         s.tstar = ord_val(p.cand_lohi[2 * r]);
@@ -642,8 +697,16 @@ __global__ __launch_bounds__(256) void k_resolve_cand(SelParams p) {
         s.k_eq = kept_ties;
       }
       s.count = count;
-      s.phase = PH_DONE;
+      s.phase = PH_EMIT;
       if (s.clamped && p.n_clamped) atomicAdd(p.n_clamped, 1);
+    }
+  }
+  __syncthreads();
+  const int keep = res[1];
+  if (keep >= 0) {
+    for (int t = keep + tid; t < nc; t += 256) {
+      const uint32_t j = ~static_cast<uint32_t>(key[t] & 0xFFFFFFFFull);
+      atomicAnd(&p.bsel[r * p.W + j / 32], ~(1u << (j % 32)));
     }
   }
 }
@@ -828,8 +891,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
                      p.qp, rows, static_cast<int>(D), p.qnorm);
   hipLaunchKernelGGL(k_kmax_init, dim3(static_cast<unsigned>((B * Hkv + 255) / 256)), dim3(256), 0,
                      stream, p.kmax, static_cast<int>(B * Hkv));
-  const int kmax_rows = (256 / (static_cast<int>(D) / 8)) * 16;
-  hipLaunchKernelGGL(k_kmax, dim3(static_cast<unsigned>((N + kmax_rows - 1) / kmax_rows), static_cast<unsigned>(B * Hkv)),
+  hipLaunchKernelGGL(k_kmax, dim3(static_cast<unsigned>((N + kKmaxRows - 1) / kKmaxRows), static_cast<unsigned>(B * Hkv)),
                      dim3(256), 0, stream, p.k, a.k.sB, a.k.sH, a.k.sN, static_cast<int>(Hkv),
                      static_cast<int>(N), static_cast<int>(D), p.kmax);
   const int64_t nh = rows * kBins;

@@ -47,12 +47,14 @@ __host__ __device__ __forceinline__ constexpr int swz(int r) {
   else return ((r & 3) << 1) | ((r >> 2) & 1);
 }
 
-// 16-byte global -> LDS copy per lane (LDS destination: wave-uniform base +
-// 16 * lane).  The 16-byte form exists only on gfx950; the host pass of the
-// compiler rejects it, so the call is compiled for the device side only.
-__device__ __forceinline__ void gather16_to_lds(const void* src, void* lds_base) {
+// 16-byte copy per lane from a buffer (byte offset voff) to LDS (destination:
+// wave-uniform base + 16 * lane).  The 16-byte form exists only on gfx950;
+// the host pass of the compiler rejects it, so it is compiled for the device
+// side only.
+__device__ __forceinline__ void gather16_to_lds(__amdgpu_buffer_rsrc_t rsrc, uint32_t voff,
+                                                void* lds_base) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  __builtin_amdgcn_global_load_lds(src, LDS_PTR(void, lds_base), 16, 0, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, LDS_PTR(void, lds_base), 16, voff, 0, 0, 0);
 #endif
 }
 
@@ -104,18 +106,27 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
 
   const int row0 = i * P + chunk * kRows;
   const int row_end = min(N, min(i * P + P, row0 + kRows));
-  const int count = static_cast<int>(min<int64_t>(max(counts[bh * Np + i], 0), cap));
+  const int count = __builtin_amdgcn_readfirstlane(
+      static_cast<int>(min<int64_t>(max(counts[bh * Np + i], 0), cap)));
   const int32_t* list = idx + (bh * Np + i) * cap;
   const int ntiles = (count + kTile - 1) / kTile;
   // Reads of the list past `count` return 0 (buffer range check).
   const __amdgpu_buffer_rsrc_t lrs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(list), 0, count * 4, 0x00020000);
 
+  // K and V of this head as buffer resources: gathers use 32-bit byte offsets
+  // (row * row_bytes + 16 * chunk; the host checks that a head spans < 2 GiB).
   const uint16_t* kh = k + b * k_sB + hk * k_sH;
   const uint16_t* vh = v + b * v_sB + hk * v_sH;
+  const uint32_t k_rowb = static_cast<uint32_t>(k_sN) * 2u;
+  const uint32_t v_rowb = static_cast<uint32_t>(v_sN) * 2u;
+  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(kh), 0, static_cast<int>((N - 1) * k_rowb + RB), 0x00020000);
+  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(vh), 0, static_cast<int>((N - 1) * v_rowb + RB), 0x00020000);
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
   const int g = lane >> 5;
   const int ln = lane & 31;
@@ -157,11 +168,11 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
   auto issue_tile = [&](int t, int st) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t r = min(max(nid[u], 0), N - 1);  // memory safety only
+      const uint32_t r = static_cast<uint32_t>(min(max(nid[u], 0), N - 1));  // memory safety only
       uint16_t* kd = kbuf(st) + (wave * U + u) * 64 * 8;
       uint16_t* vd = vbuf(st) + (wave * U + u) * 64 * 8;
-      gather16_to_lds(kh + r * k_sN + 8 * gcol(u), kd);
-      gather16_to_lds(vh + r * v_sN + 8 * gcol(u), vd);
+      gather16_to_lds(krs, __umul24(r, k_rowb) + 16u * gcol(u), kd);
+      gather16_to_lds(vrs, __umul24(r, v_rowb) + 16u * gcol(u), vd);
     }
     if (wave == 0)  // the tile's key ids (clamped to the list; entries past count are masked)
       __builtin_amdgcn_global_load_lds(list + min(t * kTile + lane, count - 1),
@@ -188,6 +199,9 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
   const int vhalf = (lane >> 4) & 1;
 
   auto step = [&](const int t, const int st) __attribute__((always_inline)) {
+    // Tile t has landed, and the ids of tile t+1 (issued right after it) too;
+    // the barrier (no fence: all LDS traffic here is waited for explicitly)
+    // also guarantees every wave is done reading the other stage.
     // Tile t has landed, and the ids of tile t+1 (issued right after it) too;
     // the barrier (no fence: all LDS traffic here is waited for explicitly)
     // also guarantees every wave is done reading the other stage.
@@ -226,30 +240,39 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
         }
       }
     }
-    float tmax = kNegInf;
+    // Lazy rescaling: x = s * scale - m_run (log2 units) is what exp2 needs
+    // anyway; the reference m_run of a row moves only when some x exceeds 8
+    // (so P stays <= 256, harmless in bf16 / fp32), and O, l are rescaled
+    // only when some row of the wave moved.  m_run = -inf (nothing seen yet)
+    // takes the same slow path.
+    float x[16];
 #pragma unroll
-    for (int e = 0; e < 16; e += 2) tmax = fmaxf(tmax, fmaxf(sacc[e], sacc[e + 1]));
-    tmax = wave_max_xor32(tmax);
-
-    // Lazy rescaling: the reference max moves only when a row's max exceeds it
-    // by more than 8 (log2 units; P stays <= 256, harmless in bf16/fp32); O and
-    // l are rescaled only when some row of the wave moved.
-    const float m_new = fmaxf(m_run, tmax * scale_log2);
-    const bool move = m_new > m_run + 8.0f;
-    if (__any(move)) {
-      const float m_ref = move ? m_new : m_run;
+    for (int e = 0; e < 16; ++e) x[e] = __builtin_fmaf(sacc[e], scale_log2, -m_run);
+    float xmax = x[0];
+#pragma unroll
+    for (int e = 1; e < 16; e += 2) xmax = fmaxf(xmax, fmaxf(x[e], x[e + 1]));
+    xmax = wave_max_xor32(xmax);
+    if (__any(!(xmax <= 8.0f))) {
+      float tmax = kNegInf;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, sacc[e]);
+      tmax = wave_max_xor32(tmax);
+      const float m_new = fmaxf(m_run, tmax * scale_log2);
+      const float m_ref = (m_new > m_run + 8.0f) ? m_new : m_run;
       const float alpha = __builtin_amdgcn_exp2f(m_run - (m_ref == kNegInf ? 0.0f : m_ref));
       l_run *= alpha;
 #pragma unroll
       for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
       m_run = m_ref;
+      const float m_sub = m_run == kNegInf ? 0.0f : m_run;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) x[e] = __builtin_fmaf(sacc[e], scale_log2, -m_sub);
     }
-    const float m_sub = m_run == kNegInf ? 0.0f : m_run;
     float psum = 0.0f;
     f32x8 pf[2];
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[e], scale_log2, -m_sub));
+      const float p = __builtin_amdgcn_exp2f(x[e]);
       psum += p;
       pf[e >> 3][e & 7] = p;
     }

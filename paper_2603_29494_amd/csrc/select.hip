@@ -40,7 +40,8 @@ constexpr int kCand = 1024;     // candidate capacity per row
 constexpr int kRounds = 2;      // a topP row whose count exceeds cap reruns as topK(cap)
 
 enum Phase : int { PH_IDLE = 0, PH_HIST = 1, PH_COLLECT = 2, PH_DONE = 3, PH_EMIT = 4 };
-enum Mode : int { MODE_HIST = 0, MODE_COLLECT = 1, MODE_EMIT = 2 };
+// MODE_HIST0: first histogram level (the interval is everything).
+enum Mode : int { MODE_HIST = 0, MODE_COLLECT = 1, MODE_EMIT = 2, MODE_HIST0 = 3 };
 
 struct RowState {
   int phase;
@@ -53,10 +54,12 @@ struct RowState {
   int count;        // final count
   int clamped;      // 1 if the threshold selection was clamped to cap
   int pad0;
+  // Scores below are raw fp32 dot products <q_p, k_j> (the softmax scale tau
+  // > 0 preserves their order; it enters only the topP masses).
   float s_lo, s_hi; // current interval: keys with s_lo <= s <= s_hi (exact float bounds)
-  float blo, binv;  // bin function of the current level: floor((s - blo) * binv)
+  float blo, binv;  // bin range of the current level: lo and bins per unit
+  float badd;       // bin of s: floor(fma(s, binv, badd)), badd = -blo * binv
   float tstar;      // cut score
-  float pad1;
   double ref;       // softmax reference (an upper bound of the row's scores)
   double Z;         // total mass (topP)
   double pZ;        // p * Z
@@ -108,44 +111,48 @@ __device__ __forceinline__ int topk_count(double r, int L) {
   return min(max(k, 1), L);
 }
 
-// exp(s - ref) for topP masses: exp2 in fp32 while the exponent is in range
-// (relative error ~1e-7), with an exact power-of-two rescale below it.
-__device__ __forceinline__ double mass_term(float s, double ref) {
-  const double y = (static_cast<double>(s) - ref) * 1.4426950408889634;
+// exp(tau * s - ref) for topP masses (s a raw score): exp2 in fp32 while the
+// exponent is in range (relative error ~1e-7), with an exact power-of-two
+// rescale below it.
+__device__ __forceinline__ double mass_term(float s, float tau, double ref) {
+  const double y = (static_cast<double>(s) * static_cast<double>(tau) - ref) * 1.4426950408889634;
   if (y > -120.0) return static_cast<double>(__builtin_amdgcn_exp2f(static_cast<float>(y)));
   const double n = floor(y);
   return ldexp(static_cast<double>(__builtin_amdgcn_exp2f(static_cast<float>(y - n))), static_cast<int>(n));
 }
 
-// Bin of s at one level (must be evaluated identically everywhere).
-// Clamped in float before the conversion (out-of-range conversions are
-// undefined); truncation equals floor on the clamped, non-negative value.
-__device__ __forceinline__ int bin_of(float s, float lo, float inv) {
-  const float x = fminf(fmaxf((s - lo) * inv, 0.0f), static_cast<float>(kBins - 1));
+// Bin of s at one level (must be evaluated identically everywhere: the
+// scoring passes and the interval search below use this one function).
+// One fma, clamped to [0, kBins - 1] in float before the conversion
+// (out-of-range conversions are undefined); truncation equals floor on the
+// clamped, non-negative value.
+__device__ __forceinline__ int bin_of(float s, float mul, float add) {
+  const float x = __builtin_amdgcn_fmed3f(__builtin_fmaf(s, mul, add), 0.0f,
+                                          static_cast<float>(kBins - 1));
   return static_cast<int>(x);
 }
 
 // The interval after choosing bins [ba, bb] of the level with bin function
-// (lo, inv) inside [s_lo, s_hi]: the bin function is monotone in s, so the
+// (mul, add) inside [s_lo, s_hi]: the bin function is monotone in s, so the
 // chosen set is again a float interval; its exact ends are found by binary
 // search over ordered float keys with the same bin function the passes use.
-__device__ __forceinline__ void narrow(float& s_lo, float& s_hi, float lo, float inv, int ba, int bb) {
+__device__ __forceinline__ void narrow(float& s_lo, float& s_hi, float mul, float add, int ba, int bb) {
   // smallest s with bin >= ba
   uint32_t a = ord_key(-FLT_MAX), z = ord_key(FLT_MAX);
-  if (bin_of(ord_val(a), lo, inv) < ba) {
+  if (bin_of(ord_val(a), mul, add) < ba) {
     while (z - a > 1) {
       const uint32_t m = a + (z - a) / 2;
-      if (bin_of(ord_val(m), lo, inv) >= ba) z = m; else a = m;
+      if (bin_of(ord_val(m), mul, add) >= ba) z = m; else a = m;
     }
     s_lo = fmaxf(s_lo, ord_val(z));
   }
   // largest s with bin <= bb
   a = ord_key(-FLT_MAX);
   z = ord_key(FLT_MAX);
-  if (bin_of(ord_val(z), lo, inv) > bb) {
+  if (bin_of(ord_val(z), mul, add) > bb) {
     while (z - a > 1) {
       const uint32_t m = a + (z - a) / 2;
-      if (bin_of(ord_val(m), lo, inv) <= bb) a = m; else z = m;
+      if (bin_of(ord_val(m), mul, add) <= bb) a = m; else z = m;
     }
     s_hi = fminf(s_hi, ord_val(a));
   }
@@ -153,7 +160,7 @@ __device__ __forceinline__ void narrow(float& s_lo, float& s_hi, float lo, float
 
 // ---------------------------------------------------------------------------
 // Per-row setup: eligible keys, targets, first interval [-c, c] with
-// c >= tau * |q_p| * max |k| (Cauchy-Schwarz, padded for fp32 rounding).
+// c >= |q_p| * max |k| (Cauchy-Schwarz, padded for fp32 rounding).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
   const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -170,7 +177,7 @@ __global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
     s.topp = p.mode_topp;
     if (!p.mode_topp) s.k_target = topk_count(p.param, s.L);
   }
-  const float c = p.tau * p.qnorm[r] * p.kmax[b * p.Hkv + h / p.group];
+  const float c = p.qnorm[r] * p.kmax[b * p.Hkv + h / p.group];
   const float cc = c * 1.0009765625f + 1e-30f;
   s.level = 0;
   s.phase = PH_HIST;
@@ -178,7 +185,8 @@ __global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
   s.s_hi = FLT_MAX;
   s.blo = -cc;
   s.binv = static_cast<float>(kBins) / (2.0f * cc);
-  s.ref = static_cast<double>(cc);
+  s.badd = -s.blo * s.binv;
+  s.ref = static_cast<double>(p.tau) * static_cast<double>(cc);  // >= every tau * score
   s.tie_partial = 0;
   s.k_eq = 0;
   p.cand_n[r] = 0;
@@ -259,11 +267,17 @@ __global__ __launch_bounds__(256) void k_kmax(const uint16_t* __restrict__ k, in
 // row tile fastest and handed out XCD by XCD, so the row tiles of one head
 // that read the same key split run together on one XCD and share its L2.
 // ---------------------------------------------------------------------------
-template <int D, int MODE>
+// TOPP: the launch selects by mass (rows restarted as topK(cap) may be mixed
+// in); otherwise no mass is computed.
+template <int D, int MODE, bool TOPP>
 __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   constexpr int DS = D / 16;
-  constexpr int HS = kBins + 1;  // odd row stride: rows hitting the same bin use different banks
-  __shared__ uint32_t s_hist[(MODE == MODE_HIST) ? kRowsWG * HS : 1];
+  constexpr bool HIST = MODE == MODE_HIST || MODE == MODE_HIST0;
+  // Row stride kBins + 1 (odd): rows hitting the same bin use different
+  // banks; slot kBins of a row takes the increments of keys outside the
+  // interval, so that every key can be counted without a branch.
+  constexpr int HS = kBins + 1;
+  __shared__ uint32_t s_hist[HIST ? kRowsWG * HS : 1];
   __shared__ double s_zred[4][kRowsWG];
   __shared__ double s_mred[4][kRowsWG];
   __shared__ uint32_t s_nred[4][kRowsWG];
@@ -294,12 +308,12 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     int part = 0;
     if (tid < nrows) {
       const int ph = p.st[row0 + tid].phase;
-      part = (MODE == MODE_HIST) ? ph == PH_HIST : (MODE == MODE_COLLECT) ? ph == PH_COLLECT : ph == PH_EMIT;
+      part = HIST ? ph == PH_HIST : (MODE == MODE_COLLECT) ? ph == PH_COLLECT : ph == PH_EMIT;
     }
     s_part[tid] = part;
     if (part) atomicOr(&s_any, 1);
   }
-  if (MODE == MODE_HIST)
+  if (HIST)
     for (int t = tid; t < kRowsWG * HS; t += kThreads) s_hist[t] = 0u;
   __syncthreads();
   if (!s_any) return;
@@ -309,8 +323,8 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   bf16x8 qf[2][DS];
   bool part[2];
   int Lr[2];
-  float slo[2], shi[2], blo[2], binv[2], ts[2];
-  bool tiep[2], lev0[2];
+  float slo[2], shi[2], bmul[2], badd[2], ts[2];
+  bool tiep[2];
   double ref[2];  // < 0: no masses needed
 #pragma unroll
   for (int rb2 = 0; rb2 < 2; ++rb2) {
@@ -321,12 +335,11 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     Lr[rb2] = s.L;
     slo[rb2] = s.s_lo;
     shi[rb2] = s.s_hi;
-    blo[rb2] = s.blo;
-    binv[rb2] = s.binv;
+    bmul[rb2] = s.binv;
+    badd[rb2] = s.badd;
     ts[rb2] = s.tstar;
     tiep[rb2] = s.tie_partial;
-    lev0[rb2] = s.level == 0;
-    ref[rb2] = s.topp ? s.ref : -1.0;
+    ref[rb2] = (TOPP && s.topp) ? s.ref : -1.0;
     const u32x4* src = reinterpret_cast<const u32x4*>(p.qp + row * D);
 #pragma unroll
     for (int s2 = 0; s2 < DS; ++s2) {
@@ -353,6 +366,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     const int kb = key0 + blk * 32;
 #pragma unroll
     for (int rb2 = 0; rb2 < 2; ++rb2) {
+      // Raw scores s = <q_p, k> of keys kl = 8 (e / 4) + 4 g + e % 4 of the block.
       f32x16 acc = f32x16{};
 #pragma unroll
       for (int s2 = 0; s2 < DS; ++s2)
@@ -360,6 +374,10 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
                                                       qf[rb2][s2], acc, 0, 0, 0);
       if (!part[rb2]) continue;
       const int lim = Lr[rb2] - kb;  // keys kl < lim are eligible
+      // Whole block eligible for every row of the wave (all blocks but the
+      // last, unless causal): no per-key test.
+      const bool full = !__any(lim < 32);
+      auto elig = [&](int kl) __attribute__((always_inline)) { return full || kl < lim; };
       if (MODE == MODE_COLLECT) {
         // Kept-key bitmask for this block: every key at or above the interval's
         // lower bound; the resolve step clears the candidates it rejects.
@@ -367,7 +385,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
-          w |= (kl < lim && acc[e] * p.tau >= slo[rb2]) ? 1u << kl : 0u;
+          w |= (elig(kl) && acc[e] >= slo[rb2]) ? 1u << kl : 0u;
         }
         w |= __shfl_xor(w, 32);
         if (g == 0) p.bsel[(row0 + rb2 * 32 + ln) * p.W + kb / 32] = w;
@@ -377,10 +395,9 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
-          const float sc = acc[e] * p.tau;
-          const bool ok = kl < lim;
-          wsel |= (ok && sc > ts[rb2]) ? 1u << kl : 0u;
-          wtie |= (ok && sc == ts[rb2]) ? 1u << kl : 0u;
+          const bool ok = elig(kl);
+          wsel |= (ok && acc[e] > ts[rb2]) ? 1u << kl : 0u;
+          wtie |= (ok && acc[e] == ts[rb2]) ? 1u << kl : 0u;
         }
         wsel |= __shfl_xor(wsel, 32);
         wtie |= __shfl_xor(wtie, 32);
@@ -393,32 +410,43 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
         continue;
       }
       const int rl = rb2 * 32 + ln;
+      uint32_t inside_mask = 0u;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
-        if (kl >= lim) continue;
-        const float sc = acc[e] * p.tau;
-        const bool above = sc > shi[rb2];
-        const bool inside = !above && sc >= slo[rb2];
-        if (ref[rb2] >= 0.0) {
-          const double mt = mass_term(sc, ref[rb2]);
-          if (MODE == MODE_HIST && lev0[rb2]) zacc[rb2] += mt;
+        const float sc = acc[e];
+        const bool ok = elig(kl);
+        bool above = false, inside = ok;
+        if (MODE != MODE_HIST0) {  // level 0: the interval is everything
+          above = ok && sc > shi[rb2];
+          inside = ok && !above && sc >= slo[rb2];
+          nacc[rb2] += above ? 1u : 0u;
+        }
+        if (TOPP && ref[rb2] >= 0.0 && ok) {
+          const double mt = mass_term(sc, p.tau, ref[rb2]);
+          if (MODE == MODE_HIST0) zacc[rb2] += mt;
           if (above) macc[rb2] += mt;
         }
-        nacc[rb2] += above ? 1u : 0u;
-        if (inside) {
-          if (MODE == MODE_HIST) {
-            atomicAdd(&s_hist[rl * HS + bin_of(sc, blo[rb2], binv[rb2])], 1u);
-          } else {  // collect
-            const int64_t row = row0 + rl;
-            const uint32_t pos = atomicAdd(&p.cand_n[row], 1u);
-            const uint32_t ok = ord_key(sc);
-            if (pos < kCand)
-              p.cand[row * kCand + pos] =
-                  (static_cast<uint64_t>(ok) << 32) | (~static_cast<uint32_t>(kb + kl));
-            atomicMin(&p.cand_lohi[2 * row], ok);
-            atomicMax(&p.cand_lohi[2 * row + 1], ok);
-          }
+        if (HIST) {
+          const int bn = inside ? bin_of(sc, bmul[rb2], badd[rb2]) : kBins;
+          atomicAdd(&s_hist[rl * HS + bn], 1u);
+        } else {
+          inside_mask |= inside ? 1u << e : 0u;
+        }
+      }
+      if (MODE == MODE_COLLECT && inside_mask) {  // candidates (a narrow interval: few)
+        const int64_t row = row0 + rl;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          if (!((inside_mask >> e) & 1u)) continue;
+          const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+          const uint32_t pos = atomicAdd(&p.cand_n[row], 1u);
+          const uint32_t ok = ord_key(acc[e]);
+          if (pos < kCand)
+            p.cand[row * kCand + pos] =
+                (static_cast<uint64_t>(ok) << 32) | (~static_cast<uint32_t>(kb + kl));
+          atomicMin(&p.cand_lohi[2 * row], ok);
+          atomicMax(&p.cand_lohi[2 * row + 1], ok);
         }
       }
     }
@@ -455,9 +483,9 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     const uint32_t n = s_nred[0][tid] + s_nred[1][tid] + s_nred[2][tid] + s_nred[3][tid];
     p.n_above[row * p.nsplit + sp] = n;
     p.m_above[row * p.nsplit + sp] = m;
-    if (MODE == MODE_HIST && p.st[row].level == 0) p.zpart[row * p.nsplit + sp] = z;
+    if (MODE == MODE_HIST0) p.zpart[row * p.nsplit + sp] = z;
   }
-  if (MODE == MODE_HIST) {
+  if (HIST) {
     for (int t = tid; t < nrows * kBins; t += kThreads) {
       const int rl = t / kBins, bn = t % kBins;
       const uint32_t c = s_hist[rl * HS + bn];
@@ -500,7 +528,8 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
     s.Z = z;
     s.pZ = p.param * z;
   }
-  const float lo = s.blo, inv = s.binv;
+  const float lo = s.blo, inv = s.binv, add = s.badd;
+  const float top = static_cast<float>(s.ref / static_cast<double>(p.tau));  // raw score bound
   int ba = -1, bb = -1;
   uint32_t above_bins = 0;  // keys in bins above bb (inside the interval)
   if (!s.topp) {
@@ -535,9 +564,9 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
       float e_lo = lo + static_cast<float>(bn) * w - slop;
       float e_hi = lo + static_cast<float>(bn + 1) * w + slop;
       if (level == 0 && bn == 0) e_lo = -FLT_MAX;
-      if (level == 0 && bn == kBins - 1) e_hi = static_cast<float>(s.ref);
-      const double mlo = hs[bn] * mass_term(e_lo, s.ref);
-      const double mhi = hs[bn] * mass_term(fminf(e_hi, static_cast<float>(s.ref)), s.ref);
+      if (level == 0 && bn == kBins - 1) e_hi = top;
+      const double mlo = hs[bn] * mass_term(e_lo, p.tau, s.ref);
+      const double mhi = hs[bn] * mass_term(fminf(e_hi, top), p.tau, s.ref);
       const bool may_before_lt = before_lo < T;          // true mass before bn may be < T
       const bool may_through_ge = before_hi + mhi >= T;  // true mass through bn may be >= T
       if (may_before_lt && may_through_ge) {
@@ -556,7 +585,7 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
   for (int bn = ba; bn <= bb; ++bn) inside += hs[bn];
   (void)above_bins;
   // New interval: the chosen bins of this level, as exact float bounds.
-  narrow(s.s_lo, s.s_hi, lo, inv, ba, bb);
+  narrow(s.s_lo, s.s_hi, inv, add, ba, bb);
   const int nl = level + 1;
   s.level = nl;
   if (inside <= static_cast<uint32_t>(kCand) || nl >= kLevels) {
@@ -566,6 +595,7 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
     const float nhi = lo + static_cast<float>(bb + 1) / inv;
     s.blo = nlo;
     s.binv = static_cast<float>(kBins) / fmaxf(nhi - nlo, FLT_MIN);
+    s.badd = -nlo * s.binv;
   }
 }
 
@@ -627,14 +657,14 @@ __global__ __launch_bounds__(256) void k_resolve_cand(SelParams p) {
     } else {
       const double T = s.pZ - mab;
       if (overflow && all_tied) {
-        const double term = mass_term(ord_val(p.cand_lohi[2 * r]), s.ref);
+        const double term = mass_term(ord_val(p.cand_lohi[2 * r]), p.tau, s.ref);
         double need = T > 0.0 ? ceil(T / term) : 1.0;
         n_sel = static_cast<int>(fmin(fmax(need, 1.0), static_cast<double>(nc_raw)));
       } else {
         double c = 0.0;
         n_sel = nc;
         for (int t = 0; t < nc; ++t) {
-          c += mass_term(ord_val(static_cast<uint32_t>(key[t] >> 32)), s.ref);
+          c += mass_term(ord_val(static_cast<uint32_t>(key[t] >> 32)), p.tau, s.ref);
           if (c >= T) { n_sel = t + 1; break; }
         }
         if (T <= 0.0) n_sel = 1;
@@ -835,6 +865,17 @@ size_t select_workspace_bytes(int64_t B, int64_t Hq, int64_t N, int64_t D, int32
   return layout(B, Hq, Hq, N, D, block, choose_split(B, Hq, N, block)).total;
 }
 
+template <int MODE>
+void score_pass(int64_t D, bool topp, dim3 grid, const SelParams& p, hipStream_t stream) {
+  if (D == 128) {
+    if (topp) hipLaunchKernelGGL((k_score_pass<128, MODE, true>), grid, dim3(kThreads), 0, stream, p);
+    else hipLaunchKernelGGL((k_score_pass<128, MODE, false>), grid, dim3(kThreads), 0, stream, p);
+  } else {
+    if (topp) hipLaunchKernelGGL((k_score_pass<64, MODE, true>), grid, dim3(kThreads), 0, stream, p);
+    else hipLaunchKernelGGL((k_score_pass<64, MODE, false>), grid, dim3(kThreads), 0, stream, p);
+  }
+}
+
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   const int64_t B = a.q.B, Hq = a.q.H, Hkv = a.k.H, N = a.q.N, D = a.q.D;
   const int32_t P = a.block;
@@ -905,16 +946,14 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   for (int round = 0; round < kRounds; ++round) {
     hipLaunchKernelGGL(k_sel_init, igrid, dim3(256), 0, stream, p, round);
     for (int lv = 0; lv < kLevels; ++lv) {
-      if (D == 128) hipLaunchKernelGGL((k_score_pass<128, MODE_HIST>), pgrid, dim3(kThreads), 0, stream, p);
-      else hipLaunchKernelGGL((k_score_pass<64, MODE_HIST>), pgrid, dim3(kThreads), 0, stream, p);
+      if (lv == 0) score_pass<MODE_HIST0>(D, p.mode_topp != 0, pgrid, p, stream);
+      else score_pass<MODE_HIST>(D, p.mode_topp != 0, pgrid, p, stream);
       hipLaunchKernelGGL(k_resolve_hist, rgrid, dim3(64), 0, stream, p, lv);
     }
-    if (D == 128) hipLaunchKernelGGL((k_score_pass<128, MODE_COLLECT>), pgrid, dim3(kThreads), 0, stream, p);
-    else hipLaunchKernelGGL((k_score_pass<64, MODE_COLLECT>), pgrid, dim3(kThreads), 0, stream, p);
+    score_pass<MODE_COLLECT>(D, p.mode_topp != 0, pgrid, p, stream);
     hipLaunchKernelGGL(k_resolve_cand, rgrid, dim3(256), 0, stream, p);
   }
-  if (D == 128) hipLaunchKernelGGL((k_score_pass<128, MODE_EMIT>), pgrid, dim3(kThreads), 0, stream, p);
-  else hipLaunchKernelGGL((k_score_pass<64, MODE_EMIT>), pgrid, dim3(kThreads), 0, stream, p);
+  score_pass<MODE_EMIT>(D, p.mode_topp != 0, pgrid, p, stream);
   hipLaunchKernelGGL(k_compact, rgrid, dim3(64), 0, stream, p);
   return hipGetLastError();
 }

@@ -41,7 +41,9 @@ constexpr int kRounds = 2;      // a topP row whose count exceeds cap reruns as 
 
 enum Phase : int { PH_IDLE = 0, PH_HIST = 1, PH_COLLECT = 2, PH_DONE = 3, PH_EMIT = 4 };
 // MODE_HIST0: first histogram level (the interval is everything).
-enum Mode : int { MODE_HIST = 0, MODE_COLLECT = 1, MODE_EMIT = 2, MODE_HIST0 = 3 };
+// MODE_SAMPLE: moments of the scores of every kSampleStride-th key block.
+enum Mode : int { MODE_HIST = 0, MODE_COLLECT = 1, MODE_EMIT = 2, MODE_HIST0 = 3, MODE_SAMPLE = 4 };
+constexpr int kSampleStride = 16;  // 32-key blocks between sampled blocks
 
 struct RowState {
   int phase;
@@ -283,6 +285,16 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   __shared__ uint32_t s_nred[4][kRowsWG];
   __shared__ int s_part[kRowsWG];
   __shared__ int s_any;
+  // COLLECT: candidates are staged per row in LDS (rank from an LDS counter)
+  // and written out with one global atomic per row at the end; a row that
+  // overflows its LDS slots appends the rest directly.
+  constexpr bool COL = MODE == MODE_COLLECT;
+  constexpr int kStage = 96;  // LDS candidate slots per row
+  __shared__ uint64_t s_cand[COL ? kRowsWG * kStage : 1];
+  __shared__ uint32_t s_ccnt[COL ? kRowsWG : 1];
+  __shared__ uint32_t s_clo[COL ? kRowsWG : 1];
+  __shared__ uint32_t s_chi[COL ? kRowsWG : 1];
+  __shared__ uint32_t s_cbase[COL ? kRowsWG : 1];
 
   const int64_t item = xcd_work_item(p.per_xcd);
   if (item >= p.items) return;
@@ -308,13 +320,21 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     int part = 0;
     if (tid < nrows) {
       const int ph = p.st[row0 + tid].phase;
-      part = HIST ? ph == PH_HIST : (MODE == MODE_COLLECT) ? ph == PH_COLLECT : ph == PH_EMIT;
+      part = (HIST || MODE == MODE_SAMPLE) ? ph == PH_HIST
+             : (MODE == MODE_COLLECT)        ? ph == PH_COLLECT
+                                             : ph == PH_EMIT;
+      if (MODE == MODE_SAMPLE) part = part && !p.st[row0 + tid].topp;
     }
     s_part[tid] = part;
     if (part) atomicOr(&s_any, 1);
   }
   if (HIST)
     for (int t = tid; t < kRowsWG * HS; t += kThreads) s_hist[t] = 0u;
+  if (COL && tid < kRowsWG) {
+    s_ccnt[tid] = 0u;
+    s_clo[tid] = 0xFFFFFFFFu;
+    s_chi[tid] = 0u;
+  }
   __syncthreads();
   if (!s_any) return;
 
@@ -434,23 +454,63 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
           inside_mask |= inside ? 1u << e : 0u;
         }
       }
-      if (MODE == MODE_COLLECT && inside_mask) {  // candidates (a narrow interval: few)
-        const int64_t row = row0 + rl;
+      if (MODE == MODE_COLLECT && inside_mask) {  // candidates
+        uint32_t lo_k = 0xFFFFFFFFu, hi_k = 0u;
+        // one LDS atomic per lane reserves the ranks of all its candidates
+        uint32_t rank = atomicAdd(&s_ccnt[rl], static_cast<uint32_t>(__builtin_popcount(inside_mask)));
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           if (!((inside_mask >> e) & 1u)) continue;
           const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
-          const uint32_t pos = atomicAdd(&p.cand_n[row], 1u);
-          const uint32_t ok = ord_key(acc[e]);
-          if (pos < kCand)
-            p.cand[row * kCand + pos] =
-                (static_cast<uint64_t>(ok) << 32) | (~static_cast<uint32_t>(kb + kl));
-          atomicMin(&p.cand_lohi[2 * row], ok);
-          atomicMax(&p.cand_lohi[2 * row + 1], ok);
+          const uint32_t okey = ord_key(acc[e]);
+          const uint64_t entry = (static_cast<uint64_t>(okey) << 32) | (~static_cast<uint32_t>(kb + kl));
+          lo_k = min(lo_k, okey);
+          hi_k = max(hi_k, okey);
+          if (rank++ < kStage) {
+            s_cand[rl * kStage + rank - 1] = entry;
+          } else {  // LDS slots of this row full: append directly
+            const int64_t row = row0 + rl;
+            const uint32_t pos = atomicAdd(&p.cand_n[row], 1u);
+            if (pos < kCand) p.cand[row * kCand + pos] = entry;
+          }
         }
+        atomicMin(&s_clo[rl], lo_k);
+        atomicMax(&s_chi[rl], hi_k);
       }
     }
   };
+  if (MODE == MODE_SAMPLE) {
+    // Sampled blocks: every kSampleStride-th 32-key block of the split (the
+    // split starts on a multiple of the stride), spread over the waves.
+    float s1[2] = {0.0f, 0.0f}, s2[2] = {0.0f, 0.0f};
+    for (int blk = wave * kSampleStride; blk < nblk; blk += 4 * kSampleStride) {
+      u32x4 ka[DS];
+      kload(ka, blk);
+      const int kb = key0 + blk * 32;
+#pragma unroll
+      for (int rb2 = 0; rb2 < 2; ++rb2) {
+        f32x16 acc = f32x16{};
+#pragma unroll
+        for (int q2 = 0; q2 < DS; ++q2)
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ka[q2]),
+                                                        qf[rb2][q2], acc, 0, 0, 0);
+        const int lim = Lr[rb2] - kb;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+          const float sc = kl < lim ? acc[e] : 0.0f;
+          s1[rb2] += sc;
+          s2[rb2] = __builtin_fmaf(sc, sc, s2[rb2]);
+          nacc[rb2] += kl < lim ? 1u : 0u;
+        }
+      }
+    }
+#pragma unroll
+    for (int rb2 = 0; rb2 < 2; ++rb2) {
+      zacc[rb2] = s1[rb2];
+      macc[rb2] = s2[rb2];
+    }
+  } else {
   u32x4 k0[DS], k1[DS];
   kload(k0, wave);
   for (int blk = wave; blk < nblk; blk += 8) {
@@ -459,6 +519,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     if (blk + 4 >= nblk) break;
     kload(k0, blk + 8);
     kproc(k1, blk + 4);
+  }
   }
   if (MODE == MODE_EMIT) return;
 
@@ -476,6 +537,24 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     }
   }
   __syncthreads();
+  if (COL) {  // staged candidates: one atomic per row, then the copy
+    if (tid < nrows && s_part[tid]) {
+      const int64_t row = row0 + tid;
+      const uint32_t c = min(s_ccnt[tid], static_cast<uint32_t>(kStage));
+      s_cbase[tid] = c ? atomicAdd(&p.cand_n[row], c) : 0u;
+      if (s_ccnt[tid]) {
+        atomicMin(&p.cand_lohi[2 * row], s_clo[tid]);
+        atomicMax(&p.cand_lohi[2 * row + 1], s_chi[tid]);
+      }
+    }
+    __syncthreads();
+    for (int t = tid; t < nrows * kStage; t += kThreads) {
+      const int rl = t / kStage, j = t % kStage;
+      if (!s_part[rl] || j >= static_cast<int>(min(s_ccnt[rl], static_cast<uint32_t>(kStage)))) continue;
+      const uint32_t pos = s_cbase[rl] + j;
+      if (pos < kCand) p.cand[(row0 + rl) * kCand + pos] = s_cand[rl * kStage + j];
+    }
+  }
   if (tid < nrows && s_part[tid]) {
     const int64_t row = row0 + tid;
     const double z = ((s_zred[0][tid] + s_zred[1][tid]) + s_zred[2][tid]) + s_zred[3][tid];
@@ -483,7 +562,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     const uint32_t n = s_nred[0][tid] + s_nred[1][tid] + s_nred[2][tid] + s_nred[3][tid];
     p.n_above[row * p.nsplit + sp] = n;
     p.m_above[row * p.nsplit + sp] = m;
-    if (MODE == MODE_HIST0) p.zpart[row * p.nsplit + sp] = z;
+    if (MODE == MODE_HIST0 || MODE == MODE_SAMPLE) p.zpart[row * p.nsplit + sp] = z;
   }
   if (HIST) {
     for (int t = tid; t < nrows * kBins; t += kThreads) {
@@ -492,6 +571,47 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
       if (c && s_part[rl]) atomicAdd(&p.hist[(row0 + rl) * kBins + bn], c);
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// Level-0 bins of topK rows from a sample of their scores.  For any set of
+// values with mean mu and deviation sigma, at most a fraction 1 / (1 + a^2)
+// lies at or above mu + a sigma, and as much at or below mu - a sigma
+// (Cantelli's inequality); with a = sqrt((L - k) / k) above and
+// sqrt((k - 1) / (L - k + 1)) below, the k-th largest of L scores lies
+// between.  mu and sigma come from the sampled keys, so the bound is widened;
+// it only places the 256 bins (the tails fall into the end bins): a cut
+// outside it costs another level, never a wrong selection.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_bracket(SelParams p) {
+  const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (r >= p.rows) return;
+  RowState& s = p.st[r];
+  if (s.phase != PH_HIST || s.level != 0 || s.topp) return;
+  const int i = static_cast<int>(r % p.Np);
+  const int rb = i / kRowsWG;
+  const int i_last = min(p.Np, (rb + 1) * kRowsWG) - 1;
+  const int ns = (eligible(i_last, p.P, p.N, p.causal) + p.split - 1) / p.split;
+  double n = 0.0, m1 = 0.0, m2 = 0.0;
+  for (int q = 0; q < ns; ++q) {
+    n += p.n_above[r * p.nsplit + q];
+    m1 += p.zpart[r * p.nsplit + q];
+    m2 += p.m_above[r * p.nsplit + q];
+  }
+  const int L = s.L, k = s.k_target;
+  if (n < 64.0 || k >= L) return;
+  const double mu = m1 / n;
+  const double sd = sqrt(fmax(m2 / n - mu * mu, 0.0));
+  if (!(sd > 0.0)) return;
+  const double a_hi = sqrt(static_cast<double>(L - k) / k);
+  const double a_lo = sqrt(static_cast<double>(k - 1) / (L - k + 1));
+  const double widen = 1.2 + 4.0 / sqrt(n);
+  const float lo = fmaxf(static_cast<float>(mu - (widen * a_lo + 0.25) * sd), s.blo);
+  const float hi = fminf(static_cast<float>(mu + (widen * a_hi + 0.25) * sd), -s.blo);
+  if (!(hi > lo)) return;
+  s.blo = lo;
+  s.binv = static_cast<float>(kBins) / (hi - lo);
+  s.badd = -lo * s.binv;
 }
 
 // ---------------------------------------------------------------------------
@@ -945,6 +1065,10 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   const dim3 igrid(static_cast<unsigned>((rows + 255) / 256));
   for (int round = 0; round < kRounds; ++round) {
     hipLaunchKernelGGL(k_sel_init, igrid, dim3(256), 0, stream, p, round);
+    if (round == 0 && !p.mode_topp) {
+      score_pass<MODE_SAMPLE>(D, false, pgrid, p, stream);
+      hipLaunchKernelGGL(k_bracket, igrid, dim3(256), 0, stream, p);
+    }
     for (int lv = 0; lv < kLevels; ++lv) {
       if (lv == 0) score_pass<MODE_HIST0>(D, p.mode_topp != 0, pgrid, p, stream);
       else score_pass<MODE_HIST>(D, p.mode_topp != 0, pgrid, p, stream);

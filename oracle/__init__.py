@@ -60,10 +60,10 @@ def _load():
     lib.ora_topk_count.argtypes = [f64, i64]
     lib.ora_topk_count.restype = i64
     lib.ora_select.argtypes = [P, P, i64, i64, i64, i64, i64, i32, i32, i32, f64, i64,
-                               P, P, P, P, i64, i32]
+                               P, P, P, P, i64, i32, i32]
     lib.ora_mins_progressive_row.argtypes = [P, i64, f64, i64, i64, P, P]
     lib.ora_sparse_attn.argtypes = [P, P, P, i64, i64, i64, i64, i64, i32, i32, f64,
-                                    P, i64, P, P, P, P, i64, i32]
+                                    P, i64, P, P, P, P, i64, i32, i32]
     lib.ora_dense_attn.argtypes = [P, P, P, i64, i64, i64, i64, i64, i32, f64, P, P, i32]
     lib.ora_sparse_attn_online.argtypes = [P, P, P, i64, i64, i64, i64, i64, i32, i32, f64,
                                            P, i64, P, i32, P, P, i32]
@@ -138,23 +138,31 @@ def pooled_scores(q: np.ndarray, k: np.ndarray, block: int, causal: bool, b: int
 
 def select(q: np.ndarray, k: np.ndarray, block: int, mode: int, param: float, causal: bool,
            cap: int, rows: Optional[Sequence[int]] = None,
-           nthreads: int = 0) -> Tuple[np.ndarray, np.ndarray, int]:
+           nthreads: int = 0, compact: bool = False) -> Tuple[np.ndarray, np.ndarray, int]:
     """Selected key lists (ascending, -1 padded), counts and number of clamped rows.
 
     ``rows`` lists flat block ids w = (b * Hq + h) * Np + i to compute; other rows
-    of the outputs are left as -1 / 0.
+    of the outputs are left as -1 / 0.  ``compact`` (with ``rows``): outputs of
+    shape [len(rows), cap] and [len(rows)], in the order of ``rows``.
     """
     q, k = _bits(q), _bits(k)
     B, Hq, N, D = q.shape
     Hkv = k.shape[1]
     Np = num_blocks(N, block)
-    idx = np.full((B, Hq, Np, cap), -1, dtype=np.int32)
-    counts = np.zeros((B, Hq, Np), dtype=np.int32)
+    if compact:
+        if rows is None:
+            raise ValueError("compact output needs rows")
+        idx = np.full((len(rows), cap), -1, dtype=np.int32)
+        counts = np.zeros(len(rows), dtype=np.int32)
+    else:
+        idx = np.full((B, Hq, Np, cap), -1, dtype=np.int32)
+        counts = np.zeros((B, Hq, Np), dtype=np.int32)
     ncl = ctypes.c_int64(0)
     rows_arr = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
     rc = _load().ora_select(_ptr(q), _ptr(k), B, Hq, Hkv, N, D, block, int(causal), int(mode),
                             float(param), int(cap), _ptr(idx), _ptr(counts), ctypes.byref(ncl),
-                            _ptr(rows_arr), 0 if rows_arr is None else rows_arr.size, nthreads)
+                            _ptr(rows_arr), 0 if rows_arr is None else rows_arr.size,
+                            int(bool(compact)), nthreads)
     if rc == 3:
         raise ValueError("capacity too small for topK")
     _check(rc, "select")
@@ -173,22 +181,32 @@ def mins_progressive(scores: np.ndarray, alpha: float, bk: int, gk: int) -> np.n
 def sparse_attn(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, counts: np.ndarray,
                 block: int, causal: bool, scale: float = 0.0,
                 blocks: Optional[Sequence[int]] = None,
-                nthreads: int = 0) -> Tuple[np.ndarray, np.ndarray]:
+                nthreads: int = 0, compact: bool = False) -> Tuple[np.ndarray, np.ndarray]:
     """Eq. 4 in fp64.  Returns (O [B,Hq,N,D] f64, LSE [B,Hq,N] f64); rows of
-    blocks not listed in ``blocks`` are left NaN."""
+    blocks not listed in ``blocks`` are left NaN.  ``compact`` (with
+    ``blocks``): idx [len(blocks), cap] and counts [len(blocks)] hold the listed
+    blocks' lists in order, and the outputs are O [len(blocks), block, D] and
+    LSE [len(blocks), block] (rows past N in a ragged last block stay NaN)."""
     q, k, v = _bits(q), _bits(k), _bits(v)
     B, Hq, N, D = q.shape
     Hkv = k.shape[1]
     idx = np.ascontiguousarray(idx, dtype=np.int32)
     counts = np.ascontiguousarray(counts, dtype=np.int32)
     cap = idx.shape[-1]
-    o = np.full((B, Hq, N, D), np.nan, dtype=np.float64)
-    lse = np.full((B, Hq, N), np.nan, dtype=np.float64)
+    if compact:
+        if blocks is None:
+            raise ValueError("compact layout needs blocks")
+        o = np.full((len(blocks), block, D), np.nan, dtype=np.float64)
+        lse = np.full((len(blocks), block), np.nan, dtype=np.float64)
+    else:
+        o = np.full((B, Hq, N, D), np.nan, dtype=np.float64)
+        lse = np.full((B, Hq, N), np.nan, dtype=np.float64)
     blk = None if blocks is None else np.ascontiguousarray(blocks, dtype=np.int64)
     _check(_load().ora_sparse_attn(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, D, block,
                                    int(causal), float(scale), _ptr(idx), cap, _ptr(counts),
                                    _ptr(o), _ptr(lse), _ptr(blk),
-                                   0 if blk is None else blk.size, nthreads), "sparse_attn")
+                                   0 if blk is None else blk.size, int(bool(compact)), nthreads),
+           "sparse_attn")
     return o, lse
 
 

@@ -299,7 +299,9 @@ int64_t ora_topk_count(double ratio, int64_t L) { return topk_count(ratio, L); }
 
 // Selection (Sec. 3.1): for every block (or for the listed flat rows
 // w = (b * Hq + h) * Np + i), the selected key indices in ascending order in
-// idx[w * cap ...], padded with -1, and their number in counts[w].
+// idx[w * cap ...], padded with -1, and their number in counts[w].  With
+// compact != 0 (only with rows), the t-th listed row goes to idx[t * cap ...]
+// and counts[t] instead (outputs sized for the listed rows only).
 // mode 0 topK (param = keep ratio), 1 topP (param = mass p), 2 minS with the
 // global row max (param = alpha).  Threshold modes that select more than cap
 // keys keep the first cap keys in (score desc, index asc) order and add one to
@@ -307,9 +309,10 @@ int64_t ora_topk_count(double ratio, int64_t L) { return topk_count(ratio, L); }
 int ora_select(const uint16_t* q, const uint16_t* k, int64_t B, int64_t Hq, int64_t Hkv, int64_t N,
                int64_t D, int32_t block, int32_t causal, int32_t mode, double param, int64_t cap,
                int32_t* idx, int32_t* counts, int64_t* n_clamped, const int64_t* rows,
-               int64_t n_rows, int32_t nthreads) {
+               int64_t n_rows, int32_t compact, int32_t nthreads) {
   Shape s{B, Hq, Hkv, N, D};
   if (!q || !k || !idx || !counts || block < 1 || cap < 1 || !shape_ok(s)) return ORA_ERR_ARG;
+  if (compact && !rows) return ORA_ERR_ARG;
   if (mode == SEL_TOPK && !(param > 0.0 && param <= 1.0)) return ORA_ERR_ARG;
   if (mode == SEL_TOPP && !(param > 0.0 && param <= 1.0)) return ORA_ERR_ARG;
   if (mode == SEL_MINS && !(param >= 0.0)) return ORA_ERR_ARG;
@@ -350,10 +353,11 @@ int ora_select(const uint16_t* q, const uint16_t* k, int64_t B, int64_t Hq, int6
       chosen.assign(ord.begin(), ord.begin() + n);
     }
     std::sort(chosen.begin(), chosen.end());
-    int32_t* row = idx + w * cap;
+    const int64_t orow = compact ? t : w;
+    int32_t* row = idx + orow * cap;
     for (int64_t c = 0; c < cap; ++c)
       row[c] = c < static_cast<int64_t>(chosen.size()) ? static_cast<int32_t>(chosen[c]) : -1;
-    counts[w] = static_cast<int32_t>(chosen.size());
+    counts[orow] = static_cast<int32_t>(chosen.size());
   }
   if (n_clamped) *n_clamped = clamped;
   return ORA_OK;
@@ -378,10 +382,14 @@ int ora_mins_progressive_row(const double* scores, int64_t L, double alpha, int6
 int ora_sparse_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v, int64_t B, int64_t Hq,
                     int64_t Hkv, int64_t N, int64_t D, int32_t block, int32_t causal, double scale,
                     const int32_t* idx, int64_t cap, const int32_t* counts, double* o, double* lse,
-                    const int64_t* blocks, int64_t n_blocks, int32_t nthreads) {
+                    const int64_t* blocks, int64_t n_blocks, int32_t compact, int32_t nthreads) {
+  // compact != 0 (only with blocks): the t-th listed block's list is
+  // idx[t * cap ...] / counts[t], and its rows go to o[(t * block + r') * D]
+  // and lse[t * block + r'] (r' = row within the block).
   Shape s{B, Hq, Hkv, N, D};
   if (!q || !k || !v || !idx || !counts || !o || block < 1 || cap < 0 || !shape_ok(s))
     return ORA_ERR_ARG;
+  if (compact && !blocks) return ORA_ERR_ARG;
   if (scale == 0.0) scale = 1.0 / std::sqrt(static_cast<double>(D));
   const int64_t Np = num_blocks(N, block);
   const int64_t total = blocks ? n_blocks : B * Hq * Np;
@@ -391,12 +399,13 @@ int ora_sparse_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v, int
   for (int64_t t = 0; t < total; ++t) {
     const int64_t w = blocks ? blocks[t] : t;
     const int64_t i = w % Np, h = (w / Np) % Hq, b = w / (Np * Hq);
-    const int32_t c = counts[w];
+    const int64_t lrow = compact ? t : w;
+    const int32_t c = counts[lrow];
     if (c < 0 || c > cap) {
       bad = 1;
       continue;
     }
-    const int32_t* list = idx + w * cap;
+    const int32_t* list = idx + lrow * cap;
     const int64_t r0 = i * block, r1 = std::min<int64_t>(N, r0 + block);
     std::vector<int64_t> keys;
     for (int64_t r = r0; r < r1; ++r) {
@@ -410,8 +419,9 @@ int ora_sparse_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v, int
         if (!causal || j <= r) keys.push_back(j);
       }
       double lse_r;
-      attend_row(q, k, v, s, b, h, r, keys, scale, o + row_off(b, h, r, Hq, N, D), &lse_r);
-      if (lse) lse[(b * Hq + h) * N + r] = lse_r;
+      const int64_t orow = compact ? t * block + (r - r0) : (b * Hq + h) * N + r;
+      attend_row(q, k, v, s, b, h, r, keys, scale, o + orow * D, &lse_r);
+      if (lse) lse[orow] = lse_r;
     }
   }
   return bad ? ORA_ERR_ARG : ORA_OK;

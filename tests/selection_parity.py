@@ -19,28 +19,39 @@ REL_TOL = 1e-5
 MASS_TOL = 1e-5
 
 
-def check_rows(q, k, block, mode, param, causal, cap, idx_gpu, cnt_gpu, rows):
-    """Returns the number of rows whose sets differ (all within the rule)."""
+def check_rows(q, k, block, mode, param, causal, cap, idx_gpu, cnt_gpu, rows, compact=False):
+    """Returns the number of rows whose sets differ (all within the rule).
+
+    compact: idx_gpu [len(rows), cap] / cnt_gpu [len(rows)] hold only the
+    sampled rows, in the order of ``rows`` (full-size layers)."""
     B, Hq, N, D = q.shape
     Np = (N + block - 1) // block
-    idx_o, cnt_o, _ = oracle.select(q, k, block, mode, param, causal, cap, rows=rows)
+    if compact:
+        idx_o, cnt_o, _ = oracle.select(q, k, block, mode, param, causal, cap, rows=rows,
+                                        compact=True)
+        pos = {int(w): t for t, w in enumerate(rows)}
+    else:
+        idx_o, cnt_o, _ = oracle.select(q, k, block, mode, param, causal, cap, rows=rows)
+        pos = {int(w): int(w) for w in rows}
     idx_o = idx_o.reshape(-1, cap)
     cnt_o = cnt_o.reshape(-1)
     idx_gpu = idx_gpu.reshape(-1, idx_gpu.shape[-1])
     cnt_gpu = cnt_gpu.reshape(-1)
     mismatched = 0
     for w in rows:
+        w = int(w)
+        pw = pos[w]
         i, h, b = w % Np, (w // Np) % Hq, w // (Np * Hq)
         s = oracle.pooled_scores(q, k, block, causal, b, h, i)
         L = len(s)
         tol = REL_TOL * np.abs(s).max()
-        cg, co = int(cnt_gpu[w]), int(cnt_o[w])
-        g = idx_gpu[w, :cg]
-        o = idx_o[w, :co]
+        cg, co = int(cnt_gpu[pw]), int(cnt_o[pw])
+        g = idx_gpu[pw, :cg]
+        o = idx_o[pw, :co]
         assert 0 <= cg <= idx_gpu.shape[1], (w, cg)
         assert np.all(np.diff(g) > 0), f"row {w}: not strictly ascending"
         assert cg == 0 or (g[0] >= 0 and g[-1] < L), f"row {w}: index out of range"
-        assert np.all(idx_gpu[w, cg:] == -1), f"row {w}: padding"
+        assert np.all(idx_gpu[pw, cg:] == -1), f"row {w}: padding"
         diff = np.setxor1d(g, o)
         if mode == oracle.TOPK or co == cap:   # topK, or a threshold row clamped to cap
             assert cg == co, f"row {w}: count {cg} != {co}"

@@ -1,0 +1,87 @@
+"""The five synthetic workloads at full size, in the launch configuration the
+benchmark times (selection with the library's default cap and workspace,
+then sparse attention on its lists), checked against the CPU oracle on a
+random sample of query blocks: the selection rule of selection_parity and
+the attention bar of test_attn_gpu (max-abs 2e-2, mean-abs 2e-3 against the
+fp64 oracle on the GPU's own lists).  Plus properties that hold for every
+block: lists ascending and in range, counts within [1, cap], and for topK the
+exact budget."""
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2603_29494_amd as va
+from paper_2603_29494_amd import synth
+from selection_parity import check_rows
+
+pytestmark = pytest.mark.gpu
+
+SAMPLE_BLOCKS = 10
+
+
+def dev(bits):
+    return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).cuda()
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
+def test_workload_full_size(gpu, cid):
+    layer = synth.make_layer(cid)
+    w = layer.w
+    q, k, v = dev(layer.q), dev(layer.k), dev(layer.v)
+    B, Hq, N, D = q.shape
+    P = w.block
+    Np = (N + P - 1) // P
+    print(f"workload {cid} {w.name}: select + attention", flush=True)
+    idx, cnt = va.select(q, k, P, w.mode, w.param, w.causal)
+    out = va.sparse_attn(q, k, v, idx, cnt, P, w.causal)
+    torch.cuda.synchronize()
+    cap = idx.shape[-1]
+
+    # Every block: counts, order, range (on the GPU, without copying the lists).
+    L = torch.tensor([min(N, (i + 1) * P) if w.causal else N for i in range(Np)], device="cuda")
+    c = cnt.long()
+    assert bool((c >= 1).all()) and bool((c <= cap).all())
+    if w.mode == "topk":
+        kt = torch.tensor([min(max(math.ceil(w.param * int(l) - 1e-9), 1), int(l)) for l in L.tolist()],
+                          device="cuda")
+        assert bool((c == kt.view(1, 1, Np)).all()), "topK budget"
+    flat = idx.view(-1, cap)
+    cflat = c.view(-1)
+    col = torch.arange(cap, device="cuda")
+    chunk = max(1, (1 << 24) // cap)  # rows per check: the lists of a long layer are large
+    for s in range(0, flat.shape[0], chunk):
+        f, cf = flat[s:s + chunk], cflat[s:s + chunk]
+        live = col.view(1, -1) < cf.view(-1, 1)
+        assert bool(((f >= 0) | ~live).all()) and bool(((f == -1) | live).all())
+        asc = (f[:, 1:] > f[:, :-1]) | ~live[:, 1:]
+        assert bool(asc.all()), "lists ascending"
+        Lrow = L[(torch.arange(s, s + f.shape[0], device="cuda") % Np)]
+        assert bool(((f < Lrow.view(-1, 1)) | ~live).all()), "keys eligible"
+
+    # Sampled blocks against the oracle.
+    rng = np.random.Generator(np.random.PCG64(4242 + cid))
+    rows = np.sort(rng.choice(B * Hq * Np, size=min(SAMPLE_BLOCKS, B * Hq * Np), replace=False))
+    rsel = torch.from_numpy(rows).cuda()
+    idx_s = flat[rsel].cpu().numpy()
+    cnt_s = cflat[rsel].int().cpu().numpy()
+    mode = oracle.TOPK if w.mode == "topk" else oracle.TOPP
+    check_rows(layer.q, layer.k, P, mode, w.param, w.causal, cap, idx_s, cnt_s, rows, compact=True)
+    nth = min(16, os.cpu_count() or 1)
+    o_ref, _ = oracle.sparse_attn(layer.q, layer.k, layer.v, idx_s, cnt_s, P, w.causal,
+                                  blocks=rows, compact=True, nthreads=nth)
+    o_gpu = out.view(B, Hq, N, D)
+    errs = []
+    for t, r in enumerate(rows):
+        i, h, b = r % Np, (r // Np) % Hq, r // (Np * Hq)
+        n = min(N, (i + 1) * P) - i * P
+        got = o_gpu[b, h, i * P:i * P + n].float().cpu().numpy()
+        errs.append(np.abs(got - o_ref[t, :n]))
+    err = np.concatenate([e.ravel() for e in errs])
+    assert np.isfinite(err).all()
+    assert err.max() <= 2e-2 and err.mean() <= 2e-3, (err.max(), err.mean())
+    print(f"workload {cid}: {len(rows)} sampled blocks, max|dO| {err.max():.2e}, "
+          f"mean|dO| {err.mean():.2e}", flush=True)

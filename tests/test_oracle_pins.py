@@ -374,3 +374,28 @@ def test_plumbing_workload_recovers_planted_columns():
     # the planted boost is 0.5 logit against a score spread of ~0.2, so most
     # (not all) planted columns land in every block's top 12.5%
     assert np.mean(recall) > 0.85
+
+
+def test_compact_row_layout_matches_full_layout():
+    """The compact layout (sampled rows only) is an indexing change: the same
+    lists, counts, outputs and LSE as the full layout, row for row."""
+    q = synth.random_bits(1, (1, 2, 300, 64))
+    k = synth.random_bits(2, (1, 2, 300, 64))
+    v = synth.random_bits(3, (1, 2, 300, 64))
+    rows = [1, 4, 7, 9]
+    Np = 5
+    for mode, param in ((oracle.TOPK, 0.2), (oracle.TOPP, 0.9)):
+        i1, c1, n1 = oracle.select(q, k, 64, mode, param, True, 300, rows=rows)
+        i2, c2, n2 = oracle.select(q, k, 64, mode, param, True, 300, rows=rows, compact=True)
+        assert n1 == n2
+        for t, r in enumerate(rows):
+            assert np.array_equal(i1.reshape(-1, 300)[r], i2[t])
+            assert c1.reshape(-1)[r] == c2[t]
+        o1, l1 = oracle.sparse_attn(q, k, v, i1, c1, 64, True, blocks=rows)
+        o2, l2 = oracle.sparse_attn(q, k, v, i2, c2, 64, True, blocks=rows, compact=True)
+        for t, r in enumerate(rows):
+            i, h = r % Np, r // Np
+            n = min(300, (i + 1) * 64) - i * 64
+            assert np.array_equal(o1[0, h, i * 64:i * 64 + n], o2[t, :n])
+            assert np.array_equal(l1[0, h, i * 64:i * 64 + n], l2[t, :n])
+            assert np.isnan(o2[t, n:]).all()

@@ -30,6 +30,25 @@ sys.path.insert(0, HERE)
 
 PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 dense bf16 FLOP/clk/CU
 PEAK_HBM_GBS = 8000.0
+TRAFFIC_RECORD = os.path.join(HERE, "profiles", "hbm_traffic_dit_wan_75k.md")
+ATTN_SOURCE = os.path.join(HERE, "paper_2603_29494_amd", "csrc", "sparse_attn.hip")
+
+
+def recorded_traffic(workload: str):
+    """Bytes per launch of the attention kernel from the committed counter
+    record (FETCH_SIZE + WRITE_SIZE, calibrated against a copy kernel), or
+    None when the record is for another workload or another kernel source."""
+    import hashlib
+    try:
+        sha = hashlib.sha256(open(ATTN_SOURCE, "rb").read()).hexdigest()
+        for line in open(TRAFFIC_RECORD):
+            f = dict(t.split("=", 1) for t in line.split() if "=" in t)
+            if line.strip().startswith("traffic ") and f.get("workload") == workload \
+                    and f.get("source_sha256") == sha:
+                return float(f["bytes_per_launch"])
+    except (OSError, ValueError, KeyError):
+        pass
+    return None
 
 
 def parse():
@@ -179,10 +198,12 @@ def main():
         "attention_mfma_pct": round(100.0 * attn_tflops / PEAK_BF16_TFLOPS, 2),
         "selection_hbm_pct": round(100.0 * bytes_sel / (sel_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 2),
         "achieved_keep": round(keep, 6),
-        "roofline": {"bound": "mfma", "kernel": "k_sparse_attn<128>",
+        "roofline": {"bound": "mfma", "kernel": f"k_sparse_attn<{D}>",
                      "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None},
+                     "traffic": recorded_traffic(w.name)},
+        # K and V rows (2 x D bf16 each) gathered per selected key, per 64-row chunk
+        "attention_gathered_bytes": 4.0 * D * float(cnt.sum()) * ((P + 63) // 64),
         "input_generation_s": round(t_gen, 1),
     }
     if not args.no_cpu_baseline:

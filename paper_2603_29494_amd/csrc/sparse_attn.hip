@@ -1,7 +1,8 @@
 // Vector-sparse attention (paper Eq. 4, Sec. 3.2; appendix Algorithm 2) for gfx950.
 //
 // One workgroup (4 waves) owns up to 64 query rows of one query block of one
-// head and walks the block's index list I[b,h,i,0:C) in tiles of 64 keys.
+// head and walks the block's index list I[b,h,i,0:C) in tiles of 64 keys
+// (starting at a clock-chosen tile and wrapping around, see below).
 // The K and V rows of a tile are gathered straight from global memory into
 // LDS (global_load_lds, 16 B per lane, no register staging) two tiles deep,
 // stored row-major with an XOR swizzle of their 16-byte chunks so that both
@@ -31,6 +32,10 @@ constexpr int kRows = 64;     // query rows per workgroup
 constexpr int kTile = 64;     // keys per gathered tile
 constexpr int kThreads = 256;
 constexpr int kStages = 2;
+// Nominal time per tile and workgroup in ticks of the 100 MHz constant clock
+// (two workgroups per CU at the 75k DiT shape); it sets the speed of the
+// sweep below.
+constexpr unsigned long long kTileTicks = 165;
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
@@ -110,6 +115,28 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
       static_cast<int>(min<int64_t>(max(counts[bh * Np + i], 0), cap)));
   const int32_t* list = idx + (bh * Np + i) * cap;
   const int ntiles = (count + kTile - 1) / kTile;
+  // Tile order.  A block's keys are random rows of the head's K/V, far more
+  // than an XCD's L2 holds; the workgroups running together on an XCD share
+  // L2 hits only if they gather from the same key range at the same time.
+  // Lists are ascending, so a workgroup's position in its list is a position
+  // in key space: each workgroup starts at the tile given by a chip-wide
+  // clock (period = the nominal time of its whole list) and wraps around, so
+  // workgroups that run together sweep the keys together.  The order of the
+  // tiles changes only the order of the softmax sums (results can differ
+  // between runs within fp32 rounding).
+  __shared__ int s_rot;
+  if (threadIdx.x == 0) {
+    const unsigned long long now = __builtin_amdgcn_s_memrealtime();
+    const unsigned long long per = static_cast<unsigned long long>(ntiles) * kTileTicks;
+    s_rot = ntiles > 1 ? static_cast<int>((now % per) / kTileTicks) : 0;
+  }
+  __syncthreads();
+  const int t_rot = __builtin_amdgcn_readfirstlane(s_rot);
+  auto tile_of = [&](int t) __attribute__((always_inline)) {  // t-th tile processed
+    if (t >= ntiles) return t;  // past the list (reads 0)
+    const int x = t + t_rot;
+    return x >= ntiles ? x - ntiles : x;
+  };
   // Reads of the list past `count` return 0 (buffer range check).
   const __amdgpu_buffer_rsrc_t lrs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(list), 0, count * 4, 0x00020000);
@@ -163,7 +190,7 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
   auto load_ids = [&](int t) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
-      nid[u] = __builtin_amdgcn_raw_buffer_load_b32(lrs, (t * kTile + grow(u)) * 4, 0, 0);
+      nid[u] = __builtin_amdgcn_raw_buffer_load_b32(lrs, (tile_of(t) * kTile + grow(u)) * 4, 0, 0);
   };
   auto issue_tile = [&](int t, int st) __attribute__((always_inline)) {
 #pragma unroll
@@ -175,7 +202,7 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
       gather16_to_lds(vrs, __umul24(r, v_rowb) + 16u * gcol(u), vd);
     }
     if (wave == 0)  // the tile's key ids (clamped to the list; entries past count are masked)
-      __builtin_amdgcn_global_load_lds(list + min(t * kTile + lane, count - 1),
+      __builtin_amdgcn_global_load_lds(list + min(tile_of(t) * kTile + lane, count - 1),
                                        LDS_PTR(void, ibuf(st)), 4, 0, 0);
   };
 
@@ -222,7 +249,7 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
 
     // Masks are needed only on the list's last tile and, when causal, on tiles
     // reaching past this wave's first row (lists are ascending).
-    const int tbase = t * kTile;
+    const int tbase = tile_of(t) * kTile;
     const int nvalid = min(kTile, count - tbase);
     const int32_t* ids = ibuf(st);
     const bool need_mask = nvalid < kTile || (causal && ids[nvalid - 1] > row0 + 32 * rw);

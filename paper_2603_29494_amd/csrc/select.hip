@@ -295,6 +295,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   __shared__ uint32_t s_clo[COL ? kRowsWG : 1];
   __shared__ uint32_t s_chi[COL ? kRowsWG : 1];
   __shared__ uint32_t s_cbase[COL ? kRowsWG : 1];
+  __shared__ __align__(16) float s_acc[COL ? 4 * 64 * 16 : 1];  // per lane: its 16 scores
 
   const int64_t item = xcd_work_item(p.per_xcd);
   if (item >= p.items) return;
@@ -399,16 +400,54 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
       const bool full = !__any(lim < 32);
       auto elig = [&](int kl) __attribute__((always_inline)) { return full || kl < lim; };
       if (MODE == MODE_COLLECT) {
-        // Kept-key bitmask for this block: every key at or above the interval's
-        // lower bound; the resolve step clears the candidates it rejects.
-        uint32_t w = 0u;
+        // Two bitmasks of this lane's keys (bit kl): at or above the interval
+        // (the kept set; the resolve step clears the candidates it rejects) and
+        // above it.  Their difference is the lane's candidates.
+        uint32_t wge = 0u, wgt = 0u;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
-          w |= (elig(kl) && acc[e] >= slo[rb2]) ? 1u << kl : 0u;
+          const bool ok = elig(kl);
+          wge |= (ok && acc[e] >= slo[rb2]) ? 1u << kl : 0u;
+          wgt |= (ok && acc[e] > shi[rb2]) ? 1u << kl : 0u;
+          if (TOPP && ref[rb2] >= 0.0 && ok && acc[e] > shi[rb2])
+            macc[rb2] += mass_term(acc[e], p.tau, ref[rb2]);
         }
-        w |= __shfl_xor(w, 32);
+        nacc[rb2] += static_cast<uint32_t>(__builtin_popcount(wgt));
+        const uint32_t ins = wge & ~wgt;
+        const uint32_t w = wge | __shfl_xor(wge, 32);
         if (g == 0) p.bsel[(row0 + rb2 * 32 + ln) * p.W + kb / 32] = w;
+        if (__any(ins != 0u)) {
+          // The lane's scores go through LDS so that a candidate's score can
+          // be read by its (per-lane) position.
+          float* sc = s_acc + (wave * 64 + lane) * 16;
+#pragma unroll
+          for (int q4 = 0; q4 < 4; ++q4)
+            *reinterpret_cast<f32x4*>(sc + 4 * q4) =
+                f32x4{acc[4 * q4], acc[4 * q4 + 1], acc[4 * q4 + 2], acc[4 * q4 + 3]};
+          if (ins) {
+            const int rl = rb2 * 32 + ln;
+            uint32_t rank = atomicAdd(&s_ccnt[rl], static_cast<uint32_t>(__builtin_popcount(ins)));
+            uint32_t lo_k = 0xFFFFFFFFu, hi_k = 0u;
+            for (uint32_t m = ins; m; m &= m - 1u) {
+              const int kl = __builtin_ctz(m);
+              const uint32_t okey = ord_key(sc[4 * (kl >> 3) + (kl & 3)]);
+              const uint64_t entry = (static_cast<uint64_t>(okey) << 32) | (~static_cast<uint32_t>(kb + kl));
+              lo_k = min(lo_k, okey);
+              hi_k = max(hi_k, okey);
+              if (rank++ < kStage) {
+                s_cand[rl * kStage + rank - 1] = entry;
+              } else {  // LDS slots of this row full: append directly
+                const int64_t row = row0 + rl;
+                const uint32_t pos = atomicAdd(&p.cand_n[row], 1u);
+                if (pos < kCand) p.cand[row * kCand + pos] = entry;
+              }
+            }
+            atomicMin(&s_clo[rl], lo_k);
+            atomicMax(&s_chi[rl], hi_k);
+          }
+        }
+        continue;
       }
       if (MODE == MODE_EMIT) {
         uint32_t wsel = 0u, wtie = 0u;
@@ -430,7 +469,6 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
         continue;
       }
       const int rl = rb2 * 32 + ln;
-      uint32_t inside_mask = 0u;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
@@ -450,32 +488,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
         if (HIST) {
           const int bn = inside ? bin_of(sc, bmul[rb2], badd[rb2]) : kBins;
           atomicAdd(&s_hist[rl * HS + bn], 1u);
-        } else {
-          inside_mask |= inside ? 1u << e : 0u;
         }
-      }
-      if (MODE == MODE_COLLECT && inside_mask) {  // candidates
-        uint32_t lo_k = 0xFFFFFFFFu, hi_k = 0u;
-        // one LDS atomic per lane reserves the ranks of all its candidates
-        uint32_t rank = atomicAdd(&s_ccnt[rl], static_cast<uint32_t>(__builtin_popcount(inside_mask)));
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          if (!((inside_mask >> e) & 1u)) continue;
-          const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
-          const uint32_t okey = ord_key(acc[e]);
-          const uint64_t entry = (static_cast<uint64_t>(okey) << 32) | (~static_cast<uint32_t>(kb + kl));
-          lo_k = min(lo_k, okey);
-          hi_k = max(hi_k, okey);
-          if (rank++ < kStage) {
-            s_cand[rl * kStage + rank - 1] = entry;
-          } else {  // LDS slots of this row full: append directly
-            const int64_t row = row0 + rl;
-            const uint32_t pos = atomicAdd(&p.cand_n[row], 1u);
-            if (pos < kCand) p.cand[row * kCand + pos] = entry;
-          }
-        }
-        atomicMin(&s_clo[rl], lo_k);
-        atomicMax(&s_chi[rl], hi_k);
       }
     }
   };

@@ -396,100 +396,104 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
       if (!part[rb2]) continue;
       const int lim = Lr[rb2] - kb;  // keys kl < lim are eligible
       // Whole block eligible for every row of the wave (all blocks but the
-      // last, unless causal): no per-key test.
+      // last, unless causal): the per-key test folds away.
       const bool full = !__any(lim < 32);
-      auto elig = [&](int kl) __attribute__((always_inline)) { return full || kl < lim; };
-      if (MODE == MODE_COLLECT) {
-        // Two bitmasks of this lane's keys (bit kl): at or above the interval
-        // (the kept set; the resolve step clears the candidates it rejects) and
-        // above it.  Their difference is the lane's candidates.
-        uint32_t wge = 0u, wgt = 0u;
+      auto rowproc = [&](const bool all_elig) __attribute__((always_inline)) {
+        auto elig = [&](int kl) __attribute__((always_inline)) { return all_elig || kl < lim; };
+        if (MODE == MODE_COLLECT) {
+          // Two bitmasks of this lane's keys (bit kl): at or above the interval
+          // (the kept set; the resolve step clears the candidates it rejects) and
+          // above it.  Their difference is the lane's candidates.
+          uint32_t wge = 0u, wgt = 0u;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+            const bool ok = elig(kl);
+            wge |= (ok && acc[e] >= slo[rb2]) ? 1u << kl : 0u;
+            wgt |= (ok && acc[e] > shi[rb2]) ? 1u << kl : 0u;
+            if (TOPP && ref[rb2] >= 0.0 && ok && acc[e] > shi[rb2])
+              macc[rb2] += mass_term(acc[e], p.tau, ref[rb2]);
+          }
+          nacc[rb2] += static_cast<uint32_t>(__builtin_popcount(wgt));
+          const uint32_t ins = wge & ~wgt;
+          const uint32_t w = wge | __shfl_xor(wge, 32);
+          if (g == 0) p.bsel[(row0 + rb2 * 32 + ln) * p.W + kb / 32] = w;
+          if (__any(ins != 0u)) {
+            // The lane's scores go through LDS so that a candidate's score can
+            // be read by its (per-lane) position.
+            float* sc = s_acc + (wave * 64 + lane) * 16;
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4)
+              *reinterpret_cast<f32x4*>(sc + 4 * q4) =
+                  f32x4{acc[4 * q4], acc[4 * q4 + 1], acc[4 * q4 + 2], acc[4 * q4 + 3]};
+            if (ins) {
+              const int rl = rb2 * 32 + ln;
+              uint32_t rank = atomicAdd(&s_ccnt[rl], static_cast<uint32_t>(__builtin_popcount(ins)));
+              uint32_t lo_k = 0xFFFFFFFFu, hi_k = 0u;
+              for (uint32_t m = ins; m; m &= m - 1u) {
+                const int kl = __builtin_ctz(m);
+                const uint32_t okey = ord_key(sc[4 * (kl >> 3) + (kl & 3)]);
+                const uint64_t entry = (static_cast<uint64_t>(okey) << 32) | (~static_cast<uint32_t>(kb + kl));
+                lo_k = min(lo_k, okey);
+                hi_k = max(hi_k, okey);
+                if (rank++ < kStage) {
+                  s_cand[rl * kStage + rank - 1] = entry;
+                } else {  // LDS slots of this row full: append directly
+                  const int64_t row = row0 + rl;
+                  const uint32_t pos = atomicAdd(&p.cand_n[row], 1u);
+                  if (pos < kCand) p.cand[row * kCand + pos] = entry;
+                }
+              }
+              atomicMin(&s_clo[rl], lo_k);
+              atomicMax(&s_chi[rl], hi_k);
+            }
+          }
+          return;
+        }
+        if (MODE == MODE_EMIT) {
+          uint32_t wsel = 0u, wtie = 0u;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+            const bool ok = elig(kl);
+            wsel |= (ok && acc[e] > ts[rb2]) ? 1u << kl : 0u;
+            wtie |= (ok && acc[e] == ts[rb2]) ? 1u << kl : 0u;
+          }
+          wsel |= __shfl_xor(wsel, 32);
+          wtie |= __shfl_xor(wtie, 32);
+          if (!tiep[rb2]) wsel |= wtie;
+          if (g == 0) {
+            const int64_t row = row0 + rb2 * 32 + ln;
+            p.bsel[row * p.W + kb / 32] = wsel;
+            if (tiep[rb2]) p.btie[row * p.W + kb / 32] = wtie;
+          }
+          return;
+        }
+        const int rl = rb2 * 32 + ln;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+          const float sc = acc[e];
           const bool ok = elig(kl);
-          wge |= (ok && acc[e] >= slo[rb2]) ? 1u << kl : 0u;
-          wgt |= (ok && acc[e] > shi[rb2]) ? 1u << kl : 0u;
-          if (TOPP && ref[rb2] >= 0.0 && ok && acc[e] > shi[rb2])
-            macc[rb2] += mass_term(acc[e], p.tau, ref[rb2]);
-        }
-        nacc[rb2] += static_cast<uint32_t>(__builtin_popcount(wgt));
-        const uint32_t ins = wge & ~wgt;
-        const uint32_t w = wge | __shfl_xor(wge, 32);
-        if (g == 0) p.bsel[(row0 + rb2 * 32 + ln) * p.W + kb / 32] = w;
-        if (__any(ins != 0u)) {
-          // The lane's scores go through LDS so that a candidate's score can
-          // be read by its (per-lane) position.
-          float* sc = s_acc + (wave * 64 + lane) * 16;
-#pragma unroll
-          for (int q4 = 0; q4 < 4; ++q4)
-            *reinterpret_cast<f32x4*>(sc + 4 * q4) =
-                f32x4{acc[4 * q4], acc[4 * q4 + 1], acc[4 * q4 + 2], acc[4 * q4 + 3]};
-          if (ins) {
-            const int rl = rb2 * 32 + ln;
-            uint32_t rank = atomicAdd(&s_ccnt[rl], static_cast<uint32_t>(__builtin_popcount(ins)));
-            uint32_t lo_k = 0xFFFFFFFFu, hi_k = 0u;
-            for (uint32_t m = ins; m; m &= m - 1u) {
-              const int kl = __builtin_ctz(m);
-              const uint32_t okey = ord_key(sc[4 * (kl >> 3) + (kl & 3)]);
-              const uint64_t entry = (static_cast<uint64_t>(okey) << 32) | (~static_cast<uint32_t>(kb + kl));
-              lo_k = min(lo_k, okey);
-              hi_k = max(hi_k, okey);
-              if (rank++ < kStage) {
-                s_cand[rl * kStage + rank - 1] = entry;
-              } else {  // LDS slots of this row full: append directly
-                const int64_t row = row0 + rl;
-                const uint32_t pos = atomicAdd(&p.cand_n[row], 1u);
-                if (pos < kCand) p.cand[row * kCand + pos] = entry;
-              }
-            }
-            atomicMin(&s_clo[rl], lo_k);
-            atomicMax(&s_chi[rl], hi_k);
+          bool above = false, inside = ok;
+          if (MODE != MODE_HIST0) {  // level 0: the interval is everything
+            above = ok && sc > shi[rb2];
+            inside = ok && !above && sc >= slo[rb2];
+            nacc[rb2] += above ? 1u : 0u;
+          }
+          if (TOPP && ref[rb2] >= 0.0 && ok) {
+            const double mt = mass_term(sc, p.tau, ref[rb2]);
+            if (MODE == MODE_HIST0) zacc[rb2] += mt;
+            if (above) macc[rb2] += mt;
+          }
+          if (HIST) {
+            const int bn = inside ? bin_of(sc, bmul[rb2], badd[rb2]) : kBins;
+            atomicAdd(&s_hist[rl * HS + bn], 1u);
           }
         }
-        continue;
-      }
-      if (MODE == MODE_EMIT) {
-        uint32_t wsel = 0u, wtie = 0u;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
-          const bool ok = elig(kl);
-          wsel |= (ok && acc[e] > ts[rb2]) ? 1u << kl : 0u;
-          wtie |= (ok && acc[e] == ts[rb2]) ? 1u << kl : 0u;
-        }
-        wsel |= __shfl_xor(wsel, 32);
-        wtie |= __shfl_xor(wtie, 32);
-        if (!tiep[rb2]) wsel |= wtie;
-        if (g == 0) {
-          const int64_t row = row0 + rb2 * 32 + ln;
-          p.bsel[row * p.W + kb / 32] = wsel;
-          if (tiep[rb2]) p.btie[row * p.W + kb / 32] = wtie;
-        }
-        continue;
-      }
-      const int rl = rb2 * 32 + ln;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
-        const float sc = acc[e];
-        const bool ok = elig(kl);
-        bool above = false, inside = ok;
-        if (MODE != MODE_HIST0) {  // level 0: the interval is everything
-          above = ok && sc > shi[rb2];
-          inside = ok && !above && sc >= slo[rb2];
-          nacc[rb2] += above ? 1u : 0u;
-        }
-        if (TOPP && ref[rb2] >= 0.0 && ok) {
-          const double mt = mass_term(sc, p.tau, ref[rb2]);
-          if (MODE == MODE_HIST0) zacc[rb2] += mt;
-          if (above) macc[rb2] += mt;
-        }
-        if (HIST) {
-          const int bn = inside ? bin_of(sc, bmul[rb2], badd[rb2]) : kBins;
-          atomicAdd(&s_hist[rl * HS + bn], 1u);
-        }
-      }
+      };
+      if (full) rowproc(true);
+      else rowproc(false);
     }
   };
   if (MODE == MODE_SAMPLE) {

@@ -195,7 +195,8 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
   auto issue_tile = [&](int t, int st) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const uint32_t r = static_cast<uint32_t>(min(max(nid[u], 0), N - 1));  // memory safety only
+      // Ids outside [0, N) (invalid input) read row N - 1: memory safety only.
+      const uint32_t r = min(static_cast<uint32_t>(nid[u]), static_cast<uint32_t>(N - 1));
       uint16_t* kd = kbuf(st) + (wave * U + u) * 64 * 8;
       uint16_t* vd = vbuf(st) + (wave * U + u) * 64 * 8;
       gather16_to_lds(krs, __umul24(r, k_rowb) + 16u * gcol(u), kd);
@@ -226,9 +227,6 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
   const int vhalf = (lane >> 4) & 1;
 
   auto step = [&](const int t, const int st) __attribute__((always_inline)) {
-    // Tile t has landed, and the ids of tile t+1 (issued right after it) too;
-    // the barrier (no fence: all LDS traffic here is waited for explicitly)
-    // also guarantees every wave is done reading the other stage.
     // Tile t has landed, and the ids of tile t+1 (issued right after it) too;
     // the barrier (no fence: all LDS traffic here is waited for explicitly)
     // also guarantees every wave is done reading the other stage.
@@ -275,10 +273,10 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
     float x[16];
 #pragma unroll
     for (int e = 0; e < 16; ++e) x[e] = __builtin_fmaf(sacc[e], scale_log2, -m_run);
-    float xmax = x[0];
+    // The test is wave-wide, so each lane checks only its own 16 keys.
+    float xmax = fmaxf(x[0], x[1]);
 #pragma unroll
-    for (int e = 1; e < 16; e += 2) xmax = fmaxf(xmax, fmaxf(x[e], x[e + 1]));
-    xmax = wave_max_xor32(xmax);
+    for (int e = 2; e < 16; e += 2) xmax = fmaxf(xmax, fmaxf(x[e], x[e + 1]));
     if (__any(!(xmax <= 8.0f))) {
       float tmax = kNegInf;
 #pragma unroll
@@ -295,17 +293,26 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
 #pragma unroll
       for (int e = 0; e < 16; ++e) x[e] = __builtin_fmaf(sacc[e], scale_log2, -m_sub);
     }
-    float psum = 0.0f;
     f32x8 pf[2];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const float p = __builtin_amdgcn_exp2f(x[e]);
-      psum += p;
-      pf[e >> 3][e & 7] = p;
-    }
-    l_run += psum;
+    for (int e = 0; e < 16; ++e) pf[e >> 3][e & 7] = __builtin_amdgcn_exp2f(x[e]);
     const bf16x8 pb0 = __builtin_convertvector(pf[0], bf16x8);
     const bf16x8 pb1 = __builtin_convertvector(pf[1], bf16x8);
+    // The normaliser sums the bf16 weights that enter P V, two per dot2.
+    // (Pairs are taken with shufflevector: reading them through a bit_cast
+    // of the 8-vector has been miscompiled.)
+    const bf16x2 one2 = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+    auto dot_pair = [&](const bf16x2 pr) __attribute__((always_inline)) {
+      l_run = __builtin_amdgcn_fdot2_f32_bf16(pr, one2, l_run, false);
+    };
+    dot_pair(__builtin_shufflevector(pb0, pb0, 0, 1));
+    dot_pair(__builtin_shufflevector(pb0, pb0, 2, 3));
+    dot_pair(__builtin_shufflevector(pb0, pb0, 4, 5));
+    dot_pair(__builtin_shufflevector(pb0, pb0, 6, 7));
+    dot_pair(__builtin_shufflevector(pb1, pb1, 0, 1));
+    dot_pair(__builtin_shufflevector(pb1, pb1, 2, 3));
+    dot_pair(__builtin_shufflevector(pb1, pb1, 4, 5));
+    dot_pair(__builtin_shufflevector(pb1, pb1, 6, 7));
 
     // O^T += V_tile^T P^T; the V^T operand comes from transposing LDS reads.
     const char* vb = reinterpret_cast<const char*>(vbuf(st));

@@ -63,6 +63,15 @@ __device__ __forceinline__ void gather16_to_lds(__amdgpu_buffer_rsrc_t rsrc, uin
 #endif
 }
 
+// 4-byte copy per lane of a list entry to LDS through the list's buffer
+// resource: offsets past the list read 0, so no index can leave the list.
+__device__ __forceinline__ void ids_to_lds(__amdgpu_buffer_rsrc_t rsrc, uint32_t voff,
+                                           void* lds_base) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, LDS_PTR(void, lds_base), 4, voff, 0, 0, 0);
+#endif
+}
+
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -202,9 +211,8 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
       gather16_to_lds(krs, __umul24(r, k_rowb) + 16u * gcol(u), kd);
       gather16_to_lds(vrs, __umul24(r, v_rowb) + 16u * gcol(u), vd);
     }
-    if (wave == 0)  // the tile's key ids (clamped to the list; entries past count are masked)
-      __builtin_amdgcn_global_load_lds(list + min(tile_of(t) * kTile + lane, count - 1),
-                                       LDS_PTR(void, ibuf(st)), 4, 0, 0);
+    if (wave == 0)  // the tile's key ids (past count: 0, and masked)
+      ids_to_lds(lrs, static_cast<uint32_t>(tile_of(t) * kTile + lane) * 4u, ibuf(st));
   };
 
   f32x16 oacc[DB];

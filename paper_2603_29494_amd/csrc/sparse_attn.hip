@@ -79,7 +79,9 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-template <int D>
+// SAME_STRIDE: K and V rows have the same stride, so a gathered row's K and V
+// offsets coincide.
+template <int D, bool SAME_STRIDE>
 __global__ __launch_bounds__(kThreads) void k_sparse_attn(
     const uint16_t* __restrict__ q, int64_t q_sB, int64_t q_sH, int64_t q_sN,
     const uint16_t* __restrict__ k, int64_t k_sB, int64_t k_sH, int64_t k_sN,
@@ -146,9 +148,13 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
     const int x = t + t_rot;
     return x >= ntiles ? x - ntiles : x;
   };
-  // Reads of the list past `count` return 0 (buffer range check).
-  const __amdgpu_buffer_rsrc_t lrs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(list), 0, count * 4, 0x00020000);
+  // The list entries of tile t as a buffer resource (scalar work only, so
+  // that per-lane offsets stay loop-invariant); reads past the list return 0.
+  auto tile_rsrc = [&](int t) __attribute__((always_inline)) {
+    const int e0 = tile_of(t) * kTile;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(list) + e0, 0,
+                                             max(count - e0, 0) * 4, 0x00020000);
+  };
 
   // K and V of this head as buffer resources: gathers use 32-bit byte offsets
   // (row * row_bytes + 16 * chunk; the host checks that a head spans < 2 GiB).
@@ -197,22 +203,25 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
   int nid[U];  // key ids of the next tile to issue (raw; clamped when used)
 
   auto load_ids = [&](int t) __attribute__((always_inline)) {
+    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(t);
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-      nid[u] = __builtin_amdgcn_raw_buffer_load_b32(lrs, (tile_of(t) * kTile + grow(u)) * 4, 0, 0);
+    for (int u = 0; u < U; ++u) nid[u] = __builtin_amdgcn_raw_buffer_load_b32(rs, grow(u) * 4, 0, 0);
   };
   auto issue_tile = [&](int t, int st) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      // Ids outside [0, N) (invalid input) read row N - 1: memory safety only.
-      const uint32_t r = min(static_cast<uint32_t>(nid[u]), static_cast<uint32_t>(N - 1));
+      // Valid ids are below N < 2^24 (a head spans < 2 GiB), as __umul24
+      // needs; an invalid id reads some row of this head or zeros, never
+      // outside it (buffer range check).
+      const uint32_t r = static_cast<uint32_t>(nid[u]);
       uint16_t* kd = kbuf(st) + (wave * U + u) * 64 * 8;
       uint16_t* vd = vbuf(st) + (wave * U + u) * 64 * 8;
-      gather16_to_lds(krs, __umul24(r, k_rowb) + 16u * gcol(u), kd);
-      gather16_to_lds(vrs, __umul24(r, v_rowb) + 16u * gcol(u), vd);
+      const uint32_t ko = __umul24(r, k_rowb) + 16u * gcol(u);
+      gather16_to_lds(krs, ko, kd);
+      gather16_to_lds(vrs, SAME_STRIDE ? ko : __umul24(r, v_rowb) + 16u * gcol(u), vd);
     }
     if (wave == 0)  // the tile's key ids (past count: 0, and masked)
-      ids_to_lds(lrs, static_cast<uint32_t>(tile_of(t) * kTile + lane) * 4u, ibuf(st));
+      ids_to_lds(tile_rsrc(t), static_cast<uint32_t>(lane) * 4u, ibuf(st));
   };
 
   f32x16 oacc[DB];
@@ -274,18 +283,42 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
       }
     }
     // Lazy rescaling: x = s * scale - m_run (log2 units) is what exp2 needs
-    // anyway; the reference m_run of a row moves only when some x exceeds 8
-    // (so P stays <= 256, harmless in bf16 / fp32), and O, l are rescaled
-    // only when some row of the wave moved.  m_run = -inf (nothing seen yet)
-    // takes the same slow path.
+    // anyway, and the weights 2^x are computed first.  Their tile sum (of the
+    // bf16 weights that enter P V, two per dot2) bounds every weight, so a sum
+    // <= 256 on all lanes shows that no weight exceeds 256 (harmless in bf16 /
+    // fp32) and the reference m_run stays.  Otherwise (a new maximum, or
+    // m_run = -inf: nothing seen yet) the rows whose maximum grew by more than
+    // 8 move their reference, O and l are rescaled, and the weights are
+    // recomputed.
     float x[16];
 #pragma unroll
     for (int e = 0; e < 16; ++e) x[e] = __builtin_fmaf(sacc[e], scale_log2, -m_run);
-    // The test is wave-wide, so each lane checks only its own 16 keys.
-    float xmax = fmaxf(x[0], x[1]);
+    bf16x8 pb0, pb1;
+    auto weights = [&]() __attribute__((always_inline)) {
+      f32x8 pf[2];
 #pragma unroll
-    for (int e = 2; e < 16; e += 2) xmax = fmaxf(xmax, fmaxf(x[e], x[e + 1]));
-    if (__any(!(xmax <= 8.0f))) {
+      for (int e = 0; e < 16; ++e) pf[e >> 3][e & 7] = __builtin_amdgcn_exp2f(x[e]);
+      pb0 = __builtin_convertvector(pf[0], bf16x8);
+      pb1 = __builtin_convertvector(pf[1], bf16x8);
+      // Pairs are taken with shufflevector: reading them through a bit_cast of
+      // the 8-vector has been miscompiled.
+      const bf16x2 one2 = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+      float sum = 0.0f;
+      auto dot_pair = [&](const bf16x2 pr) __attribute__((always_inline)) {
+        sum = __builtin_amdgcn_fdot2_f32_bf16(pr, one2, sum, false);
+      };
+      dot_pair(__builtin_shufflevector(pb0, pb0, 0, 1));
+      dot_pair(__builtin_shufflevector(pb0, pb0, 2, 3));
+      dot_pair(__builtin_shufflevector(pb0, pb0, 4, 5));
+      dot_pair(__builtin_shufflevector(pb0, pb0, 6, 7));
+      dot_pair(__builtin_shufflevector(pb1, pb1, 0, 1));
+      dot_pair(__builtin_shufflevector(pb1, pb1, 2, 3));
+      dot_pair(__builtin_shufflevector(pb1, pb1, 4, 5));
+      dot_pair(__builtin_shufflevector(pb1, pb1, 6, 7));
+      return sum;
+    };
+    float tsum = weights();
+    if (__any(!(tsum <= 256.0f))) {
       float tmax = kNegInf;
 #pragma unroll
       for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, sacc[e]);
@@ -300,27 +333,9 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
       const float m_sub = m_run == kNegInf ? 0.0f : m_run;
 #pragma unroll
       for (int e = 0; e < 16; ++e) x[e] = __builtin_fmaf(sacc[e], scale_log2, -m_sub);
+      tsum = weights();
     }
-    f32x8 pf[2];
-#pragma unroll
-    for (int e = 0; e < 16; ++e) pf[e >> 3][e & 7] = __builtin_amdgcn_exp2f(x[e]);
-    const bf16x8 pb0 = __builtin_convertvector(pf[0], bf16x8);
-    const bf16x8 pb1 = __builtin_convertvector(pf[1], bf16x8);
-    // The normaliser sums the bf16 weights that enter P V, two per dot2.
-    // (Pairs are taken with shufflevector: reading them through a bit_cast
-    // of the 8-vector has been miscompiled.)
-    const bf16x2 one2 = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
-    auto dot_pair = [&](const bf16x2 pr) __attribute__((always_inline)) {
-      l_run = __builtin_amdgcn_fdot2_f32_bf16(pr, one2, l_run, false);
-    };
-    dot_pair(__builtin_shufflevector(pb0, pb0, 0, 1));
-    dot_pair(__builtin_shufflevector(pb0, pb0, 2, 3));
-    dot_pair(__builtin_shufflevector(pb0, pb0, 4, 5));
-    dot_pair(__builtin_shufflevector(pb0, pb0, 6, 7));
-    dot_pair(__builtin_shufflevector(pb1, pb1, 0, 1));
-    dot_pair(__builtin_shufflevector(pb1, pb1, 2, 3));
-    dot_pair(__builtin_shufflevector(pb1, pb1, 4, 5));
-    dot_pair(__builtin_shufflevector(pb1, pb1, 6, 7));
+    l_run += tsum;
 
     // O^T += V_tile^T P^T; the V^T operand comes from transposing LDS reads.
     const char* vb = reinterpret_cast<const char*>(vbuf(st));
@@ -411,18 +426,20 @@ hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream) {
   const uint16_t* k = static_cast<const uint16_t*>(a.k.ptr);
   const uint16_t* v = static_cast<const uint16_t*>(a.v.ptr);
   uint16_t* o = static_cast<uint16_t*>(a.o);
+  const bool same = a.k.sN == a.v.sN;
+  auto launch = [&](auto kernel) {
+    hipLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, stream, q, a.q.sB, a.q.sH, a.q.sN, k,
+                       a.k.sB, a.k.sH, a.k.sN, v, a.v.sB, a.v.sH, a.v.sN, o, a.o_sB, a.o_sH,
+                       a.o_sN, a.lse, a.idx, a.counts, a.cap, static_cast<int32_t>(Hq), group,
+                       static_cast<int32_t>(N), P, Np, chunks, a.causal, scale_log2, total,
+                       per_xcd);
+  };
   if (D == 128) {
-    hipLaunchKernelGGL(k_sparse_attn<128>, grid, dim3(kThreads), 0, stream, q, a.q.sB, a.q.sH,
-                       a.q.sN, k, a.k.sB, a.k.sH, a.k.sN, v, a.v.sB, a.v.sH, a.v.sN, o, a.o_sB,
-                       a.o_sH, a.o_sN, a.lse, a.idx, a.counts, a.cap, static_cast<int32_t>(Hq),
-                       group, static_cast<int32_t>(N), P, Np, chunks, a.causal, scale_log2, total,
-                       per_xcd);
+    if (same) launch(k_sparse_attn<128, true>);
+    else launch(k_sparse_attn<128, false>);
   } else {
-    hipLaunchKernelGGL(k_sparse_attn<64>, grid, dim3(kThreads), 0, stream, q, a.q.sB, a.q.sH,
-                       a.q.sN, k, a.k.sB, a.k.sH, a.k.sN, v, a.v.sB, a.v.sH, a.v.sN, o, a.o_sB,
-                       a.o_sH, a.o_sN, a.lse, a.idx, a.counts, a.cap, static_cast<int32_t>(Hq),
-                       group, static_cast<int32_t>(N), P, Np, chunks, a.causal, scale_log2, total,
-                       per_xcd);
+    if (same) launch(k_sparse_attn<64, true>);
+    else launch(k_sparse_attn<64, false>);
   }
   return hipGetLastError();
 }

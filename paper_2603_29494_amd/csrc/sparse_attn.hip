@@ -42,14 +42,19 @@ typedef short i16x8 __attribute__((ext_vector_type(8)));
 #define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
 
 
-// Chunk swizzle: 16-byte chunk c of row r lives at chunk c ^ swz(r).  swz is
-// a bijection on the row's low bits, so 16 consecutive rows reading the same
-// chunk hit 16 different chunks; r % 4 drives output bits 1-2, so 4
-// consecutive rows x 2 adjacent chunks land on 8 distinct chunks.
+// Chunk swizzle: 16-byte chunk c of row r lives at chunk c ^ swz(r).  LDS has
+// 64 banks of 4 bytes; a 16-byte read serves 16 lanes per cycle, an 8-byte
+// read 32.  K reads (16 lanes = 16 consecutive rows, one logical chunk) need
+// swz to separate the rows that share banks: a bijection on r % 16 for
+// 256-byte rows, on (r / 2) % 8 for 128-byte rows (two rows per bank line).
+// Transposing V reads (32 lanes = 4 consecutive rows x 4 chunks x 2 halves)
+// need the row's contribution to move whole groups of 4 chunks: r % 4 drives
+// bits 2-3 (D = 128), or r / 2 % 2 drives bit 2 across the rows that share
+// banks (D = 64).  Both read patterns are then free of bank conflicts.
 template <int D>
 __host__ __device__ __forceinline__ constexpr int swz(int r) {
-  if constexpr (D == 128) return ((r & 3) << 1) | ((r >> 2) & 1) | (r & 8);
-  else return ((r & 3) << 1) | ((r >> 2) & 1);
+  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  else return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
 }
 
 // 16-byte copy per lane from a buffer (byte offset voff) to LDS (destination:

@@ -883,6 +883,11 @@ __global__ __launch_bounds__(256) void k_resolve_cand(SelParams p) {
 // 32-key word per step into LDS at its prefix position, then the wave copies
 // the staged indices out contiguously.
 // ---------------------------------------------------------------------------
+// Bitmask words (64 per chunk, one per lane) whose loads are in flight
+// together: the row's chunks are processed strictly in order, but their
+// loads do not wait for one another.
+constexpr int kCompactBatch = 8;
+
 __global__ __launch_bounds__(64) void k_compact(SelParams p) {
   const int64_t r = blockIdx.x;
   const RowState& s = p.st[r];
@@ -892,51 +897,63 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
   const int nw = (L + 31) / 32;
   const bool tiep = s.tie_partial;
   const int k_eq = s.k_eq;
+  const uint32_t* bsel = p.bsel + r * p.W;
+  const uint32_t* btie = p.btie + r * p.W;
   int base = 0;      // entries written so far
   int ties_seen = 0; // tied keys met so far (ascending index)
   int32_t* out = p.idx + r * p.cap;
-  for (int w0 = 0; w0 < nw; w0 += 64) {
-    const int wd = w0 + lane;
-    const bool valid = wd < nw;
-    uint32_t m = valid ? p.bsel[r * p.W + wd] : 0u;
-    if (tiep) {  // uniform per row: keep only the first k_eq tied keys
-      const uint32_t tw = valid ? p.btie[r * p.W + wd] : 0u;
-      const int nt = __builtin_popcount(tw);
-      int incl = nt;
+  for (int c0 = 0; c0 < nw; c0 += 64 * kCompactBatch) {
+    uint32_t mb[kCompactBatch], tb[kCompactBatch];
+#pragma unroll
+    for (int j = 0; j < kCompactBatch; ++j) {
+      const int wd = c0 + 64 * j + lane;
+      mb[j] = wd < nw ? bsel[wd] : 0u;
+      tb[j] = (tiep && wd < nw) ? btie[wd] : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < kCompactBatch; ++j) {
+      const int wd = c0 + 64 * j + lane;
+      if (c0 + 64 * j >= nw) break;  // uniform
+      uint32_t m = mb[j];
+      if (tiep) {  // uniform per row: keep only the first k_eq tied keys
+        const uint32_t tw = tb[j];
+        const int nt = __builtin_popcount(tw);
+        int incl = nt;
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(incl, o);
+          if (lane >= o) incl += y;
+        }
+        int room = k_eq - (ties_seen + incl - nt);  // ties this lane may still keep
+        uint32_t t2 = tw;
+        while (t2 && room > 0) {
+          const uint32_t bit = t2 & (~t2 + 1u);
+          m |= bit;
+          t2 ^= bit;
+          --room;
+        }
+        ties_seen += __shfl(incl, 63);
+      }
+      if (wd < nw && L - 32 * wd < 32) m &= (1u << (L - 32 * wd)) - 1u;
+      const int nb = __builtin_popcount(m);
+      int pre = nb;
       for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(incl, o);
-        if (lane >= o) incl += y;
+        const int y = __shfl_up(pre, o);
+        if (lane >= o) pre += y;
       }
-      int room = k_eq - (ties_seen + incl - nt);  // ties this lane may still keep
-      uint32_t t2 = tw;
-      while (t2 && room > 0) {
-        const uint32_t bit = t2 & (~t2 + 1u);
-        m |= bit;
-        t2 ^= bit;
-        --room;
+      const int total = __shfl(pre, 63);
+      int pos = pre - nb;
+      uint32_t mm = m;
+      while (mm) {
+        const int bit = __builtin_ctz(mm);
+        mm &= mm - 1;
+        stage[pos++] = 32 * wd + bit;
       }
-      ties_seen += __shfl(incl, 63);
+      __syncthreads();
+      for (int t = lane; t < total; t += 64)
+        if (base + t < p.cap) out[base + t] = stage[t];
+      __syncthreads();
+      base += total;
     }
-    if (valid && L - 32 * wd < 32) m &= (1u << (L - 32 * wd)) - 1u;
-    const int nb = __builtin_popcount(m);
-    int pre = nb;
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(pre, o);
-      if (lane >= o) pre += y;
-    }
-    const int total = __shfl(pre, 63);
-    int pos = pre - nb;
-    uint32_t mm = m;
-    while (mm) {
-      const int bit = __builtin_ctz(mm);
-      mm &= mm - 1;
-      stage[pos++] = 32 * wd + bit;
-    }
-    __syncthreads();
-    for (int t = lane; t < total; t += 64)
-      if (base + t < p.cap) out[base + t] = stage[t];
-    __syncthreads();
-    base += total;
   }
   const int n = min(base, static_cast<int>(p.cap));
   for (int t = n + lane; t < p.cap; t += 64) out[t] = -1;

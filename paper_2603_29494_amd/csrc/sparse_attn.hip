@@ -32,10 +32,13 @@ constexpr int kRows = 64;     // query rows per workgroup
 constexpr int kTile = 64;     // keys per gathered tile
 constexpr int kThreads = 256;
 constexpr int kStages = 2;
-// Nominal time per tile and workgroup in ticks of the 100 MHz constant clock
-// (two workgroups per CU at the 75k DiT shape); it sets the speed of the
-// sweep below.
-constexpr unsigned long long kTileTicks = 165;
+// Tiles processed by this kernel on each XCD since the library was loaded
+// (wraps at 2^32).  It is the clock of the tile order below: a locality hint
+// only, so concurrent calls sharing it affect speed, never results.
+__device__ unsigned int g_herd_tiles[8];
+// Tiles counted per update of that counter: updates to one address serialise
+// in L2, so they must be rare next to the gathers.
+constexpr unsigned int kHerdBatch = 16;
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
@@ -94,7 +97,7 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
     uint16_t* __restrict__ o, int64_t o_sB, int64_t o_sH, int64_t o_sN, float* __restrict__ lse,
     const int32_t* __restrict__ idx, const int32_t* __restrict__ counts, int64_t cap, int32_t Hq,
     int32_t group, int32_t N, int32_t P, int32_t Np, int32_t chunks, int32_t causal,
-    float scale_log2, int64_t total, int64_t per_xcd) {
+    float scale_log2, int64_t total, int64_t per_xcd, int32_t herd_slots) {
   constexpr int CH = D / 8;                 // 16-byte chunks per row
   constexpr int U = kTile * CH / kThreads;  // direct-load instructions per wave per matrix
   constexpr int DS = D / 16;                // MFMA K-steps over the head dimension
@@ -135,16 +138,20 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
   // than an XCD's L2 holds; the workgroups running together on an XCD share
   // L2 hits only if they gather from the same key range at the same time.
   // Lists are ascending, so a workgroup's position in its list is a position
-  // in key space: each workgroup starts at the tile given by a chip-wide
-  // clock (period = the nominal time of its whole list) and wraps around, so
-  // workgroups that run together sweep the keys together.  The order of the
-  // tiles changes only the order of the softmax sums (results can differ
-  // between runs within fp32 rounding).
+  // in key space.  Every workgroup counts its tiles into its XCD's counter;
+  // that count over the XCD's workgroup slots is the mean position of the
+  // workgroups running there, and a new workgroup starts at that tile (then
+  // wraps around), so the workgroups on an XCD sweep the keys together at
+  // their actual pace.  The order of the tiles changes only the order of the
+  // softmax sums (results can differ between runs within fp32 rounding).
+  const int xcd = blockIdx.x & 7;  // the hardware deals workgroup x to XCD x % 8
   __shared__ int s_rot;
   if (threadIdx.x == 0) {
-    const unsigned long long now = __builtin_amdgcn_s_memrealtime();
-    const unsigned long long per = static_cast<unsigned long long>(ntiles) * kTileTicks;
-    s_rot = ntiles > 1 ? static_cast<int>((now % per) / kTileTicks) : 0;
+    const unsigned int herd =
+        __hip_atomic_load(&g_herd_tiles[xcd], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_rot = ntiles > 1 ? static_cast<int>((herd / static_cast<unsigned int>(herd_slots)) %
+                                          static_cast<unsigned int>(ntiles))
+                       : 0;
   }
   __syncthreads();
   const int t_rot = __builtin_amdgcn_readfirstlane(s_rot);
@@ -254,6 +261,9 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
     // also guarantees every wave is done reading the other stage.
     wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
+    if (wave == 0 && lane == 0 && (t % kHerdBatch) == kHerdBatch - 1)
+      __hip_atomic_fetch_add(&g_herd_tiles[xcd], kHerdBatch, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
     if (t + 1 < ntiles) issue_tile(t + 1, st ^ 1);
     load_ids(t + 2);  // past the list these read 0
 
@@ -366,6 +376,10 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
     if (t + 1 < ntiles) step(t + 1, 1);
   }
 
+  if (wave == 0 && lane == 0 && ntiles % kHerdBatch != 0)
+    __hip_atomic_fetch_add(&g_herd_tiles[xcd], static_cast<unsigned int>(ntiles) % kHerdBatch,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
   // Merge the two key halves (kw = 1 hands its state to kw = 0 through LDS).
   l_run += __shfl_xor(l_run, 32);
   wait_vmcnt<0>();  // no gather may still be landing in the buffers reused below
@@ -432,21 +446,23 @@ hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream) {
   const uint16_t* v = static_cast<const uint16_t*>(a.v.ptr);
   uint16_t* o = static_cast<uint16_t*>(a.o);
   const bool same = a.k.sN == a.v.sN;
-  auto launch = [&](auto kernel) {
+  auto launch = [&](auto kernel) -> hipError_t {
+    // Workgroup slots per XCD (resident workgroups per CU x CUs per XCD).
+    int dev = 0, cus = 0, per_cu = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0);
+    if (e != hipSuccess) return e;
+    const int32_t slots = max(1, per_cu * cus / 8);
     hipLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, stream, q, a.q.sB, a.q.sH, a.q.sN, k,
                        a.k.sB, a.k.sH, a.k.sN, v, a.v.sB, a.v.sH, a.v.sN, o, a.o_sB, a.o_sH,
                        a.o_sN, a.lse, a.idx, a.counts, a.cap, static_cast<int32_t>(Hq), group,
                        static_cast<int32_t>(N), P, Np, chunks, a.causal, scale_log2, total,
-                       per_xcd);
+                       per_xcd, slots);
+    return hipGetLastError();
   };
-  if (D == 128) {
-    if (same) launch(k_sparse_attn<128, true>);
-    else launch(k_sparse_attn<128, false>);
-  } else {
-    if (same) launch(k_sparse_attn<64, true>);
-    else launch(k_sparse_attn<64, false>);
-  }
-  return hipGetLastError();
+  if (D == 128) return same ? launch(k_sparse_attn<128, true>) : launch(k_sparse_attn<128, false>);
+  return same ? launch(k_sparse_attn<64, true>) : launch(k_sparse_attn<64, false>);
 }
 
 }  // namespace vecattn

@@ -2,7 +2,8 @@
 //
 // One workgroup (4 waves) owns up to 64 query rows of one query block of one
 // head and walks the block's index list I[b,h,i,0:C) in tiles of 64 keys
-// (starting at a clock-chosen tile and wrapping around, see below).
+// (starting at the tile where the workgroups running on its XCD are, and
+// wrapping around; see below).
 // The K and V rows of a tile are gathered straight from global memory into
 // LDS (global_load_lds, 16 B per lane, no register staging) two tiles deep,
 // stored row-major with an XOR swizzle of their 16-byte chunks so that both
@@ -33,8 +34,8 @@ constexpr int kTile = 64;     // keys per gathered tile
 constexpr int kThreads = 256;
 constexpr int kStages = 2;
 // Tiles processed by this kernel on each XCD since the library was loaded
-// (wraps at 2^32).  It is the clock of the tile order below: a locality hint
-// only, so concurrent calls sharing it affect speed, never results.
+// (wraps at 2^32).  It paces the tile order below: a locality hint only, so
+// concurrent calls sharing it affect speed, never results.
 __device__ unsigned int g_herd_tiles[8];
 // Tiles counted per update of that counter: updates to one address serialise
 // in L2, so they must be rare next to the gathers.
@@ -276,6 +277,24 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
       sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), qf[s2], sacc,
                                                      0, 0, 0);
     }
+    // The V^T operands (transposing LDS reads) are fetched now, so that their
+    // latency hides behind the score MFMAs and the softmax.
+    const char* vb = reinterpret_cast<const char*>(vbuf(st));
+    i16x8 vfrag[DB][2];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int d = 32 * db + 16 * vhalf + 4 * tp;  // first of the 4 head-dim values addressed
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const int k0 = 32 * kw + 16 * ks + 4 * g + tq;  // key row this lane addresses
+        const int k1 = k0 + 8;
+        const char* a0 = vb + k0 * RB + 16 * ((d >> 3) ^ swz<D>(k0)) + 8 * ((d >> 2) & 1);
+        const char* a1 = vb + k1 * RB + 16 * ((d >> 3) ^ swz<D>(k1)) + 8 * ((d >> 2) & 1);
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(i16x4, a0));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(i16x4, a1));
+        vfrag[db][ks] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+    }
 
     // Masks are needed only on the list's last tile and, when causal, on tiles
     // reaching past this wave's first row (lists are ascending).
@@ -352,24 +371,13 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
     }
     l_run += tsum;
 
-    // O^T += V_tile^T P^T; the V^T operand comes from transposing LDS reads.
-    const char* vb = reinterpret_cast<const char*>(vbuf(st));
+    // O^T += V_tile^T P^T.
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const int d = 32 * db + 16 * vhalf + 4 * tp;  // first of the 4 head-dim values addressed
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const int k0 = 32 * kw + 16 * ks + 4 * g + tq;  // key row this lane addresses
-        const int k1 = k0 + 8;
-        const char* a0 = vb + k0 * RB + 16 * ((d >> 3) ^ swz<D>(k0)) + 8 * ((d >> 2) & 1);
-        const char* a1 = vb + k1 * RB + 16 * ((d >> 3) ^ swz<D>(k1)) + 8 * ((d >> 2) & 1);
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(i16x4, a0));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(i16x4, a1));
-        const i16x8 av = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av),
+      for (int ks = 0; ks < 2; ++ks)
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vfrag[db][ks]),
                                                            ks ? pb1 : pb0, oacc[db], 0, 0, 0);
-      }
-    }
   };
   for (int t = 0; t < ntiles; t += 2) {
     step(t, 0);

@@ -329,15 +329,17 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     s_part[tid] = part;
     if (part) atomicOr(&s_any, 1);
   }
-  if (HIST)
-    for (int t = tid; t < kRowsWG * HS; t += kThreads) s_hist[t] = 0u;
   if (COL && tid < kRowsWG) {
     s_ccnt[tid] = 0u;
     s_clo[tid] = 0xFFFFFFFFu;
     s_chi[tid] = 0u;
   }
   __syncthreads();
-  if (!s_any) return;
+  if (!s_any) return;  // passes late in the refinement find most workgroups idle
+  if (HIST) {
+    for (int t = tid; t < kRowsWG * HS; t += kThreads) s_hist[t] = 0u;
+    __syncthreads();
+  }
 
   // This lane's two rows (rl = 32 * rb2 + ln): pooled query as the B operand
   // (head-dim slots 16s + 8g .. +7) and the row's interval in registers.
@@ -1097,7 +1099,9 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   const dim3 pgrid(static_cast<unsigned>(p.per_xcd * 8));
   const dim3 rgrid(static_cast<unsigned>(rows));
   const dim3 igrid(static_cast<unsigned>((rows + 255) / 256));
-  for (int round = 0; round < kRounds; ++round) {
+  // Only topP rows can be sent back for a second round (count above cap).
+  const int rounds = p.mode_topp ? kRounds : 1;
+  for (int round = 0; round < rounds; ++round) {
     hipLaunchKernelGGL(k_sel_init, igrid, dim3(256), 0, stream, p, round);
     if (round == 0 && !p.mode_topp) {
       score_pass<MODE_SAMPLE>(D, false, pgrid, p, stream);

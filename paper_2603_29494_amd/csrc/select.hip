@@ -35,7 +35,7 @@ namespace {
 constexpr int kRowsWG = 64;     // pooled rows per workgroup
 constexpr int kThreads = 256;
 constexpr int kBins = 256;
-constexpr int kLevels = 4;      // histogram refinements per round
+constexpr int kLevels = 6;      // histogram refinements per round (idle ones cost ~25 us)
 constexpr int kCand = 1024;     // candidate capacity per row
 constexpr int kRounds = 2;      // a topP row whose count exceeds cap reruns as topK(cap)
 
@@ -55,7 +55,7 @@ struct RowState {
   int k_eq;         // keys tied at t* that are kept
   int count;        // final count
   int clamped;      // 1 if the threshold selection was clamped to cap
-  int pad0;
+  int tie_interval; // 1: the keys tied at the cut are all those in [s_lo, s_hi]
   // Scores below are raw fp32 dot products <q_p, k_j> (the softmax scale tau
   // > 0 preserves their order; it enters only the topP masses).
   float s_lo, s_hi; // current interval: keys with s_lo <= s <= s_hi (exact float bounds)
@@ -191,6 +191,7 @@ __global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
   s.ref = static_cast<double>(p.tau) * static_cast<double>(cc);  // >= every tau * score
   s.tie_partial = 0;
   s.k_eq = 0;
+  s.tie_interval = 0;
   p.cand_n[r] = 0;
   p.cand_lohi[2 * r] = 0xFFFFFFFFu;
   p.cand_lohi[2 * r + 1] = 0u;
@@ -347,7 +348,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   bool part[2];
   int Lr[2];
   float slo[2], shi[2], bmul[2], badd[2], ts[2];
-  bool tiep[2];
+  bool tiep[2], tiei[2];
   double ref[2];  // < 0: no masses needed
 #pragma unroll
   for (int rb2 = 0; rb2 < 2; ++rb2) {
@@ -362,6 +363,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     badd[rb2] = s.badd;
     ts[rb2] = s.tstar;
     tiep[rb2] = s.tie_partial;
+    tiei[rb2] = s.tie_interval;
     ref[rb2] = (TOPP && s.topp) ? s.ref : -1.0;
     const u32x4* src = reinterpret_cast<const u32x4*>(p.qp + row * D);
 #pragma unroll
@@ -459,7 +461,9 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
             const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
             const bool ok = elig(kl);
             wsel |= (ok && acc[e] > ts[rb2]) ? 1u << kl : 0u;
-            wtie |= (ok && acc[e] == ts[rb2]) ? 1u << kl : 0u;
+            const bool tie = tiei[rb2] ? (acc[e] >= slo[rb2] && acc[e] <= shi[rb2])
+                                       : acc[e] == ts[rb2];
+            wtie |= (ok && tie) ? 1u << kl : 0u;
           }
           wsel |= __shfl_xor(wsel, 32);
           wtie |= __shfl_xor(wtie, 32);
@@ -730,8 +734,11 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
   if (inside <= static_cast<uint32_t>(kCand) || nl >= kLevels) {
     s.phase = PH_COLLECT;
   } else {
-    const float nlo = lo + static_cast<float>(ba) / inv;
-    const float nhi = lo + static_cast<float>(bb + 1) / inv;
+    // An end bin also holds the scores beyond the bin range (level 0 of topK
+    // rows bins a sampled bracket, not the whole range): the next level spans
+    // the chosen bins' actual extent, within the Cauchy-Schwarz bound.
+    const float nlo = ba == 0 ? fmaxf(s.s_lo, -top) : lo + static_cast<float>(ba) / inv;
+    const float nhi = bb == kBins - 1 ? fminf(s.s_hi, top) : lo + static_cast<float>(bb + 1) / inv;
     s.blo = nlo;
     s.binv = static_cast<float>(kBins) / fmaxf(nhi - nlo, FLT_MIN);
     s.badd = -nlo * s.binv;
@@ -746,32 +753,25 @@ __global__ __launch_bounds__(256) void k_resolve_cand(SelParams p) {
   const int64_t r = blockIdx.x;
   RowState& s = p.st[r];
   if (s.phase != PH_COLLECT) return;
-  __shared__ uint64_t key[kCand];
+  __shared__ uint64_t kin[kCand];  // candidates as collected
+  __shared__ uint64_t key[kCand];  // sorted, descending
   __shared__ int res[4];
   const int tid = threadIdx.x;
   const uint32_t nc_raw = p.cand_n[r];
   const int nc = static_cast<int>(min(nc_raw, static_cast<uint32_t>(kCand)));
-  int np2 = 1;
-  while (np2 < nc) np2 <<= 1;
-  for (int t = tid; t < np2; t += 256) key[t] = t < nc ? p.cand[r * kCand + t] : 0ull;
+  for (int t = tid; t < nc; t += 256) kin[t] = p.cand[r * kCand + t];
   __syncthreads();
-  // bitonic sort, descending
-  for (int k2 = 2; k2 <= np2; k2 <<= 1) {
-    for (int j = k2 >> 1; j > 0; j >>= 1) {
-      for (int t = tid; t < np2; t += 256) {
-        const int x = t ^ j;
-        if (x > t) {
-          const bool desc = (t & k2) == 0;
-          const uint64_t a = key[t], c = key[x];
-          if (desc ? (a < c) : (a > c)) {
-            key[t] = c;
-            key[x] = a;
-          }
-        }
-      }
-      __syncthreads();
-    }
+  // Counting sort: the keys (ordered score, complemented index) are distinct,
+  // so a candidate's place is the number of larger ones.  The reads of kin[j]
+  // are the same address across the workgroup (LDS broadcast).
+  for (int t = tid; t < nc; t += 256) {
+    const uint64_t mine = kin[t];
+    int rank = 0;
+#pragma unroll 4
+    for (int j = 0; j < nc; ++j) rank += kin[j] > mine ? 1 : 0;
+    key[rank] = mine;
   }
+  __syncthreads();
   // statistics of the final interval
   const int64_t bh = r / p.Np;
   (void)bh;
@@ -844,26 +844,15 @@ __global__ __launch_bounds__(256) void k_resolve_cand(SelParams p) {
         s.tstar = ord_val(p.cand_lohi[2 * r]);
         s.tie_partial = n_sel < static_cast<int>(nc_raw);
         s.k_eq = n_sel;
-      } else if (n_sel == 0) {
-        // nothing kept from the interval: cut just above it
-        s.tstar = nc > 0 ? ord_val(static_cast<uint32_t>(key[0] >> 32)) : FLT_MAX;
-        s.tie_partial = 1;
-        s.k_eq = 0;
       } else {
-        const int m = min(n_sel, max(nc, 1)) - 1;
-        const uint32_t tk = static_cast<uint32_t>(key[m] >> 32);
-        s.tstar = ord_val(tk);
-        // ties at t*: kept ones are sorted first by index
-        int kept_ties = 0, all_ties = 0;
-        for (int t = 0; t < nc; ++t) {
-          const uint32_t kk = static_cast<uint32_t>(key[t] >> 32);
-          if (kk == tk) {
-            ++all_ties;
-            if (t <= m) ++kept_ties;
-          }
-        }
-        s.tie_partial = kept_ties < all_ties;
-        s.k_eq = kept_ties;
+        // More than kCand distinct scores are left in an interval narrower
+        // than the refinement resolves (after kLevels levels: only for scores
+        // a few ulps apart, or the nothing-kept case): its keys count as
+        // tied at the cut and the first n_sel by index are kept.
+        s.tstar = s.s_hi;
+        s.tie_interval = 1;
+        s.tie_partial = 1;
+        s.k_eq = n_sel;
       }
       s.count = count;
       s.phase = PH_EMIT;

@@ -115,3 +115,23 @@ def test_selection_then_attention_end_to_end(gpu):
     o_ref, _ = oracle.sparse_attn(q, k, v, idx, cnt, 64, True)
     err = np.abs(o.float().cpu().numpy() - o_ref)
     assert err.max() <= 2e-2 and err.mean() <= 2e-3
+
+
+@pytest.mark.parametrize("sampled_high", [False, True])
+def test_level0_interval_from_misleading_sample(gpu, sampled_high):
+    # The first interval of a topK row is estimated from every 16th 32-key
+    # block.  Shifting only the unsampled blocks' keys (or only the sampled
+    # ones) toward the queries' direction puts the true cut above (or below)
+    # that estimate; the refinement must still find the exact set.
+    rng = np.random.default_rng(11 + int(sampled_high))
+    N, D, block = 8192, 128, 64
+    u = rng.standard_normal(D).astype(np.float32)
+    u /= np.linalg.norm(u)
+    q = rng.standard_normal((1, 2, N, D)).astype(np.float32) + 2.0 * u
+    k = rng.standard_normal((1, 2, N, D)).astype(np.float32)
+    sampled = ((np.arange(N) // 32) % 16) == 0
+    shifted = sampled if sampled_high else ~sampled
+    k[:, :, shifted] += 3.0 * u
+    qb, kb = synth.to_bf16_bits(q), synth.to_bf16_bits(k)
+    idx, cnt, cap, _ = run(qb, kb, block, oracle.TOPK, 0.1, False)
+    check_rows(qb, kb, block, oracle.TOPK, 0.1, False, cap, idx, cnt, all_rows(qb, block))

@@ -11,11 +11,14 @@
 //            in a 256-bin LDS histogram, keys above are counted (and their
 //            softmax mass summed for topP).  A resolve kernel picks the bin
 //            range that must hold the cut, which becomes the next interval.
-//   COLLECT  once the interval holds at most kCand keys, their (score, index)
-//            pairs are gathered; a resolve kernel sorts them and fixes the cut
-//            score t* and how many keys tied at t* are kept (lowest indices).
-//   EMIT     one more pass sets a bit per kept key (score > t*), and one per
-//            key tied at t* when only some ties are kept.
+//   COLLECT  once the interval holds at most kCand keys: a bit per key at or
+//            above the interval, and the (score, index) pairs of the keys
+//            inside it; a resolve kernel ranks those candidates, fixes the cut
+//            score t* and how many keys tied at t* are kept (lowest indices),
+//            and clears the bits of the rejected ones.
+//   EMIT     only for rows whose interval still held more than kCand keys:
+//            one more pass sets a bit per kept key (score > t*), and one per
+//            key tied at the cut when only some ties are kept.
 //   COMPACT  bitmasks -> ascending index lists and counts.
 // All passes compute every score with the same MFMA sequence, so a key's
 // score is bit-identical in every pass.

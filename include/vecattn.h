@@ -56,8 +56,9 @@ typedef enum vecattn_sel_mode {
   VECATTN_SEL_TOPP = 1, /* param = mass p in (0, 1]: block i keeps the shortest
                            prefix, in (score desc, index asc) order, whose softmax
                            mass over its eligible keys is >= p */
-  VECATTN_SEL_MINS = 2  /* param = alpha >= 0, Eq. 3; not built: returns
-                           VECATTN_ERR_UNSUPPORTED */
+  VECATTN_SEL_MINS = 2  /* param = alpha >= 0 (Eq. 3, minS): block i keeps every
+                           eligible key whose score is >= its largest score
+                           minus alpha (alpha = +inf keeps all) */
 } vecattn_sel_mode;
 
 typedef struct vecattn_tdesc {
@@ -113,8 +114,9 @@ vecattn_status vecattn_select_workspace_size(const vecattn_tdesc* qd, const veca
  *            (those blocks keep their cap highest-scoring keys).
  *   workspace : device memory of at least vecattn_select_workspace_size bytes.
  * Errors: INVALID_ARG (null pointer, shape mismatch between q and k, block < 1,
- * param outside (0, 1], cap < 1); CAPACITY (topK with cap < max_i k_i, or a
- * workspace that is too small); UNSUPPORTED (D not in {64, 128}, mode MINS).
+ * param outside (0, 1] for topK / topP or negative / NaN for minS, cap < 1);
+ * CAPACITY (topK with cap < max_i k_i, or a workspace that is too small);
+ * UNSUPPORTED (D not in {64, 128}).
  */
 vecattn_status vecattn_select(const void* q, const vecattn_tdesc* qd, const void* k,
                               const vecattn_tdesc* kd, int32_t block, int32_t causal, int32_t mode,

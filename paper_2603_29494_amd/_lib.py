@@ -139,7 +139,7 @@ def select(q: torch.Tensor, k: torch.Tensor, block: int, mode, param: float,
            idx: Optional[torch.Tensor] = None, counts: Optional[torch.Tensor] = None,
            workspace: Optional[torch.Tensor] = None,
            n_clamped: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
-    """Per-block key-index lists (I, C) of Algorithm 1 for topK / topP selection."""
+    """Per-block key-index lists (I, C) of Algorithm 1 for topK / topP / minS (Eq. 3) selection."""
     _bf16_cuda(q, "q")
     _bf16_cuda(k, "k")
     B, Hq, N, Dd = q.shape

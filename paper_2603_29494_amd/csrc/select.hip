@@ -1,7 +1,8 @@
 // Important-vector selection (paper Sec. 3.1; the outputs I and C of
-// Algorithm 1) for gfx950: row-wise topK (a budget) and topP (a cumulative
-// softmax-mass threshold) over the estimated map Q_p K^T / sqrt(D), without
-// ever writing that map to memory (the TilingSelect principle, Sec. 3.1.3).
+// Algorithm 1) for gfx950: row-wise topK (a budget), topP (a cumulative
+// softmax-mass threshold) and minS (Eq. 3: within alpha of the row maximum)
+// over the estimated map Q_p K^T / sqrt(D), without ever writing that map to
+// memory (the TilingSelect principle, Sec. 3.1.3).
 //
 // Exact selection needs the score of the k-th key (topK) or of the key where
 // the mass reaches p (topP).  Every row therefore narrows a score interval
@@ -20,6 +21,9 @@
 //            one more pass sets a bit per kept key (score > t*), and one per
 //            key tied at the cut when only some ties are kept.
 //   COMPACT  bitmasks -> ascending index lists and counts.
+// minS rows start from a MAX pass (the row maximum fixes the threshold); with
+// a cap no block can exceed they are emitted directly, otherwise the level-0
+// pass counts them and the rows over cap continue as topK(cap).
 // All passes compute every score with the same MFMA sequence, so a key's
 // score is bit-identical in every pass.
 //
@@ -45,7 +49,10 @@ constexpr int kRounds = 2;      // a topP row whose count exceeds cap reruns as 
 enum Phase : int { PH_IDLE = 0, PH_HIST = 1, PH_COLLECT = 2, PH_DONE = 3, PH_EMIT = 4 };
 // MODE_HIST0: first histogram level (the interval is everything).
 // MODE_SAMPLE: moments of the scores of every kSampleStride-th key block.
-enum Mode : int { MODE_HIST = 0, MODE_COLLECT = 1, MODE_EMIT = 2, MODE_HIST0 = 3, MODE_SAMPLE = 4 };
+// MODE_MAX: the largest score of each minS row.
+enum Mode : int {
+  MODE_HIST = 0, MODE_COLLECT = 1, MODE_EMIT = 2, MODE_HIST0 = 3, MODE_SAMPLE = 4, MODE_MAX = 5
+};
 constexpr int kSampleStride = 16;  // 32-key blocks between sampled blocks
 
 struct RowState {
@@ -59,6 +66,8 @@ struct RowState {
   int count;        // final count
   int clamped;      // 1 if the threshold selection was clamped to cap
   int tie_interval; // 1: the keys tied at the cut are all those in [s_lo, s_hi]
+  int mins;         // 1: minS row before its count is known (level 0)
+  int pad0;
   // Scores below are raw fp32 dot products <q_p, k_j> (the softmax scale tau
   // > 0 preserves their order; it enters only the topP masses).
   float s_lo, s_hi; // current interval: keys with s_lo <= s <= s_hi (exact float bounds)
@@ -93,6 +102,8 @@ struct SelParams {
   int64_t rows;
   int B, Hq, Hkv, group, N, P, Np, D, causal, split, nsplit, W, nrb;  // nrb: row blocks per head
   int mode_topp;
+  int mode_mins;
+  int mins_direct;  // minS with cap >= every block's eligible keys: no count needed
   double param;
   float tau;
   int64_t items;    // score-pass work items
@@ -180,7 +191,7 @@ __global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
     s.L = eligible(i, p.P, p.N, p.causal);
     s.clamped = 0;
     s.topp = p.mode_topp;
-    if (!p.mode_topp) s.k_target = topk_count(p.param, s.L);
+    if (!p.mode_topp && !p.mode_mins) s.k_target = topk_count(p.param, s.L);
   }
   const float c = p.qnorm[r] * p.kmax[b * p.Hkv + h / p.group];
   const float cc = c * 1.0009765625f + 1e-30f;
@@ -195,6 +206,7 @@ __global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
   s.tie_partial = 0;
   s.k_eq = 0;
   s.tie_interval = 0;
+  s.mins = p.mode_mins && round == 0;
   p.cand_n[r] = 0;
   p.cand_lohi[2 * r] = 0xFFFFFFFFu;
   p.cand_lohi[2 * r + 1] = 0u;
@@ -300,6 +312,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   __shared__ uint32_t s_chi[COL ? kRowsWG : 1];
   __shared__ uint32_t s_cbase[COL ? kRowsWG : 1];
   __shared__ __align__(16) float s_acc[COL ? 4 * 64 * 16 : 1];  // per lane: its 16 scores
+  __shared__ uint32_t s_max[MODE == MODE_MAX ? kRowsWG : 1];  // ordered keys of row maxima
 
   const int64_t item = xcd_work_item(p.per_xcd);
   if (item >= p.items) return;
@@ -325,10 +338,11 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     int part = 0;
     if (tid < nrows) {
       const int ph = p.st[row0 + tid].phase;
-      part = (HIST || MODE == MODE_SAMPLE) ? ph == PH_HIST
+      part = (HIST || MODE == MODE_SAMPLE || MODE == MODE_MAX) ? ph == PH_HIST
              : (MODE == MODE_COLLECT)        ? ph == PH_COLLECT
                                              : ph == PH_EMIT;
       if (MODE == MODE_SAMPLE) part = part && !p.st[row0 + tid].topp;
+      if (MODE == MODE_MAX) part = part && p.st[row0 + tid].mins;
     }
     s_part[tid] = part;
     if (part) atomicOr(&s_any, 1);
@@ -338,6 +352,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     s_clo[tid] = 0xFFFFFFFFu;
     s_chi[tid] = 0u;
   }
+  if (MODE == MODE_MAX && tid < kRowsWG) s_max[tid] = 0u;  // below every ordered key
   __syncthreads();
   if (!s_any) return;  // passes late in the refinement find most workgroups idle
   if (HIST) {
@@ -407,6 +422,17 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
       const bool full = !__any(lim < 32);
       auto rowproc = [&](const bool all_elig) __attribute__((always_inline)) {
         auto elig = [&](int kl) __attribute__((always_inline)) { return all_elig || kl < lim; };
+        if (MODE == MODE_MAX) {
+          float m = kNegInf;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+            if (elig(kl)) m = fmaxf(m, acc[e]);
+          }
+          m = fmaxf(m, __shfl_xor(m, 32));
+          if (g == 0) atomicMax(&s_max[rb2 * 32 + ln], ord_key(m));
+          return;
+        }
         if (MODE == MODE_COLLECT) {
           // Two bitmasks of this lane's keys (bit kl): at or above the interval
           // (the kept set; the resolve step clears the candidates it rejects) and
@@ -548,6 +574,11 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   }
   }
   if (MODE == MODE_EMIT) return;
+  if (MODE == MODE_MAX) {
+    __syncthreads();
+    if (tid < nrows && s_part[tid]) atomicMax(&p.cand_lohi[2 * (row0 + tid) + 1], s_max[tid]);
+    return;
+  }
 
   // Reduce per-row partials: lanes (ln, g = 0 / 1) of each wave, then the 4
   // waves in a fixed order (deterministic sums).
@@ -641,6 +672,42 @@ __global__ __launch_bounds__(256) void k_bracket(SelParams p) {
 }
 
 // ---------------------------------------------------------------------------
+// minS (Eq. 3): a key is kept when tau * s >= tau * max - alpha, i.e. when its
+// raw score s >= max - alpha / tau.  The first interval is [threshold, max]:
+// the level-0 pass counts the keys in it; the resolve step either emits them
+// all (at most cap) or keeps the cap best (topK(cap), counted as clamped).
+// One thread per row.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_mins(SelParams p) {
+  const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (r >= p.rows) return;
+  RowState& s = p.st[r];
+  if (s.phase != PH_HIST || !s.mins) return;
+  const float mx = ord_val(p.cand_lohi[2 * r + 1]);
+  p.cand_lohi[2 * r + 1] = 0u;  // ready for the collect pass
+  const float top = static_cast<float>(s.ref / static_cast<double>(p.tau));  // >= every |s|
+  const double t = static_cast<double>(mx) - p.param / static_cast<double>(p.tau);
+  float tf = static_cast<float>(t);
+  if (static_cast<double>(tf) > t) tf = ord_val(ord_key(tf) - 1u);  // round down: keep ties
+  tf = fmaxf(tf, -top);
+  const float hi = fmaxf(mx, tf);
+  s.s_lo = tf;
+  s.s_hi = FLT_MAX;
+  if (p.mins_direct) {  // no block can exceed cap: emit s >= threshold at once
+    s.mins = 0;
+    s.tstar = tf;
+    s.tie_partial = 0;
+    s.tie_interval = 0;
+    s.k_eq = 0;
+    s.phase = PH_EMIT;
+    return;
+  }
+  s.blo = tf;
+  s.binv = static_cast<float>(kBins) / fmaxf(hi - tf, FLT_MIN);
+  s.badd = -tf * s.binv;
+}
+
+// ---------------------------------------------------------------------------
 // Resolve after a HIST pass: one wave per row.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
@@ -678,6 +745,24 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
   const float top = static_cast<float>(s.ref / static_cast<double>(p.tau));  // raw score bound
   int ba = -1, bb = -1;
   uint32_t above_bins = 0;  // keys in bins above bb (inside the interval)
+  if (s.mins) {  // level 0 of a minS row: the histogram counts the keys it keeps
+    s.mins = 0;
+    uint32_t tot = 0;
+    for (int bn = 0; bn < kBins; ++bn) tot += hs[bn];
+    tot += nab;
+    if (tot <= static_cast<uint32_t>(p.cap)) {
+      s.tstar = s.s_lo;  // the emit pass keeps s > t* and, all ties kept, s == t*
+      s.tie_partial = 0;
+      s.tie_interval = 0;
+      s.k_eq = 0;
+      s.count = static_cast<int>(tot);
+      s.level = level + 1;
+      s.phase = PH_EMIT;
+      return;
+    }
+    s.k_target = static_cast<int>(p.cap);  // more than cap: keep the cap best
+    s.clamped = 1;
+  }
   if (!s.topp) {
     const int k_rem = s.k_target - static_cast<int>(nab);  // rank of the cut inside the interval
     uint32_t cum = 0;
@@ -1070,6 +1155,8 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.W = static_cast<int>((N + 31) / 32);
   p.nrb = static_cast<int>((Np + kRowsWG - 1) / kRowsWG);
   p.mode_topp = a.mode == 1;
+  p.mode_mins = a.mode == 2;
+  p.mins_direct = p.mode_mins && a.cap >= N;
   p.param = a.param;
   p.tau = 1.0f / sqrtf(static_cast<float>(D));
 
@@ -1095,12 +1182,17 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   const int rounds = p.mode_topp ? kRounds : 1;
   for (int round = 0; round < rounds; ++round) {
     hipLaunchKernelGGL(k_sel_init, igrid, dim3(256), 0, stream, p, round);
-    if (round == 0 && !p.mode_topp) {
+    if (p.mode_mins) {  // minS: the row maxima fix each row's threshold
+      score_pass<MODE_MAX>(D, false, pgrid, p, stream);
+      hipLaunchKernelGGL(k_mins, igrid, dim3(256), 0, stream, p);
+    } else if (round == 0 && !p.mode_topp) {
       score_pass<MODE_SAMPLE>(D, false, pgrid, p, stream);
       hipLaunchKernelGGL(k_bracket, igrid, dim3(256), 0, stream, p);
     }
+    if (p.mins_direct) break;  // every row goes straight to the emit pass
     for (int lv = 0; lv < kLevels; ++lv) {
-      if (lv == 0) score_pass<MODE_HIST0>(D, p.mode_topp != 0, pgrid, p, stream);
+      // Level 0 bins every key, except for minS rows, which count [threshold, max].
+      if (lv == 0 && !p.mode_mins) score_pass<MODE_HIST0>(D, p.mode_topp != 0, pgrid, p, stream);
       else score_pass<MODE_HIST>(D, p.mode_topp != 0, pgrid, p, stream);
       hipLaunchKernelGGL(k_resolve_hist, rgrid, dim3(64), 0, stream, p, lv);
     }

@@ -120,7 +120,6 @@ vecattn_status vecattn_select(const void* q, const vecattn_tdesc* qd, const void
   if (mode != VECATTN_SEL_TOPK && mode != VECATTN_SEL_TOPP && mode != VECATTN_SEL_MINS)
     return VECATTN_ERR_INVALID_ARG;
   if (!param_ok(mode, param)) return VECATTN_ERR_INVALID_ARG;
-  if (mode == VECATTN_SEL_MINS) return VECATTN_ERR_UNSUPPORTED;
   if (mode == VECATTN_SEL_TOPK && cap < max_count(qd->N, block, causal, mode, param))
     return VECATTN_ERR_CAPACITY;
   const size_t need = vecattn::select_workspace_bytes(qd->B, qd->H, qd->N, qd->D, block, mode, cap);

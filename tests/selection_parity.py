@@ -5,6 +5,8 @@ GPU computes them from the same bf16 inputs with fp32 accumulation, so sets
 may differ only where two keys' scores are within 1e-5 * max|s| of the cut:
   topK: equal counts; every key in the symmetric difference lies within the
         tolerance of the oracle's k-th score.
+  minS: every key in the symmetric difference lies within the tolerance of
+        rowmax - alpha (rows clamped to cap follow the topK rule);
   topP: every key in the symmetric difference lies within the tolerance of
         the oracle's cut score, or the oracle's cumulative mass at the cut is
         within 1e-5 of p (then the counts differ by at most one); the GPU set's
@@ -53,6 +55,13 @@ def check_rows(q, k, block, mode, param, causal, cap, idx_gpu, cnt_gpu, rows, co
         assert cg == 0 or (g[0] >= 0 and g[-1] < L), f"row {w}: index out of range"
         assert np.all(idx_gpu[pw, cg:] == -1), f"row {w}: padding"
         diff = np.setxor1d(g, o)
+        if mode == oracle.MINS and co < cap:   # minS: keys at or above rowmax - alpha
+            if diff.size:
+                mismatched += 1
+                thr = s.max() - param
+                assert np.all(np.abs(s[diff] - thr) <= tol), \
+                    f"row {w}: minS differs beyond near-threshold: {np.abs(s[diff] - thr).max()}"
+            continue
         if mode == oracle.TOPK or co == cap:   # topK, or a threshold row clamped to cap
             assert cg == co, f"row {w}: count {cg} != {co}"
             if diff.size:

@@ -109,7 +109,8 @@ def test_select_rejects_bad_arguments():
     assert select(mode=7) == INVALID
     assert select(kd=desc(1, 3, 256, 128)) == INVALID
     assert select(kd=desc(1, 2, 255, 128)) == INVALID
-    assert select(mode=2, param=0.5) == UNSUPPORTED        # minS is not built
+    assert select(mode=2, param=-0.5) == INVALID           # minS: alpha >= 0
+    assert select(mode=2, param=float('nan')) == INVALID
     assert select(cap=63) == CAPACITY                      # topK 25% of 256 keys = 64
     assert select(ws=None) == CAPACITY
     assert select(ws_bytes=16) == CAPACITY

@@ -135,3 +135,45 @@ def test_level0_interval_from_misleading_sample(gpu, sampled_high):
     qb, kb = synth.to_bf16_bits(q), synth.to_bf16_bits(k)
     idx, cnt, cap, _ = run(qb, kb, block, oracle.TOPK, 0.1, False)
     check_rows(qb, kb, block, oracle.TOPK, 0.1, False, cap, idx, cnt, all_rows(qb, block))
+
+
+MINS_CASES = [
+    # B, Hq, Hkv, N, D, block, causal, alpha
+    (1, 2, 2, 700, 128, 64, False, 0.0),
+    (1, 2, 2, 700, 128, 64, False, 0.5),
+    (1, 4, 2, 1000, 128, 64, True, 1.0),
+    (2, 2, 1, 513, 64, 32, False, 2.0),
+    (1, 2, 2, 600, 64, 64, True, float("inf")),
+    (1, 1, 1, 6000, 128, 64, False, 1.5),
+]
+
+
+@pytest.mark.parametrize("case", MINS_CASES)
+def test_mins_matches_oracle(gpu, case):
+    # Eq. 3: every eligible key within alpha (in units of the scaled score) of
+    # the block's largest score.
+    B, Hq, Hkv, N, D, block, causal, alpha = case
+    q, k, _ = synth.planted_case(hash(case) % 10000 + 100, B, Hq, Hkv, N, D)
+    cap = va.max_count(N, block, causal, "mins", alpha)
+    ncl = torch.zeros(1, dtype=torch.int32, device="cuda")
+    idx, cnt = va.select(dev(q), dev(k), block, "mins", alpha, causal, cap=cap, n_clamped=ncl)
+    torch.cuda.synchronize()
+    assert int(ncl.item()) == 0
+    rows = all_rows(q, block)
+    mism = check_rows(q, k, block, oracle.MINS, alpha, causal, cap, idx.cpu().numpy(),
+                      cnt.cpu().numpy(), rows)
+    assert mism <= max(1, len(rows) // 20)
+
+
+def test_mins_clamped_to_cap(gpu):
+    # A wide alpha selects more than cap keys: each such block keeps its cap
+    # best (counted in n_clamped), the others their full minS set.
+    q, k, _ = synth.planted_case(12, 1, 2, 2, 2000, 128)
+    cap = 150
+    ncl = torch.zeros(1, dtype=torch.int32, device="cuda")
+    idx, cnt = va.select(dev(q), dev(k), 64, "mins", 3.0, False, cap=cap, n_clamped=ncl)
+    torch.cuda.synchronize()
+    _, cnt_o, ncl_o = oracle.select(q, k, 64, oracle.MINS, 3.0, False, cap)
+    assert int(ncl.item()) == ncl_o and ncl_o > 0
+    check_rows(q, k, 64, oracle.MINS, 3.0, False, cap, idx.cpu().numpy(), cnt.cpu().numpy(),
+               all_rows(q, 64))

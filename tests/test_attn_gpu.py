@@ -160,3 +160,22 @@ def test_plumbing_workload_with_oracle_indices(gpu):
                             torch.from_numpy(cnt).cuda(), w.block, w.causal, return_lse=True)
     torch.cuda.synchronize()
     check_attn(o, lse, o_ref, lse_ref, "plumbing_1k")
+
+
+@pytest.mark.parametrize("D", [64, 128])
+def test_k_and_v_with_different_row_strides(gpu, D):
+    # V stored [B, N, Hkv, D] (row stride Hkv * D) and K [B, Hkv, N, D]: the
+    # gathers then need separate K and V offsets.
+    B, Hq, Hkv, N, P = 1, 4, 2, 300, 64
+    q = synth.random_bits(41, (B, Hq, N, D))
+    k = synth.random_bits(42, (B, Hkv, N, D))
+    v = synth.random_bits(43, (B, N, Hkv, D))
+    vc = np.ascontiguousarray(v.transpose(0, 2, 1, 3))
+    Np = (N + P - 1) // P
+    idx, cnt = random_lists(44, B, Hq, Np, N, P, True, N, N, min_count=1)
+    o_ref, lse_ref = oracle.sparse_attn(q, k, vc, idx, cnt, P, True)
+    o, lse = va.sparse_attn(dev(q), dev(k), dev(v).permute(0, 2, 1, 3),
+                            torch.from_numpy(idx).cuda(), torch.from_numpy(cnt).cuda(), P, True,
+                            return_lse=True)
+    torch.cuda.synchronize()
+    check_attn(o, lse, o_ref, lse_ref, f"kv strides D={D}")

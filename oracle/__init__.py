@@ -12,6 +12,7 @@ Functions and the passages they follow:
 * :func:`pooled_scores`   -- the estimated map's scores Q_p K^T / sqrt(D), Sec. 3.1.1.
 * :func:`select`          -- row-wise topK / topP (Sec. 3.1.2) and minS (Eq. 3).
 * :func:`mins_progressive`-- Eq. 3 as Algorithm 1 applies it (running max per K-group).
+* :func:`select_mins_tiled` -- Algorithm 1's selection (cross-tile minS, Sec. 3.1.3) per block.
 * :func:`sparse_attn`     -- Eq. 4 (materialised softmax over the selected keys).
 * :func:`sparse_attn_online` -- Algorithm 2's online recurrence (second route to Eq. 4).
 * :func:`dense_attn`      -- Eq. 1, textbook dense attention.
@@ -29,7 +30,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "vecattn_ref.cpp")
 _LIB_PATH = os.path.join(_HERE, "libvecattn_ref.so")
 
-TOPK, TOPP, MINS = 0, 1, 2
+TOPK, TOPP, MINS, MINS_TILED = 0, 1, 2, 3
 
 _lib = None
 
@@ -62,13 +63,15 @@ def _load():
     lib.ora_select.argtypes = [P, P, i64, i64, i64, i64, i64, i32, i32, i32, f64, i64,
                                P, P, P, P, i64, i32, i32]
     lib.ora_mins_progressive_row.argtypes = [P, i64, f64, i64, i64, P, P]
+    lib.ora_select_mins_tiled.argtypes = [P, P, i64, i64, i64, i64, i64, i32, i32, f64, i64, i64,
+                                          i64, P, P, P, P, i64, i32, i32]
     lib.ora_sparse_attn.argtypes = [P, P, P, i64, i64, i64, i64, i64, i32, i32, f64,
                                     P, i64, P, P, P, P, i64, i32, i32]
     lib.ora_dense_attn.argtypes = [P, P, P, i64, i64, i64, i64, i64, i32, f64, P, P, i32]
     lib.ora_sparse_attn_online.argtypes = [P, P, P, i64, i64, i64, i64, i64, i32, i32, f64,
                                            P, i64, P, i32, P, P, i32]
     for name in ("ora_bf16_round", "ora_pool", "ora_pooled_scores", "ora_select",
-                 "ora_mins_progressive_row", "ora_sparse_attn", "ora_dense_attn",
+                 "ora_mins_progressive_row", "ora_select_mins_tiled", "ora_sparse_attn", "ora_dense_attn",
                  "ora_sparse_attn_online"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
@@ -166,6 +169,36 @@ def select(q: np.ndarray, k: np.ndarray, block: int, mode: int, param: float, ca
     if rc == 3:
         raise ValueError("capacity too small for topK")
     _check(rc, "select")
+    return idx, counts, int(ncl.value)
+
+
+def select_mins_tiled(q: np.ndarray, k: np.ndarray, block: int, alpha: float, causal: bool,
+                      cap: int, bk: int = 16, gk: int = 16, rows: Optional[Sequence[int]] = None,
+                      nthreads: int = 0,
+                      compact: bool = False) -> Tuple[np.ndarray, np.ndarray, int]:
+    """Algorithm 1's selection: per block, the eligible keys kept by the cross-tile
+    minS rule (groups of gk tiles of bk keys, running maximum within a group;
+    Sec. 3.1.3), ascending; a block keeping more than cap keys keeps its first
+    cap and is counted.  Outputs as :func:`select`."""
+    q, k = _bits(q), _bits(k)
+    B, Hq, N, D = q.shape
+    Hkv = k.shape[1]
+    Np = num_blocks(N, block)
+    if compact:
+        if rows is None:
+            raise ValueError("compact output needs rows")
+        idx = np.full((len(rows), cap), -1, dtype=np.int32)
+        counts = np.zeros(len(rows), dtype=np.int32)
+    else:
+        idx = np.full((B, Hq, Np, cap), -1, dtype=np.int32)
+        counts = np.zeros((B, Hq, Np), dtype=np.int32)
+    ncl = ctypes.c_int64(0)
+    rows_arr = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+    _check(_load().ora_select_mins_tiled(_ptr(q), _ptr(k), B, Hq, Hkv, N, D, block, int(causal),
+                                         float(alpha), int(bk), int(gk), int(cap), _ptr(idx),
+                                         _ptr(counts), ctypes.byref(ncl), _ptr(rows_arr),
+                                         0 if rows_arr is None else rows_arr.size,
+                                         int(bool(compact)), nthreads), "select_mins_tiled")
     return idx, counts, int(ncl.value)
 
 

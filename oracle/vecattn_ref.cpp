@@ -19,11 +19,14 @@
 //   * Sec. 3.1.2: row-wise topK (keep exactly the k largest entries) and topP
 //     (keep entries until their cumulative attention mass reaches p).
 //   * Eq. 3 (Sec. 3.1.2): minS, Idx(i) = { j : s_ij >= rowmax_i - alpha }.
+//   * Algorithm 1 (appendix, Important-Vector Selection) and Sec. 3.1.3
+//     (cross-tile minS): the same rule against a running maximum that each
+//     group of G_K tiles of B_K keys accumulates tile by tile.
 //   * Eq. 4 (Sec. 3.2): O[I_B(i)] = softmax(Q[I_B(i)] K[Idx(i)]^T / sqrt(D)) V[Idx(i)].
 //   * Algorithm 2 (appendix, Vector-Sparse Computation): the tiled online-softmax
 //     recurrence, used here only as a second route to Eq. 4 for self-checks.
 //
-// Readings where the paper is silent (each is listed in the design doc):
+// Readings where the paper is silent (the design notes list each one):
 //   ragged last block pools only its existing rows; Q_p is rounded once from the
 //   exact double mean to bf16 (round to nearest, ties to even); causal selection
 //   ranges over keys up to the block's last row; ties are broken by lower key
@@ -353,6 +356,46 @@ int ora_select(const uint16_t* q, const uint16_t* k, int64_t B, int64_t Hq, int6
       chosen.assign(ord.begin(), ord.begin() + n);
     }
     std::sort(chosen.begin(), chosen.end());
+    const int64_t orow = compact ? t : w;
+    int32_t* row = idx + orow * cap;
+    for (int64_t c = 0; c < cap; ++c)
+      row[c] = c < static_cast<int64_t>(chosen.size()) ? static_cast<int32_t>(chosen[c]) : -1;
+    counts[orow] = static_cast<int32_t>(chosen.size());
+  }
+  if (n_clamped) *n_clamped = clamped;
+  return ORA_OK;
+}
+
+// Selection with Algorithm 1's cross-tile minS for every listed block (all
+// blocks when rows == NULL): the block's eligible pooled scores filtered by
+// mins_progressive, in ascending key order.  A block that keeps more than cap
+// keys keeps the first cap of them (the order in which Algorithm 1 appends its
+// tiles) and is counted in *n_clamped.
+int ora_select_mins_tiled(const uint16_t* q, const uint16_t* k, int64_t B, int64_t Hq, int64_t Hkv,
+                          int64_t N, int64_t D, int32_t block, int32_t causal, double alpha,
+                          int64_t bk, int64_t gk, int64_t cap, int32_t* idx, int32_t* counts,
+                          int64_t* n_clamped, const int64_t* rows, int64_t n_rows, int32_t compact,
+                          int32_t nthreads) {
+  Shape s{B, Hq, Hkv, N, D};
+  if (!q || !k || !idx || !counts || block < 1 || cap < 1 || bk < 1 || gk < 1 || !shape_ok(s))
+    return ORA_ERR_ARG;
+  if (compact && !rows) return ORA_ERR_ARG;
+  if (!(alpha >= 0.0)) return ORA_ERR_ARG;
+  const int64_t Np = num_blocks(N, block);
+  const int64_t total = rows ? n_rows : B * Hq * Np;
+  int64_t clamped = 0;
+  set_threads(nthreads);
+#pragma omp parallel for schedule(dynamic) reduction(+ : clamped)
+  for (int64_t t = 0; t < total; ++t) {
+    const int64_t w = rows ? rows[t] : t;
+    const int64_t i = w % Np, h = (w / Np) % Hq, b = w / (Np * Hq);
+    std::vector<double> sc;
+    pooled_scores(q, k, s, block, causal, b, h, i, sc);
+    std::vector<int64_t> chosen = mins_progressive(sc, alpha, bk, gk);
+    if (static_cast<int64_t>(chosen.size()) > cap) {
+      chosen.resize(static_cast<size_t>(cap));
+      clamped += 1;
+    }
     const int64_t orow = compact ? t : w;
     int32_t* row = idx + orow * cap;
     for (int64_t c = 0; c < cap; ++c)

@@ -260,6 +260,55 @@ def test_mins_special_cases():
     assert list(idx[0, 0, 0, :cnt[0, 0, 0]]) == [int(np.argmax(sc))]
 
 
+def test_mins_tiled_worked_examples():
+    # Algorithm 1 by hand, bk = 2, gk = 2 (groups of 4 keys), alpha = 1.5:
+    #   group {0..3}: tile {0,1} running max 3 -> keep s >= 1.5: key 1;
+    #                 tile {2,3} running max 5 -> keep s >= 3.5: key 3;
+    #   group {4,5}:  running max restarts, 3.2 -> keep s >= 1.7: key 5.
+    # (A running max over earlier tiles only would keep key 0; one never reset
+    # would drop key 5; the row maximum of Eq. 3 keeps only key 3.)
+    s = np.array([1.0, 3.0, 2.0, 5.0, 0.0, 3.2])
+    assert list(oracle.mins_progressive(s, 1.5, 2, 2)) == [1, 3, 5]
+    # comparator >= (Eq. 3): a key exactly alpha below the running max stays
+    assert list(oracle.mins_progressive(np.array([2.0, 1.0]), 1.0, 2, 1)) == [0, 1]
+
+
+def test_mins_tiled_single_group_is_prefix_max():
+    # one group, one-key tiles: key j is kept iff s_j >= max(s_0..s_j) - alpha
+    r = np.random.Generator(np.random.PCG64(71))
+    s = r.standard_normal(3000)
+    for alpha in (0.0, 0.3, 1.0):
+        expect = np.nonzero(s >= np.maximum.accumulate(s) - alpha)[0]
+        assert np.array_equal(oracle.mins_progressive(s, alpha, 1, 10 ** 6), expect)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_select_mins_tiled_per_block(causal):
+    q, k = _tiny_layer(73, 300, D=32)
+    Np = 5
+    idx, cnt, ncl = oracle.select_mins_tiled(q, k, 64, 0.05, causal, 300, bk=16, gk=4)
+    assert ncl == 0
+    gidx, gcnt, _ = oracle.select(q, k, 64, oracle.MINS, 0.05, causal, 300)
+    for i in range(Np):
+        s = oracle.pooled_scores(q, k, 64, causal, 0, 0, i)
+        row = idx[0, 0, i, :cnt[0, 0, i]]
+        assert np.array_equal(row, oracle.mins_progressive(s, 0.05, 16, 4))
+        assert np.all(idx[0, 0, i, cnt[0, 0, i]:] == -1)
+        assert set(gidx[0, 0, i, :gcnt[0, 0, i]]) <= set(row)   # running max <= row max
+    # alpha = inf keeps every eligible key
+    idx, cnt, _ = oracle.select_mins_tiled(q, k, 64, np.inf, causal, 300, bk=16, gk=16)
+    for i in range(Np):
+        L = min(300, 64 * (i + 1)) if causal else 300
+        assert list(idx[0, 0, i, :cnt[0, 0, i]]) == list(range(L))
+    # a block keeping more than cap keys keeps its first cap keys and is counted
+    full, fcnt, _ = oracle.select_mins_tiled(q, k, 64, 0.05, causal, 300, bk=16, gk=4)
+    cap = int(np.median(fcnt))
+    idx, cnt, ncl = oracle.select_mins_tiled(q, k, 64, 0.05, causal, cap, bk=16, gk=4)
+    assert ncl == int(np.sum(fcnt > cap))
+    assert np.array_equal(cnt, np.minimum(fcnt, cap))
+    assert np.array_equal(idx[0, 0], full[0, 0, :, :cap])
+
+
 def _all_keys(N, P, causal, Np, B=1, H=1):
     cap = N
     idx = np.full((B, H, Np, cap), -1, dtype=np.int32)

@@ -7,8 +7,9 @@
  *      queries (Eq. 2), score every eligible key with the pooled query
  *      (estimated map A_p, Sec. 3.1.1) and keep the important key columns
  *      ("vertical vectors") by a budget (row-wise topK) or a cumulative-mass
- *      threshold (row-wise topP), Sec. 3.1.2.  Output: the index matrix I and
- *      count vector C of Algorithm 1.
+ *      threshold (row-wise topP), Sec. 3.1.2, or the minS filter (Eq. 3), also
+ *      with Algorithm 1's cross-tile running maximum (vecattn_select_mins_tiled).
+ *      Output: the index matrix I and count vector C of Algorithm 1.
  *   2. vecattn_sparse_attn: attention of each query block restricted to the
  *      gathered K/V rows of its selected keys (Eq. 4, Algorithm 2).
  *
@@ -56,9 +57,13 @@ typedef enum vecattn_sel_mode {
   VECATTN_SEL_TOPP = 1, /* param = mass p in (0, 1]: block i keeps the shortest
                            prefix, in (score desc, index asc) order, whose softmax
                            mass over its eligible keys is >= p */
-  VECATTN_SEL_MINS = 2  /* param = alpha >= 0 (Eq. 3, minS): block i keeps every
+  VECATTN_SEL_MINS = 2, /* param = alpha >= 0 (Eq. 3, minS): block i keeps every
                            eligible key whose score is >= its largest score
                            minus alpha (alpha = +inf keeps all) */
+  VECATTN_SEL_MINS_TILED = 3 /* param = alpha >= 0: minS against Algorithm 1's
+                           cross-tile running maximum (Sec. 3.1.3), with the
+                           paper's B_K = 16 keys per tile and G_K = 16 tiles per
+                           group; see vecattn_select_mins_tiled */
 } vecattn_sel_mode;
 
 typedef struct vecattn_tdesc {
@@ -85,7 +90,8 @@ vecattn_status vecattn_pool(const void* q, const vecattn_tdesc* qd, int32_t bloc
 
 /*
  * Largest number of keys any block can select, for sizing cap.  topK: max_i k_i;
- * topP: max_i L_i, where L_i = N (non-causal) or min(N, (i+1)*P) (causal).
+ * the other modes: max_i L_i, where L_i = N (non-causal) or min(N, (i+1)*P)
+ * (causal).
  * Errors: INVALID_ARG for N < 1, block < 1, out == NULL, or param outside the
  * mode's range.
  */
@@ -111,7 +117,8 @@ vecattn_status vecattn_select_workspace_size(const vecattn_tdesc* qd, const veca
  *   counts : int32 [B, Hq, N_p] output
  *   n_clamped : optional device int32; when not NULL, the number of blocks
  *            whose threshold-mode selection exceeded cap is ADDED to it
- *            (those blocks keep their cap highest-scoring keys).
+ *            (topP and minS blocks keep their cap highest-scoring keys;
+ *            cross-tile minS blocks their first cap keys).
  *   workspace : device memory of at least vecattn_select_workspace_size bytes.
  * Errors: INVALID_ARG (null pointer, shape mismatch between q and k, block < 1,
  * param outside (0, 1] for topK / topP or negative / NaN for minS, cap < 1);
@@ -123,6 +130,37 @@ vecattn_status vecattn_select(const void* q, const vecattn_tdesc* qd, const void
                               double param, int32_t* idx, int64_t cap, int32_t* counts,
                               int32_t* n_clamped, void* workspace, size_t workspace_bytes,
                               void* stream);
+
+/*
+ * Important-vector selection with Algorithm 1's cross-tile minS filter
+ * (appendix Algorithm 1; Sec. 3.1.3, "Cross-tile minS optimization"; the rule
+ * is Eq. 3's with a running maximum in place of the row maximum).  Block i's
+ * eligible keys (as for vecattn_select) fall into groups of tile * group_tiles
+ * consecutive keys, the first starting at key 0; inside a group the tiles of
+ * `tile` keys are visited in ascending order, and a key of tile t is kept when
+ * its score is >= (largest score in the group's tiles 0..t) - alpha.  Scores
+ * are computed as for vecattn_select; alpha = +inf keeps every eligible key.
+ *   tile        : B_K, 16 or 32 keys
+ *   group_tiles : G_K, a power of two, tile * group_tiles <= 2^30 (a group
+ *                 longer than N makes the running maximum span the whole row)
+ *   idx, counts, workspace : as for vecattn_select (workspace size from
+ *            vecattn_select_workspace_size with mode VECATTN_SEL_MINS_TILED)
+ *   n_clamped : optional device int32; the number of blocks that selected more
+ *            than cap keys is ADDED to it.  Such a block keeps its first cap
+ *            selected keys in key order (the order in which Algorithm 1 appends
+ *            its tiles) and reports count = cap.
+ * vecattn_select with mode VECATTN_SEL_MINS_TILED equals this call with
+ * tile = 16, group_tiles = 16.
+ * Errors: INVALID_ARG (null pointer, shape mismatch, block < 1, cap < 1, alpha
+ * negative or NaN, tile not 16 or 32, group_tiles not a power of two or too
+ * large); CAPACITY (workspace too small); UNSUPPORTED (D not in {64, 128}).
+ */
+vecattn_status vecattn_select_mins_tiled(const void* q, const vecattn_tdesc* qd, const void* k,
+                                         const vecattn_tdesc* kd, int32_t block, int32_t causal,
+                                         double alpha, int32_t tile, int32_t group_tiles,
+                                         int32_t* idx, int64_t cap, int32_t* counts,
+                                         int32_t* n_clamped, void* workspace,
+                                         size_t workspace_bytes, void* stream);
 
 /*
  * Vector-sparse attention, Eq. 4 (Sec. 3.2) and Algorithm 2.  For query row r

@@ -2,13 +2,14 @@
 
 After VecAttention (arXiv 2603.29494): per query block, pool the queries
 (Eq. 2), score every key with the pooled query and keep the important key
-columns (row-wise topK budget or topP mass threshold, Sec. 3.1), then run
+columns (row-wise topK budget, topP mass threshold, or the minS filter of
+Eq. 3, also with Algorithm 1's cross-tile running maximum; Sec. 3.1), then run
 attention restricted to the gathered K/V rows of those columns (Eq. 4,
 Algorithm 2).  Both stages are HIP kernels in libvecattn.so behind the C ABI
 of include/vecattn.h; this package only marshals torch tensors to it.
 """
-from ._lib import (SEL_MINS, SEL_TOPK, SEL_TOPP, VecattnError, load, max_count, pool, select,
-                   sparse_attn, workspace_bytes)
+from ._lib import (SEL_MINS, SEL_MINS_TILED, SEL_TOPK, SEL_TOPP, VecattnError, load, max_count,
+                   pool, select, sparse_attn, workspace_bytes)
 
-__all__ = ["SEL_TOPK", "SEL_TOPP", "SEL_MINS", "VecattnError", "load", "max_count", "pool",
-           "select", "sparse_attn", "workspace_bytes"]
+__all__ = ["SEL_TOPK", "SEL_TOPP", "SEL_MINS", "SEL_MINS_TILED", "VecattnError", "load",
+           "max_count", "pool", "select", "sparse_attn", "workspace_bytes"]

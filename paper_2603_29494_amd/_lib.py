@@ -17,8 +17,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libvecattn.so")
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_CAPACITY, ERR_DEVICE = range(5)
-SEL_TOPK, SEL_TOPP, SEL_MINS = 0, 1, 2
-_MODES = {"topk": SEL_TOPK, "topp": SEL_TOPP, "mins": SEL_MINS}
+SEL_TOPK, SEL_TOPP, SEL_MINS, SEL_MINS_TILED = 0, 1, 2, 3
+_MODES = {"topk": SEL_TOPK, "topp": SEL_TOPP, "mins": SEL_MINS, "mins_tiled": SEL_MINS_TILED}
 
 
 class VecattnError(RuntimeError):
@@ -57,9 +57,11 @@ def load() -> ctypes.CDLL:
                                                   ctypes.POINTER(ctypes.c_size_t)]
     lib.vecattn_select.argtypes = [P, D, P, D, i32, i32, i32, f64, P, i64, P, P, P,
                                    ctypes.c_size_t, P]
+    lib.vecattn_select_mins_tiled.argtypes = [P, D, P, D, i32, i32, f64, i32, i32, P, i64, P, P,
+                                              P, ctypes.c_size_t, P]
     lib.vecattn_sparse_attn.argtypes = [P, D, P, D, P, D, P, i64, P, i32, i32, f32, P, D, P, P]
     for name in ("vecattn_pool", "vecattn_select_max_count", "vecattn_select_workspace_size",
-                 "vecattn_select", "vecattn_sparse_attn"):
+                 "vecattn_select", "vecattn_select_mins_tiled", "vecattn_sparse_attn"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -138,8 +140,11 @@ def select(q: torch.Tensor, k: torch.Tensor, block: int, mode, param: float,
            causal: bool = False, cap: Optional[int] = None,
            idx: Optional[torch.Tensor] = None, counts: Optional[torch.Tensor] = None,
            workspace: Optional[torch.Tensor] = None,
-           n_clamped: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
-    """Per-block key-index lists (I, C) of Algorithm 1 for topK / topP / minS (Eq. 3) selection."""
+           n_clamped: Optional[torch.Tensor] = None, tile: Optional[int] = None,
+           group_tiles: Optional[int] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Per-block key-index lists (I, C) of Algorithm 1 for topK / topP / minS (Eq. 3)
+    selection, or minS with Algorithm 1's cross-tile running maximum ("mins_tiled":
+    ``tile`` = B_K and ``group_tiles`` = G_K, both 16 when not given)."""
     _bf16_cuda(q, "q")
     _bf16_cuda(k, "k")
     B, Hq, N, Dd = q.shape
@@ -159,10 +164,20 @@ def select(q: torch.Tensor, k: torch.Tensor, block: int, mode, param: float,
     if workspace is None and need > 0:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
     qd, kd = desc(q), desc(k)
+    nws = 0 if workspace is None else workspace.numel()
+    if mode_id(mode) == SEL_MINS_TILED:
+        _check(load().vecattn_select_mins_tiled(
+            _ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd), int(block), int(bool(causal)),
+            float(param), 16 if tile is None else int(tile),
+            16 if group_tiles is None else int(group_tiles), _ptr(idx), int(cap), _ptr(counts),
+            _ptr(n_clamped), _ptr(workspace), nws, _stream(q)), "select_mins_tiled")
+        return idx, counts
+    if tile is not None or group_tiles is not None:
+        raise ValueError("tile / group_tiles apply to mode 'mins_tiled' only")
     _check(load().vecattn_select(_ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd), int(block),
                                  int(bool(causal)), mode_id(mode), float(param), _ptr(idx),
-                                 int(cap), _ptr(counts), _ptr(n_clamped), _ptr(workspace),
-                                 0 if workspace is None else workspace.numel(), _stream(q)),
+                                 int(cap), _ptr(counts), _ptr(n_clamped), _ptr(workspace), nws,
+                                 _stream(q)),
            "select")
     return idx, counts
 

@@ -38,6 +38,8 @@ struct SelectArgs {
   int32_t causal;
   int32_t mode;
   double param;
+  int32_t tile;         // cross-tile minS: keys per tile (16 or 32)
+  int32_t group_tiles;  // cross-tile minS: tiles per group (a power of two)
   int32_t* idx;
   int64_t cap;
   int32_t* counts;

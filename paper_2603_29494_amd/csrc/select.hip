@@ -104,6 +104,13 @@ struct SelParams {
   int mode_topp;
   int mode_mins;
   int mins_direct;  // minS with cap >= every block's eligible keys: no count needed
+  int mode_tiled;   // cross-tile minS (Algorithm 1)
+  int tiled_tile;   // keys per tile: 16 or 32
+  int tiled_gs;     // keys per group of tiles (a power of two)
+  int tiled_sb;     // 32-key blocks per segment a wave walks in order
+  int tiled_carry;  // groups span several splits: waves start from a carried maximum
+  double tiled_a;   // alpha / tau: alpha in raw-score units
+  float* qmax;      // [rows][nsplit * 4]: per quarter split, its maximum, then the carried one
   double param;
   float tau;
   int64_t items;    // score-pass work items
@@ -708,6 +715,192 @@ __global__ __launch_bounds__(256) void k_mins(SelParams p) {
 }
 
 // ---------------------------------------------------------------------------
+// Cross-tile minS (Algorithm 1; Sec. 3.1.3).  Keys fall into groups of gs =
+// tile * group_tiles consecutive keys (groups start at key 0); inside a group
+// the tiles of `tile` keys are taken in key order and a key of tile t is kept
+// when its score is >= (largest score of the group's tiles 0..t) - alpha.
+// A workgroup owns 64 pooled rows and one split of keys; each wave walks whole
+// segments of the split in key order and keeps the running maximum of each of
+// its rows in a register.  A segment is one group (a 32-key block when groups
+// are smaller); when groups span more than a split (tiled_carry), each wave
+// takes one quarter of the split and starts from the maximum of the group's
+// earlier quarters, which the MAXQ pass (EMIT = false) and k_tiled_carry
+// provide.  The pass sets one bit per kept key; k_compact lists them.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float tiled_threshold(float m, double a) {
+  // Largest float <= m - a (exact, so a key at the threshold is kept).
+  const double t = static_cast<double>(m) - a;
+  float tf = static_cast<float>(t);
+  if (static_cast<double>(tf) > t) tf = ord_val(ord_key(tf) - 1u);
+  return tf;
+}
+
+template <int D, bool EMIT>
+__global__ __launch_bounds__(kThreads) void k_mins_tiled(SelParams p) {
+  constexpr int DS = D / 16;
+  const int64_t item = xcd_work_item(p.per_xcd);
+  if (item >= p.items) return;
+  const int rb = static_cast<int>(item % p.nrb);
+  const int64_t rest = item / p.nrb;
+  const int sp = static_cast<int>(rest % p.nsplit);
+  const int64_t bh = rest / p.nsplit;
+  const int b = static_cast<int>(bh / p.Hq), h = static_cast<int>(bh % p.Hq);
+  const int hk = h / p.group;
+  const int i0 = rb * kRowsWG;
+  const int nrows = min(kRowsWG, p.Np - i0);
+  const int Ltile = eligible(i0 + nrows - 1, p.P, p.N, p.causal);
+  const int key0 = sp * p.split;
+  if (key0 >= Ltile) return;
+  const int key1 = min(key0 + p.split, Ltile);
+  const int64_t row0 = bh * p.Np + i0;
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63, g = lane >> 5, ln = lane & 31;
+  const int SB = p.tiled_sb;
+  const int nblk = (key1 - key0 + 31) / 32;
+  if (wave * SB >= nblk) return;  // no segment left for this wave (no barriers below)
+  const int nq = 4 * p.nsplit;    // quarters per row in qmax
+
+  // This lane's two rows (rl = 32 * rb2 + ln): pooled query (B operand), the
+  // row's eligible keys, running maximum and current threshold.
+  bf16x8 qf[2][DS];
+  int Lr[2];
+  bool have[2];
+  float m[2], thr[2];
+#pragma unroll
+  for (int rb2 = 0; rb2 < 2; ++rb2) {
+    const int rl = rb2 * 32 + ln;
+    have[rb2] = rl < nrows;
+    const int64_t row = row0 + (have[rb2] ? rl : 0);
+    Lr[rb2] = have[rb2] ? eligible(i0 + rl, p.P, p.N, p.causal) : 0;
+    const u32x4* src = reinterpret_cast<const u32x4*>(p.qp + row * D);
+#pragma unroll
+    for (int s2 = 0; s2 < DS; ++s2) {
+      const u32x4 t = have[rb2] ? src[2 * s2 + g] : u32x4{0, 0, 0, 0};
+      qf[rb2][s2] = __builtin_bit_cast(bf16x8, t);
+    }
+    m[rb2] = (EMIT && p.tiled_carry && have[rb2]) ? p.qmax[row * nq + sp * 4 + wave] : kNegInf;
+    thr[rb2] = tiled_threshold(m[rb2], p.tiled_a);
+  }
+
+  const uint16_t* kh = p.k + b * p.k_sB + hk * p.k_sH;
+  auto kload = [&](u32x4 (&dst)[DS], int blk) __attribute__((always_inline)) {
+    const int kr = min(key0 + blk * 32 + ln, p.N - 1);  // clamped: loads past the end are safe
+    const u32x4* ksrc = reinterpret_cast<const u32x4*>(kh + static_cast<int64_t>(kr) * p.k_sN);
+#pragma unroll
+    for (int s2 = 0; s2 < DS; ++s2) dst[s2] = ksrc[2 * s2 + g];
+  };
+  // The j-th block this wave visits: segments wave, wave + 4, ... of SB blocks.
+  auto blk_of = [&](int j) __attribute__((always_inline)) {
+    return ((j / SB) * 4 + wave) * SB + j % SB;
+  };
+  const uint32_t gmask = static_cast<uint32_t>(p.tiled_gs) - 1u;
+  const bool two_tiles = p.tiled_tile == 16;
+
+  auto proc = [&](const u32x4 (&ka)[DS], int blk) __attribute__((always_inline)) {
+    const int kb = key0 + blk * 32;
+#pragma unroll
+    for (int rb2 = 0; rb2 < 2; ++rb2) {
+      // Raw scores of keys kl = 8 (e / 4) + 4 g + e % 4 of the block (keys
+      // 0-15, the first 16-key tile, are e < 8).
+      f32x16 acc = f32x16{};
+#pragma unroll
+      for (int s2 = 0; s2 < DS; ++s2)
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ka[s2]),
+                                                      qf[rb2][s2], acc, 0, 0, 0);
+      if (!have[rb2]) continue;
+      const int lim = Lr[rb2] - kb;  // keys kl < lim are eligible
+      if (!EMIT) {
+        float tm = kNegInf;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+          if (kl < lim) tm = fmaxf(tm, acc[e]);
+        }
+        m[rb2] = fmaxf(m[rb2], tm);
+        continue;
+      }
+      uint32_t w = 0u;
+      auto do_tile = [&](const int e0, const int ne, const int toff) __attribute__((always_inline)) {
+        float tm = kNegInf;
+#pragma unroll
+        for (int e = e0; e < e0 + ne; ++e) {
+          const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+          if (kl < lim) tm = fmaxf(tm, acc[e]);
+        }
+        tm = fmaxf(tm, __shfl_xor(tm, 32));
+        const bool fresh = (static_cast<uint32_t>(kb + toff) & gmask) == 0u;  // a group starts
+        const float mn = fmaxf(fresh ? kNegInf : m[rb2], tm);
+        if (__any(mn != m[rb2])) thr[rb2] = tiled_threshold(mn, p.tiled_a);
+        m[rb2] = mn;
+#pragma unroll
+        for (int e = e0; e < e0 + ne; ++e) {
+          const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+          w |= (kl < lim && acc[e] >= thr[rb2]) ? 1u << kl : 0u;
+        }
+      };
+      if (two_tiles) {
+        do_tile(0, 8, 0);
+        do_tile(8, 8, 16);
+      } else {
+        do_tile(0, 16, 0);
+      }
+      w |= __shfl_xor(w, 32);
+      if (g == 0) p.bsel[(row0 + rb2 * 32 + ln) * p.W + kb / 32] = w;
+    }
+  };
+
+  u32x4 k0[DS], k1[DS];
+  int j = 0;
+  kload(k0, blk_of(0));
+  for (; blk_of(j + 1) < nblk; j += 2) {
+    kload(k1, blk_of(j + 1));
+    proc(k0, blk_of(j));
+    kload(k0, blk_of(j + 2));
+    proc(k1, blk_of(j + 1));
+  }
+  if (blk_of(j) < nblk) proc(k0, blk_of(j));
+
+  if (!EMIT) {  // this wave's quarter: its maximum per row
+#pragma unroll
+    for (int rb2 = 0; rb2 < 2; ++rb2) {
+      const float mx = fmaxf(m[rb2], __shfl_xor(m[rb2], 32));
+      if (have[rb2] && g == 0) p.qmax[(row0 + rb2 * 32 + ln) * nq + sp * 4 + wave] = mx;
+    }
+  }
+}
+
+// Per row: replace each quarter's maximum by the running maximum of the
+// group's earlier quarters (-inf where a group starts).  One thread per row.
+__global__ __launch_bounds__(256) void k_tiled_carry(SelParams p) {
+  const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (r >= p.rows) return;
+  const int i = static_cast<int>(r % p.Np);
+  const int L = eligible(i, p.P, p.N, p.causal);
+  const int rq = p.split / 4;
+  const int nq = 4 * p.nsplit;
+  const int used = (L + rq - 1) / rq;  // quarters holding eligible keys of this row
+  float run = kNegInf;
+  for (int q = 0; q < used; ++q) {
+    if ((static_cast<int64_t>(q) * rq) % p.tiled_gs == 0) run = kNegInf;
+    const float x = p.qmax[r * nq + q];
+    p.qmax[r * nq + q] = run;
+    run = fmaxf(run, x);
+  }
+}
+
+// Row state the compact step reads, for cross-tile minS launches.
+__global__ __launch_bounds__(256) void k_tiled_init(SelParams p) {
+  const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (r >= p.rows) return;
+  RowState& s = p.st[r];
+  s.L = eligible(static_cast<int>(r % p.Np), p.P, p.N, p.causal);
+  s.tie_partial = 0;
+  s.k_eq = 0;
+  s.phase = PH_EMIT;
+}
+
+// ---------------------------------------------------------------------------
 // Resolve after a HIST pass: one wave per row.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
@@ -1037,6 +1230,8 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
   const int n = min(base, static_cast<int>(p.cap));
   for (int t = n + lane; t < p.cap; t += 64) out[t] = -1;
   if (lane == 0) p.counts[r] = n;
+  // Cross-tile minS keeps a block's first cap keys (key order) and counts it.
+  if (lane == 0 && p.mode_tiled && base > p.cap && p.n_clamped) atomicAdd(p.n_clamped, 1);
 }
 
 __global__ __launch_bounds__(256) void k_zero_u32(uint32_t* p, int64_t n) {
@@ -1048,7 +1243,7 @@ __global__ __launch_bounds__(256) void k_zero_u32(uint32_t* p, int64_t n) {
 // Workspace layout.
 // ---------------------------------------------------------------------------
 struct Layout {
-  size_t qp, state, hist, nab, mab, zp, cand_n, cand_lohi, cand, bsel, btie, qnorm, kmax, total;
+  size_t qp, state, hist, nab, mab, zp, cand_n, cand_lohi, cand, bsel, btie, qnorm, kmax, qmax, total;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -1074,6 +1269,7 @@ Layout layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t D, int32_t 
   l.btie = take(rows * W * 4);
   l.qnorm = take(rows * 4);
   l.kmax = take(B * Hkv * 4);
+  l.qmax = take(rows * nsplit * 4 * 4);
   l.total = o;
   return l;
 }
@@ -1157,12 +1353,57 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.mode_topp = a.mode == 1;
   p.mode_mins = a.mode == 2;
   p.mins_direct = p.mode_mins && a.cap >= N;
+  p.mode_tiled = a.mode == 3;
+  p.qmax = reinterpret_cast<float*>(ws + l.qmax);
   p.param = a.param;
   p.tau = 1.0f / sqrtf(static_cast<float>(D));
 
   // Pooled queries (Eq. 2) into the workspace, contiguous [rows][D].
   hipError_t e = launch_pool(a.q, P, const_cast<uint16_t*>(p.qp), Hq * Np * D, Np * D, D, stream);
   if (e != hipSuccess) return e;
+  const dim3 rgrid(static_cast<unsigned>(rows));
+  const dim3 igrid(static_cast<unsigned>((rows + 255) / 256));
+
+  if (p.mode_tiled) {
+    // Cross-tile minS: one emitting pass (after a quarter-maximum pass when a
+    // group of tiles spans more than a split), then the lists.  Splits hold
+    // whole groups when groups are at most a split long.
+    const int64_t gs = static_cast<int64_t>(a.tile) * a.group_tiles;  // a power of two
+    int64_t st = N < 4096 ? ((N + 127) / 128) * 128 : 4096;
+    if (gs <= st) {
+      const int64_t unit = gs > 128 ? gs : 128;
+      if (N < 4096) st = ((N + unit - 1) / unit) * unit;
+      p.tiled_carry = 0;
+      p.tiled_sb = static_cast<int>((gs > 32 ? gs : 32) / 32);
+    } else {
+      p.tiled_carry = 1;
+      p.tiled_sb = static_cast<int>(st / 128);  // a quarter of the split
+    }
+    p.split = static_cast<int>(st);
+    p.nsplit = static_cast<int>((N + st - 1) / st);
+    p.tiled_tile = a.tile;
+    p.tiled_gs = static_cast<int>(gs);
+    p.tiled_a = a.param * sqrt(static_cast<double>(D));  // alpha / tau
+    p.items = B * Hq * static_cast<int64_t>(p.nsplit) * p.nrb;
+    p.per_xcd = (p.items + 7) / 8;
+    const dim3 tgrid(static_cast<unsigned>(p.per_xcd * 8));
+    hipLaunchKernelGGL(k_tiled_init, igrid, dim3(256), 0, stream, p);
+    if (D == 128) {
+      if (p.tiled_carry) {
+        hipLaunchKernelGGL((k_mins_tiled<128, false>), tgrid, dim3(kThreads), 0, stream, p);
+        hipLaunchKernelGGL(k_tiled_carry, igrid, dim3(256), 0, stream, p);
+      }
+      hipLaunchKernelGGL((k_mins_tiled<128, true>), tgrid, dim3(kThreads), 0, stream, p);
+    } else {
+      if (p.tiled_carry) {
+        hipLaunchKernelGGL((k_mins_tiled<64, false>), tgrid, dim3(kThreads), 0, stream, p);
+        hipLaunchKernelGGL(k_tiled_carry, igrid, dim3(256), 0, stream, p);
+      }
+      hipLaunchKernelGGL((k_mins_tiled<64, true>), tgrid, dim3(kThreads), 0, stream, p);
+    }
+    hipLaunchKernelGGL(k_compact, rgrid, dim3(64), 0, stream, p);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_qnorm, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream,
                      p.qp, rows, static_cast<int>(D), p.qnorm);
   hipLaunchKernelGGL(k_kmax_init, dim3(static_cast<unsigned>((B * Hkv + 255) / 256)), dim3(256), 0,
@@ -1176,8 +1417,6 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.items = B * Hq * static_cast<int64_t>(p.nsplit) * p.nrb;
   p.per_xcd = (p.items + 7) / 8;
   const dim3 pgrid(static_cast<unsigned>(p.per_xcd * 8));
-  const dim3 rgrid(static_cast<unsigned>(rows));
-  const dim3 igrid(static_cast<unsigned>((rows + 255) / 256));
   // Only topP rows can be sent back for a second round (count above cap).
   const int rounds = p.mode_topp ? kRounds : 1;
   for (int round = 0; round < rounds; ++round) {

@@ -41,10 +41,23 @@ int64_t topk_count(double ratio, int64_t L) {
   return k;
 }
 
+bool mode_ok(int32_t mode) {
+  return mode == VECATTN_SEL_TOPK || mode == VECATTN_SEL_TOPP || mode == VECATTN_SEL_MINS ||
+         mode == VECATTN_SEL_MINS_TILED;
+}
+
 bool param_ok(int32_t mode, double param) {
   if (mode == VECATTN_SEL_TOPK || mode == VECATTN_SEL_TOPP) return param > 0.0 && param <= 1.0;
-  if (mode == VECATTN_SEL_MINS) return param >= 0.0;
+  if (mode == VECATTN_SEL_MINS || mode == VECATTN_SEL_MINS_TILED) return param >= 0.0;
   return false;
+}
+
+// Tile of 16 or 32 keys; a power-of-two number of tiles per group, at most
+// 2^30 keys per group.
+bool tiling_ok(int32_t tile, int32_t group_tiles) {
+  if (tile != 16 && tile != 32) return false;
+  if (group_tiles < 1 || (group_tiles & (group_tiles - 1)) != 0) return false;
+  return static_cast<int64_t>(tile) * group_tiles <= (int64_t(1) << 30);
 }
 
 // Largest count any block can produce (k_i is non-decreasing in L_i, so the
@@ -55,11 +68,38 @@ int64_t max_count(int64_t N, int32_t P, int32_t causal, int32_t mode, double par
   return mode == VECATTN_SEL_TOPK ? topk_count(param, Lmax) : Lmax;
 }
 
+vecattn_status select_impl(const void* q, const vecattn_tdesc* qd, const void* k,
+                           const vecattn_tdesc* kd, int32_t block, int32_t causal, int32_t mode,
+                           double param, int32_t tile, int32_t group_tiles, int32_t* idx,
+                           int64_t cap, int32_t* counts, int32_t* n_clamped, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  vecattn_status st = check_desc(q, qd);
+  if (st != VECATTN_OK) return st;
+  st = check_desc(k, kd);
+  if (st != VECATTN_OK) return st;
+  if (kd->B != qd->B || kd->N != qd->N || kd->D != qd->D || qd->H % kd->H != 0)
+    return VECATTN_ERR_INVALID_ARG;
+  if (!idx || !counts || block < 1 || cap < 1 || cap > kMaxN) return VECATTN_ERR_INVALID_ARG;
+  if (!mode_ok(mode) || !param_ok(mode, param)) return VECATTN_ERR_INVALID_ARG;
+  if (mode == VECATTN_SEL_MINS_TILED && !tiling_ok(tile, group_tiles))
+    return VECATTN_ERR_INVALID_ARG;
+  if (mode == VECATTN_SEL_TOPK && cap < max_count(qd->N, block, causal, mode, param))
+    return VECATTN_ERR_CAPACITY;
+  const size_t need = vecattn::select_workspace_bytes(qd->B, qd->H, qd->N, qd->D, block, mode, cap);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return VECATTN_ERR_CAPACITY;
+  if (workspace && !aligned16(workspace)) return VECATTN_ERR_INVALID_ARG;
+  vecattn::SelectArgs a{to_tensor(q, qd), to_tensor(k, kd), block, causal ? 1 : 0, mode, param,
+                        tile, group_tiles, idx, cap, counts, n_clamped, workspace,
+                        workspace_bytes};
+  hipError_t e = vecattn::launch_select(a, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
+}
+
 }  // namespace
 
 extern "C" {
 
-int32_t vecattn_version(void) { return 100; }
+int32_t vecattn_version(void) { return 101; }
 
 const char* vecattn_status_string(vecattn_status s) {
   switch (s) {
@@ -88,7 +128,7 @@ vecattn_status vecattn_pool(const void* q, const vecattn_tdesc* qd, int32_t bloc
 
 vecattn_status vecattn_select_max_count(int64_t N, int32_t block, int32_t causal, int32_t mode,
                                         double param, int64_t* out) {
-  if (!out || N < 1 || N > kMaxN || block < 1 || !param_ok(mode, param))
+  if (!out || N < 1 || N > kMaxN || block < 1 || !mode_ok(mode) || !param_ok(mode, param))
     return VECATTN_ERR_INVALID_ARG;
   *out = max_count(N, block, causal, mode, param);
   return VECATTN_OK;
@@ -99,8 +139,7 @@ vecattn_status vecattn_select_workspace_size(const vecattn_tdesc* qd, const veca
                                              int64_t cap, size_t* bytes) {
   (void)causal;
   if (!qd || !kd || !bytes || block < 1 || cap < 1) return VECATTN_ERR_INVALID_ARG;
-  if (mode != VECATTN_SEL_TOPK && mode != VECATTN_SEL_TOPP && mode != VECATTN_SEL_MINS)
-    return VECATTN_ERR_INVALID_ARG;
+  if (!mode_ok(mode)) return VECATTN_ERR_INVALID_ARG;
   *bytes = vecattn::select_workspace_bytes(qd->B, qd->H, qd->N, qd->D, block, mode, cap);
   return VECATTN_OK;
 }
@@ -110,25 +149,19 @@ vecattn_status vecattn_select(const void* q, const vecattn_tdesc* qd, const void
                               double param, int32_t* idx, int64_t cap, int32_t* counts,
                               int32_t* n_clamped, void* workspace, size_t workspace_bytes,
                               void* stream) {
-  vecattn_status st = check_desc(q, qd);
-  if (st != VECATTN_OK) return st;
-  st = check_desc(k, kd);
-  if (st != VECATTN_OK) return st;
-  if (kd->B != qd->B || kd->N != qd->N || kd->D != qd->D || qd->H % kd->H != 0)
-    return VECATTN_ERR_INVALID_ARG;
-  if (!idx || !counts || block < 1 || cap < 1 || cap > kMaxN) return VECATTN_ERR_INVALID_ARG;
-  if (mode != VECATTN_SEL_TOPK && mode != VECATTN_SEL_TOPP && mode != VECATTN_SEL_MINS)
-    return VECATTN_ERR_INVALID_ARG;
-  if (!param_ok(mode, param)) return VECATTN_ERR_INVALID_ARG;
-  if (mode == VECATTN_SEL_TOPK && cap < max_count(qd->N, block, causal, mode, param))
-    return VECATTN_ERR_CAPACITY;
-  const size_t need = vecattn::select_workspace_bytes(qd->B, qd->H, qd->N, qd->D, block, mode, cap);
-  if (need > 0 && (!workspace || workspace_bytes < need)) return VECATTN_ERR_CAPACITY;
-  if (workspace && !aligned16(workspace)) return VECATTN_ERR_INVALID_ARG;
-  vecattn::SelectArgs a{to_tensor(q, qd), to_tensor(k, kd), block, causal ? 1 : 0, mode, param,
-                        idx, cap, counts, n_clamped, workspace, workspace_bytes};
-  hipError_t e = vecattn::launch_select(a, static_cast<hipStream_t>(stream));
-  return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
+  // Cross-tile minS through this entry point uses the paper's B_K = G_K = 16.
+  return select_impl(q, qd, k, kd, block, causal, mode, param, 16, 16, idx, cap, counts,
+                     n_clamped, workspace, workspace_bytes, stream);
+}
+
+vecattn_status vecattn_select_mins_tiled(const void* q, const vecattn_tdesc* qd, const void* k,
+                                         const vecattn_tdesc* kd, int32_t block, int32_t causal,
+                                         double alpha, int32_t tile, int32_t group_tiles,
+                                         int32_t* idx, int64_t cap, int32_t* counts,
+                                         int32_t* n_clamped, void* workspace,
+                                         size_t workspace_bytes, void* stream) {
+  return select_impl(q, qd, k, kd, block, causal, VECATTN_SEL_MINS_TILED, alpha, tile,
+                     group_tiles, idx, cap, counts, n_clamped, workspace, workspace_bytes, stream);
 }
 
 vecattn_status vecattn_sparse_attn(const void* q, const vecattn_tdesc* qd, const void* k,

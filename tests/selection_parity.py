@@ -7,6 +7,9 @@ may differ only where two keys' scores are within 1e-5 * max|s| of the cut:
         tolerance of the oracle's k-th score.
   minS: every key in the symmetric difference lies within the tolerance of
         rowmax - alpha (rows clamped to cap follow the topK rule);
+  cross-tile minS (Algorithm 1): every key in the symmetric difference lies
+        within the tolerance of its own threshold, the running maximum of its
+        group's tiles up to its tile, minus alpha;
   topP: every key in the symmetric difference lies within the tolerance of
         the oracle's cut score, or the oracle's cumulative mass at the cut is
         within 1e-5 of p (then the counts differ by at most one); the GPU set's
@@ -86,4 +89,63 @@ def check_rows(q, k, block, mode, param, causal, cap, idx_gpu, cnt_gpu, rows, co
             if cg < cap:
                 e = np.exp(s - s.max())
                 assert e[g].sum() / e.sum() >= param - MASS_TOL, f"row {w}: mass below p"
+    return mismatched
+
+
+def running_threshold(s, alpha, bk, gk):
+    """Per key: (maximum over its group's tiles up to its own tile) - alpha,
+    the threshold Algorithm 1 compares it with (used only to place the
+    tolerance of the cross-tile minS rule; the reference set is the oracle's)."""
+    L = len(s)
+    thr = np.empty(L)
+    gs = bk * gk
+    for g0 in range(0, L, gs):
+        run = -np.inf
+        for t0 in range(g0, min(L, g0 + gs), bk):
+            t1 = min(L, t0 + bk)
+            run = max(run, s[t0:t1].max())
+            thr[t0:t1] = run - alpha
+    return thr
+
+
+def check_rows_tiled(q, k, block, alpha, causal, bk, gk, idx_gpu, cnt_gpu, rows, compact=False):
+    """Cross-tile minS parity for rows none of which exceeded the GPU's cap.
+    Returns the number of rows whose sets differ (all within the rule)."""
+    B, Hq, N, D = q.shape
+    Np = (N + block - 1) // block
+    cap_o = N
+    if compact:
+        idx_o, cnt_o, ncl = oracle.select_mins_tiled(q, k, block, alpha, causal, cap_o, bk, gk,
+                                                     rows=rows, compact=True)
+        pos = {int(w): t for t, w in enumerate(rows)}
+    else:
+        idx_o, cnt_o, ncl = oracle.select_mins_tiled(q, k, block, alpha, causal, cap_o, bk, gk,
+                                                     rows=rows)
+        pos = {int(w): int(w) for w in rows}
+    assert ncl == 0
+    idx_o = idx_o.reshape(-1, cap_o)
+    cnt_o = cnt_o.reshape(-1)
+    idx_gpu = idx_gpu.reshape(-1, idx_gpu.shape[-1])
+    cnt_gpu = cnt_gpu.reshape(-1)
+    mismatched = 0
+    for w in rows:
+        w = int(w)
+        pw = pos[w]
+        i, h, b = w % Np, (w // Np) % Hq, w // (Np * Hq)
+        s = oracle.pooled_scores(q, k, block, causal, b, h, i)
+        L = len(s)
+        tol = REL_TOL * np.abs(s).max()
+        cg, co = int(cnt_gpu[pw]), int(cnt_o[pw])
+        g = idx_gpu[pw, :cg]
+        o = idx_o[pw, :co]
+        assert cg < idx_gpu.shape[1] or cg == co, (w, cg)
+        assert np.all(np.diff(g) > 0), f"row {w}: not strictly ascending"
+        assert cg == 0 or (g[0] >= 0 and g[-1] < L), f"row {w}: index out of range"
+        assert np.all(idx_gpu[pw, cg:] == -1), f"row {w}: padding"
+        diff = np.setxor1d(g, o)
+        if diff.size:
+            mismatched += 1
+            thr = running_threshold(s, alpha, bk, gk)
+            gap = np.abs(s[diff] - thr[diff])
+            assert np.all(gap <= tol), f"row {w}: cross-tile minS differs beyond near-threshold: {gap.max()}"
     return mismatched

@@ -111,11 +111,42 @@ def test_select_rejects_bad_arguments():
     assert select(kd=desc(1, 2, 255, 128)) == INVALID
     assert select(mode=2, param=-0.5) == INVALID           # minS: alpha >= 0
     assert select(mode=2, param=float('nan')) == INVALID
+    assert select(mode=3, param=-0.5) == INVALID           # cross-tile minS: alpha >= 0
+    assert select(mode=3, param=float('nan')) == INVALID
     assert select(cap=63) == CAPACITY                      # topK 25% of 256 keys = 64
     assert select(ws=None) == CAPACITY
     assert select(ws_bytes=16) == CAPACITY
     d64 = desc(1, 4, 256, 96)
     assert select(qd=d64, kd=desc(1, 2, 256, 96)) == UNSUPPORTED
+
+
+def select_tiled(q=FAKE, qd=None, k=FAKE, kd=None, block=64, causal=0, alpha=0.5, tile=16,
+                 group_tiles=16, idx=FAKE, cap=256, cnt=FAKE, ws=FAKE, ws_bytes=1 << 40):
+    lib = _lib.load()
+    qd = qd or desc(1, 4, 256, 128)
+    kd = kd or desc(1, 2, 256, 128)
+    return lib.vecattn_select_mins_tiled(q, ctypes.byref(qd), k, ctypes.byref(kd), block, causal,
+                                         alpha, tile, group_tiles, idx, cap, cnt, None, ws,
+                                         ws_bytes, None)
+
+
+def test_select_mins_tiled_rejects_bad_arguments():
+    assert select_tiled(q=None) == INVALID
+    assert select_tiled(idx=None) == INVALID
+    assert select_tiled(alpha=-1.0) == INVALID
+    assert select_tiled(alpha=float("nan")) == INVALID
+    for tile in (0, 8, 24, 64):
+        assert select_tiled(tile=tile) == INVALID
+    for gt in (0, -4, 3, 12):
+        assert select_tiled(group_tiles=gt) == INVALID
+    assert select_tiled(group_tiles=1 << 27) == INVALID     # 2^30 keys per group at most
+    assert select_tiled(block=0) == INVALID
+    assert select_tiled(cap=0) == INVALID
+    assert select_tiled(ws=None) == CAPACITY                 # otherwise valid
+    d96 = desc(1, 4, 256, 96)
+    assert select_tiled(qd=d96, kd=desc(1, 2, 256, 96)) == UNSUPPORTED
+    assert va.max_count(75600, 64, False, "mins_tiled", 0.5) == 75600
+    assert va.max_count(1000, 64, True, "mins_tiled", 0.5) == 1000
 
 
 def test_workspace_size_query():

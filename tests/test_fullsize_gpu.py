@@ -5,7 +5,8 @@ random sample of query blocks: the selection rule of selection_parity and
 the attention bar of test_attn_gpu (max-abs 2e-2, mean-abs 2e-3 against the
 fp64 oracle on the GPU's own lists).  Plus properties that hold for every
 block: lists ascending and in range, counts within [1, cap], and for topK the
-exact budget."""
+exact budget.  Algorithm 1's cross-tile minS runs on the 75k DiT layer's
+full sequence length (8 of its heads, so that cap = N lists stay small)."""
 import math
 import os
 
@@ -16,7 +17,7 @@ import torch
 import oracle
 import paper_2603_29494_amd as va
 from paper_2603_29494_amd import synth
-from selection_parity import check_rows
+from selection_parity import check_rows, check_rows_tiled
 
 pytestmark = pytest.mark.gpu
 
@@ -85,3 +86,36 @@ def test_workload_full_size(gpu, cid):
     assert err.max() <= 2e-2 and err.mean() <= 2e-3, (err.max(), err.mean())
     print(f"workload {cid}: {len(rows)} sampled blocks, max|dO| {err.max():.2e}, "
           f"mean|dO| {err.mean():.2e}", flush=True)
+
+
+@pytest.mark.parametrize("group_tiles", [16, 8192])
+def test_mins_tiled_full_length(gpu, group_tiles):
+    layer = synth.make_layer(4, heads=range(8))
+    w = layer.w
+    q, k = dev(layer.q), dev(layer.k)
+    B, Hq, N, D = q.shape
+    P = w.block
+    Np = (N + P - 1) // P
+    alpha = 0.5
+    print(f"cross-tile minS, N {N}, G_K {group_tiles}", flush=True)
+    ncl = torch.zeros(1, dtype=torch.int32, device="cuda")
+    idx, cnt = va.select(q, k, P, "mins_tiled", alpha, False, cap=N, n_clamped=ncl, tile=16,
+                         group_tiles=group_tiles)
+    torch.cuda.synchronize()
+    assert int(ncl.item()) == 0
+    c = cnt.long().view(-1)
+    assert bool((c >= 1).all()) and bool((c <= N).all())
+    flat = idx.view(-1, N)
+    col = torch.arange(N, device="cuda")
+    for s in range(0, flat.shape[0], 256):
+        f, cf = flat[s:s + 256], c[s:s + 256]
+        live = col.view(1, -1) < cf.view(-1, 1)
+        assert bool(((f >= 0) & (f < N) | ~live).all()) and bool(((f == -1) | live).all())
+        assert bool(((f[:, 1:] > f[:, :-1]) | ~live[:, 1:]).all()), "lists ascending"
+    rng = np.random.Generator(np.random.PCG64(5151 + group_tiles))
+    rows = np.sort(rng.choice(B * Hq * Np, size=SAMPLE_BLOCKS, replace=False))
+    rsel = torch.from_numpy(rows).cuda()
+    check_rows_tiled(layer.q, layer.k, P, alpha, False, 16, group_tiles,
+                     flat[rsel].cpu().numpy(), c[rsel].int().cpu().numpy(), rows, compact=True)
+    print(f"cross-tile minS G_K {group_tiles}: mean keep {float(c.double().mean()) / N:.3f}",
+          flush=True)

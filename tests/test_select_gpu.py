@@ -1,6 +1,6 @@
 """GPU parity of important-vector selection (Sec. 3.1: pooled-query scores,
-row-wise topK / topP) against the oracle, through the C ABI.  The index-set
-rule is in selection_parity.py."""
+row-wise topK / topP, minS of Eq. 3 and Algorithm 1's cross-tile minS) against
+the oracle, through the C ABI.  The index-set rule is in selection_parity.py."""
 import numpy as np
 import pytest
 import torch
@@ -9,7 +9,7 @@ import oracle
 import paper_2603_29494_amd as va
 from paper_2603_29494_amd import synth
 
-from selection_parity import check_rows
+from selection_parity import check_rows, check_rows_tiled
 
 pytestmark = pytest.mark.gpu
 
@@ -177,3 +177,55 @@ def test_mins_clamped_to_cap(gpu):
     assert int(ncl.item()) == ncl_o and ncl_o > 0
     check_rows(q, k, 64, oracle.MINS, 3.0, False, cap, idx.cpu().numpy(), cnt.cpu().numpy(),
                all_rows(q, 64))
+
+
+TILED_CASES = [
+    # B, Hq, Hkv, N, D, block, causal, alpha, tile (B_K), group_tiles (G_K)
+    (1, 2, 2, 700, 128, 64, False, 0.0, 16, 16),
+    (1, 2, 2, 700, 128, 64, False, 0.3, 16, 1),       # every 16-key tile its own group
+    (1, 4, 2, 1000, 128, 64, True, 0.5, 32, 4),
+    (2, 2, 1, 513, 64, 32, False, 1.0, 16, 16),
+    (1, 2, 2, 600, 64, 64, True, float("inf"), 16, 16),
+    (1, 2, 2, 300, 128, 64, False, 0.2, 16, 16),       # groups inside one short split
+    (1, 2, 2, 300, 128, 64, False, 0.2, 16, 32),       # a group longer than the split
+    (1, 1, 1, 6000, 128, 64, False, 0.4, 16, 16),
+    (1, 1, 1, 6000, 128, 64, True, 0.4, 16, 8192),     # one group per row, across splits
+    (1, 1, 1, 9000, 64, 16, False, 0.6, 32, 256),      # 8192-key groups: a reset mid-row
+]
+
+
+@pytest.mark.parametrize("case", TILED_CASES)
+def test_mins_tiled_matches_oracle(gpu, case):
+    B, Hq, Hkv, N, D, block, causal, alpha, bk, gk = case
+    q, k, _ = synth.planted_case(hash(case) % 10000 + 200, B, Hq, Hkv, N, D)
+    cap = va.max_count(N, block, causal, "mins_tiled", alpha)
+    ncl = torch.zeros(1, dtype=torch.int32, device="cuda")
+    idx, cnt = va.select(dev(q), dev(k), block, "mins_tiled", alpha, causal, cap=cap,
+                         n_clamped=ncl, tile=bk, group_tiles=gk)
+    torch.cuda.synchronize()
+    assert int(ncl.item()) == 0
+    rows = all_rows(q, block)
+    mism = check_rows_tiled(q, k, block, alpha, causal, bk, gk, idx.cpu().numpy(),
+                            cnt.cpu().numpy(), rows)
+    assert mism <= max(1, len(rows) // 20)
+
+
+def test_mins_tiled_default_tiling_and_clamp(gpu):
+    # mode "mins_tiled" without tiling arguments is B_K = G_K = 16; a block
+    # selecting more than cap keys keeps its first cap keys and is counted.
+    q, k, _ = synth.planted_case(14, 1, 2, 2, 2000, 128)
+    full = va.max_count(2000, 64, False, "mins_tiled", 1.0)
+    a_idx, a_cnt = va.select(dev(q), dev(k), 64, "mins_tiled", 1.0, False, cap=full)
+    b_idx, b_cnt = va.select(dev(q), dev(k), 64, va.SEL_MINS_TILED, 1.0, False, cap=full,
+                             tile=16, group_tiles=16)
+    cap = 120
+    ncl = torch.zeros(1, dtype=torch.int32, device="cuda")
+    c_idx, c_cnt = va.select(dev(q), dev(k), 64, "mins_tiled", 1.0, False, cap=cap, n_clamped=ncl)
+    torch.cuda.synchronize()
+    assert torch.equal(a_idx, b_idx) and torch.equal(a_cnt, b_cnt)
+    a_cnt, a_idx = a_cnt.cpu().numpy(), a_idx.cpu().numpy()
+    c_cnt, c_idx = c_cnt.cpu().numpy(), c_idx.cpu().numpy()
+    assert int(ncl.item()) == int(np.sum(a_cnt > cap)) > 0
+    assert np.array_equal(c_cnt, np.minimum(a_cnt, cap))
+    assert np.array_equal(c_idx, a_idx[..., :cap])
+    check_rows_tiled(q, k, 64, 1.0, False, 16, 16, a_idx, a_cnt, all_rows(q, 64))

@@ -30,7 +30,8 @@
 // Work decomposition of a pass: a workgroup owns 64 pooled rows (query
 // blocks) of one head and one split of up to `split` keys; its 4 waves take
 // the split's 32-key blocks in turn.  S^T = K_blk Q_p^T uses
-// v_mfma_f32_32x32x16_bf16 with the pooled queries held in registers.
+// v_mfma_f32_32x32x16_bf16 with the pooled queries held in registers and K
+// read from a copy in MFMA operand order that each call writes once.
 #include <float.h>
 
 #include "device_common.h"
@@ -82,7 +83,8 @@ struct RowState {
 struct SelParams {
   const uint16_t* qp;     // pooled queries, [rows][D] contiguous, rows = bh * Np + i
   const uint16_t* k;
-  int64_t k_sB, k_sH, k_sN;
+  const u32x4* kop;       // K in MFMA operand order: [B * Hkv][nkb][D / 16][64 lanes] x 16 B
+  int nkb;                // 32-key blocks per key/value head
   RowState* st;
   uint32_t* hist;         // [rows][kBins]
   uint32_t* n_above;      // [rows][nsplit]
@@ -185,6 +187,31 @@ __device__ __forceinline__ void narrow(float& s_lo, float& s_hi, float mul, floa
 // Per-row setup: eligible keys, targets, first interval [-c, c] with
 // c >= |q_p| * max |k| (Cauchy-Schwarz, padded for fp32 rounding).
 // ---------------------------------------------------------------------------
+// K of every key/value head in MFMA operand order, once per call: for each
+// 32-key block and head-dim step s2, the 64 lanes' A-operand pieces (lane l:
+// key l % 32 of the block, head-dim values 16 s2 + 8 (l / 32) .. +7) lie
+// contiguously, so a score pass fetches each step with one fully coalesced
+// 1 KB load instead of 32 rows x 32 bytes.  Keys past N repeat key N - 1
+// (they are never eligible).  One wave per 32-key block.
+template <int D>
+__global__ __launch_bounds__(256) void k_k_operand_order(const uint16_t* __restrict__ k, int64_t sB,
+                                                         int64_t sH, int64_t sN, int Hkv, int N,
+                                                         int nkb, int64_t nblk_total,
+                                                         u32x4* __restrict__ kop) {
+  constexpr int DS = D / 16;
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (t >= nblk_total) return;
+  const int lane = threadIdx.x & 63, g = lane >> 5, ln = lane & 31;
+  const int blk = static_cast<int>(t % nkb);
+  const int64_t bh = t / nkb;
+  const int64_t b = bh / Hkv, hk = bh % Hkv;
+  const int key = min(blk * 32 + ln, N - 1);
+  const u32x4* src = reinterpret_cast<const u32x4*>(k + b * sB + hk * sH + key * sN);
+  u32x4* dst = kop + t * (DS * 64) + lane;
+#pragma unroll
+  for (int s2 = 0; s2 < DS; ++s2) dst[s2 * 64] = src[2 * s2 + g];
+}
+
 __global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
   const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (r >= p.rows) return;
@@ -401,16 +428,17 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   double zacc[2] = {0.0, 0.0}, macc[2] = {0.0, 0.0};
   uint32_t nacc[2] = {0u, 0u};
 
-  const uint16_t* kh = p.k + b * p.k_sB + hk * p.k_sH;
   const int nblk = (key1 - key0 + 31) / 32;
   // K of a 32-key block as the A operand (lane -> key ln, head-dim slots
-  // 16s + 8g .. +7); the next block of this wave is loaded while the current
-  // one is processed (addresses are clamped, so loads past the end are safe).
+  // 16s + 8g .. +7), from the operand-order copy: one coalesced 1 KB load per
+  // head-dim step.  The next block of this wave is loaded while the current
+  // one is processed (block indices are clamped, so loads past the end are safe).
   auto kload = [&](u32x4 (&dst)[DS], int blk) __attribute__((always_inline)) {
-    const int kr = min(key0 + blk * 32 + ln, p.N - 1);
-    const u32x4* ksrc = reinterpret_cast<const u32x4*>(kh + static_cast<int64_t>(kr) * p.k_sN);
+    const int kbi = min(key0 / 32 + blk, p.nkb - 1);
+    const u32x4* ksrc =
+        p.kop + ((static_cast<int64_t>(b) * p.Hkv + hk) * p.nkb + kbi) * (DS * 64) + lane;
 #pragma unroll
-    for (int s2 = 0; s2 < DS; ++s2) dst[s2] = ksrc[2 * s2 + g];
+    for (int s2 = 0; s2 < DS; ++s2) dst[s2] = ksrc[s2 * 64];
   };
   auto kproc = [&](const u32x4 (&ka)[DS], int blk) __attribute__((always_inline)) {
     const int kb = key0 + blk * 32;
@@ -783,12 +811,12 @@ __global__ __launch_bounds__(kThreads) void k_mins_tiled(SelParams p) {
     thr[rb2] = tiled_threshold(m[rb2], p.tiled_a);
   }
 
-  const uint16_t* kh = p.k + b * p.k_sB + hk * p.k_sH;
   auto kload = [&](u32x4 (&dst)[DS], int blk) __attribute__((always_inline)) {
-    const int kr = min(key0 + blk * 32 + ln, p.N - 1);  // clamped: loads past the end are safe
-    const u32x4* ksrc = reinterpret_cast<const u32x4*>(kh + static_cast<int64_t>(kr) * p.k_sN);
+    const int kbi = min(key0 / 32 + blk, p.nkb - 1);  // clamped: loads past the end are safe
+    const u32x4* ksrc =
+        p.kop + ((static_cast<int64_t>(b) * p.Hkv + hk) * p.nkb + kbi) * (DS * 64) + lane;
 #pragma unroll
-    for (int s2 = 0; s2 < DS; ++s2) dst[s2] = ksrc[2 * s2 + g];
+    for (int s2 = 0; s2 < DS; ++s2) dst[s2] = ksrc[s2 * 64];
   };
   // The j-th block this wave visits: segments wave, wave + 4, ... of SB blocks.
   auto blk_of = [&](int j) __attribute__((always_inline)) {
@@ -1243,7 +1271,8 @@ __global__ __launch_bounds__(256) void k_zero_u32(uint32_t* p, int64_t n) {
 // Workspace layout.
 // ---------------------------------------------------------------------------
 struct Layout {
-  size_t qp, state, hist, nab, mab, zp, cand_n, cand_lohi, cand, bsel, btie, qnorm, kmax, qmax, total;
+  size_t qp, state, hist, nab, mab, zp, cand_n, cand_lohi, cand, bsel, btie, qnorm, kmax, qmax, kop,
+      total;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -1270,6 +1299,7 @@ Layout layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t D, int32_t 
   l.qnorm = take(rows * 4);
   l.kmax = take(B * Hkv * 4);
   l.qmax = take(rows * nsplit * 4 * 4);
+  l.kop = take(B * Hkv * ((N + 31) / 32) * 32 * D * 2);
   l.total = o;
   return l;
 }
@@ -1317,9 +1347,6 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   SelParams p{};
   p.qp = reinterpret_cast<const uint16_t*>(ws + l.qp);
   p.k = static_cast<const uint16_t*>(a.k.ptr);
-  p.k_sB = a.k.sB;
-  p.k_sH = a.k.sH;
-  p.k_sN = a.k.sN;
   p.st = reinterpret_cast<RowState*>(ws + l.state);
   p.hist = reinterpret_cast<uint32_t*>(ws + l.hist);
   p.n_above = reinterpret_cast<uint32_t*>(ws + l.nab);
@@ -1355,6 +1382,8 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.mins_direct = p.mode_mins && a.cap >= N;
   p.mode_tiled = a.mode == 3;
   p.qmax = reinterpret_cast<float*>(ws + l.qmax);
+  p.kop = reinterpret_cast<const u32x4*>(ws + l.kop);
+  p.nkb = static_cast<int>((N + 31) / 32);
   p.param = a.param;
   p.tau = 1.0f / sqrtf(static_cast<float>(D));
 
@@ -1363,6 +1392,18 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   if (e != hipSuccess) return e;
   const dim3 rgrid(static_cast<unsigned>(rows));
   const dim3 igrid(static_cast<unsigned>((rows + 255) / 256));
+  {
+    const int64_t nbt = B * Hkv * p.nkb;
+    const dim3 kgrid(static_cast<unsigned>((nbt + 3) / 4));
+    if (D == 128)
+      hipLaunchKernelGGL(k_k_operand_order<128>, kgrid, dim3(256), 0, stream, p.k, a.k.sB, a.k.sH,
+                         a.k.sN, static_cast<int>(Hkv), static_cast<int>(N), p.nkb, nbt,
+                         const_cast<u32x4*>(p.kop));
+    else
+      hipLaunchKernelGGL(k_k_operand_order<64>, kgrid, dim3(256), 0, stream, p.k, a.k.sB, a.k.sH,
+                         a.k.sN, static_cast<int>(Hkv), static_cast<int>(N), p.nkb, nbt,
+                         const_cast<u32x4*>(p.kop));
+  }
 
   if (p.mode_tiled) {
     // Cross-tile minS: one emitting pass (after a quarter-maximum pass when a

@@ -192,24 +192,59 @@ __device__ __forceinline__ void narrow(float& s_lo, float& s_hi, float mul, floa
 // key l % 32 of the block, head-dim values 16 s2 + 8 (l / 32) .. +7) lie
 // contiguously, so a score pass fetches each step with one fully coalesced
 // 1 KB load instead of 32 rows x 32 bytes.  Keys past N repeat key N - 1
-// (they are never eligible).  One wave per 32-key block.
+// (they are never eligible).  One wave per 32-key block.  The same read of K
+// gives the largest key norm per key/value head (kmax, zeroed beforehand):
+// one atomic per workgroup and head.
 template <int D>
 __global__ __launch_bounds__(256) void k_k_operand_order(const uint16_t* __restrict__ k, int64_t sB,
                                                          int64_t sH, int64_t sN, int Hkv, int N,
                                                          int nkb, int64_t nblk_total,
-                                                         u32x4* __restrict__ kop) {
+                                                         u32x4* __restrict__ kop,
+                                                         float* __restrict__ kmax) {
   constexpr int DS = D / 16;
-  const int64_t t = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
-  if (t >= nblk_total) return;
+  __shared__ float s_n2[4];
+  __shared__ int64_t s_bh[4];
+  const int wave = threadIdx.x >> 6;
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * 4 + wave;
   const int lane = threadIdx.x & 63, g = lane >> 5, ln = lane & 31;
-  const int blk = static_cast<int>(t % nkb);
-  const int64_t bh = t / nkb;
-  const int64_t b = bh / Hkv, hk = bh % Hkv;
-  const int key = min(blk * 32 + ln, N - 1);
-  const u32x4* src = reinterpret_cast<const u32x4*>(k + b * sB + hk * sH + key * sN);
-  u32x4* dst = kop + t * (DS * 64) + lane;
+  float n2 = 0.0f;
+  int64_t bh = -1;
+  if (t < nblk_total) {
+    const int blk = static_cast<int>(t % nkb);
+    bh = t / nkb;
+    const int64_t b = bh / Hkv, hk = bh % Hkv;
+    const int key = min(blk * 32 + ln, N - 1);
+    const u32x4* src = reinterpret_cast<const u32x4*>(k + b * sB + hk * sH + key * sN);
+    u32x4* dst = kop + t * (DS * 64) + lane;
 #pragma unroll
-  for (int s2 = 0; s2 < DS; ++s2) dst[s2 * 64] = src[2 * s2 + g];
+    for (int s2 = 0; s2 < DS; ++s2) {
+      const u32x4 w = src[2 * s2 + g];
+      dst[s2 * 64] = w;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float x0 = bf16_bits_to_f32(w[e] & 0xFFFFu), x1 = bf16_bits_to_f32(w[e] >> 16);
+        n2 = __builtin_fmaf(x0, x0, n2);
+        n2 = __builtin_fmaf(x1, x1, n2);
+      }
+    }
+    n2 += __shfl_xor(n2, 32);  // the key's two halves
+    for (int o = 16; o > 0; o >>= 1) n2 = fmaxf(n2, __shfl_xor(n2, o));
+  }
+  if (lane == 0) {
+    s_n2[wave] = n2;
+    s_bh[wave] = bh;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {  // the 4 blocks belong to at most two heads (nkb >= 1: in order)
+    for (int w0 = 0; w0 < 4;) {
+      if (s_bh[w0] < 0) break;
+      float m = s_n2[w0];
+      int w1 = w0 + 1;
+      while (w1 < 4 && s_bh[w1] == s_bh[w0]) m = fmaxf(m, s_n2[w1++]);
+      atomicMax(reinterpret_cast<unsigned int*>(kmax + s_bh[w0]), __float_as_uint(sqrtf(m)));
+      w0 = w1;
+    }
+  }
 }
 
 __global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
@@ -247,8 +282,9 @@ __global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
 }
 
 // ---------------------------------------------------------------------------
-// Norms for the bound: |q_p| per pooled row (from its bf16 values) and the
-// largest |k_j| per key/value head.
+// Norms for the bound: |q_p| per pooled row (from its bf16 values); the
+// largest |k_j| per key/value head comes from k_k_operand_order, after
+// k_kmax_init has zeroed it.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_qnorm(const uint16_t* __restrict__ qp, int64_t rows, int D,
                                                float* __restrict__ out) {
@@ -267,51 +303,6 @@ __global__ __launch_bounds__(256) void k_qnorm(const uint16_t* __restrict__ qp, 
 __global__ __launch_bounds__(256) void k_kmax_init(float* kmax, int n) {
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
   if (t < n) kmax[t] = 0.0f;
-}
-
-constexpr int kKmaxRows = 1024;  // key rows per workgroup of the key-norm kernel
-
-__global__ __launch_bounds__(256) void k_kmax(const uint16_t* __restrict__ k, int64_t sB, int64_t sH,
-                                              int64_t sN, int Hkv, int N, int D,
-                                              float* __restrict__ kmax) {
-  // D / 8 lanes read one key row (16 B each); the workgroup steps over
-  // kKmaxRows rows, four row groups per step, and issues one atomic.
-  __shared__ float s_red[4];
-  const int bh = blockIdx.y;
-  const int b = bh / Hkv, h = bh % Hkv;
-  const int lpr = D / 8;
-  const int rpi = 256 / lpr;
-  const int j0 = blockIdx.x * kKmaxRows + threadIdx.x / lpr;
-  const int j1 = min(N, static_cast<int>(blockIdx.x + 1) * kKmaxRows);
-  const uint16_t* base = k + b * sB + h * sH + 8 * (threadIdx.x % lpr);
-  float best = 0.0f;
-  for (int j = j0; j < j1; j += 4 * rpi) {
-    u32x4 w[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int jj = min(j + u * rpi, j1 - 1);
-      w[u] = *reinterpret_cast<const u32x4*>(base + static_cast<int64_t>(jj) * sN);
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      float acc = 0.0f;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float x0 = bf16_bits_to_f32(w[u][e] & 0xFFFFu), x1 = bf16_bits_to_f32(w[u][e] >> 16);
-        acc = __builtin_fmaf(x0, x0, acc);
-        acc = __builtin_fmaf(x1, x1, acc);
-      }
-      for (int o = 1; o < lpr; o <<= 1) acc += __shfl_xor(acc, o);
-      best = fmaxf(best, acc);  // rows past j1 repeat row j1 - 1
-    }
-  }
-  for (int o = 32; o > 0; o >>= 1) best = fmaxf(best, __shfl_xor(best, o));
-  if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = best;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const float m = sqrtf(fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3])));
-    atomicMax(reinterpret_cast<unsigned int*>(kmax + bh), __float_as_uint(m));
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1392,17 +1383,19 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   if (e != hipSuccess) return e;
   const dim3 rgrid(static_cast<unsigned>(rows));
   const dim3 igrid(static_cast<unsigned>((rows + 255) / 256));
-  {
+  {  // K in operand order, and the largest key norm per head
+    hipLaunchKernelGGL(k_kmax_init, dim3(static_cast<unsigned>((B * Hkv + 255) / 256)), dim3(256),
+                       0, stream, p.kmax, static_cast<int>(B * Hkv));
     const int64_t nbt = B * Hkv * p.nkb;
     const dim3 kgrid(static_cast<unsigned>((nbt + 3) / 4));
     if (D == 128)
       hipLaunchKernelGGL(k_k_operand_order<128>, kgrid, dim3(256), 0, stream, p.k, a.k.sB, a.k.sH,
                          a.k.sN, static_cast<int>(Hkv), static_cast<int>(N), p.nkb, nbt,
-                         const_cast<u32x4*>(p.kop));
+                         const_cast<u32x4*>(p.kop), p.kmax);
     else
       hipLaunchKernelGGL(k_k_operand_order<64>, kgrid, dim3(256), 0, stream, p.k, a.k.sB, a.k.sH,
                          a.k.sN, static_cast<int>(Hkv), static_cast<int>(N), p.nkb, nbt,
-                         const_cast<u32x4*>(p.kop));
+                         const_cast<u32x4*>(p.kop), p.kmax);
   }
 
   if (p.mode_tiled) {
@@ -1447,11 +1440,6 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   }
   hipLaunchKernelGGL(k_qnorm, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream,
                      p.qp, rows, static_cast<int>(D), p.qnorm);
-  hipLaunchKernelGGL(k_kmax_init, dim3(static_cast<unsigned>((B * Hkv + 255) / 256)), dim3(256), 0,
-                     stream, p.kmax, static_cast<int>(B * Hkv));
-  hipLaunchKernelGGL(k_kmax, dim3(static_cast<unsigned>((N + kKmaxRows - 1) / kKmaxRows), static_cast<unsigned>(B * Hkv)),
-                     dim3(256), 0, stream, p.k, a.k.sB, a.k.sH, a.k.sN, static_cast<int>(Hkv),
-                     static_cast<int>(N), static_cast<int>(D), p.kmax);
   const int64_t nh = rows * kBins;
   hipLaunchKernelGGL(k_zero_u32, dim3(static_cast<unsigned>((nh + 255) / 256)), dim3(256), 0, stream,
                      p.hist, nh);

@@ -184,6 +184,27 @@ vecattn_status vecattn_sparse_attn(const void* q, const vecattn_tdesc* qd, const
                                    int32_t block, int32_t causal, float scale, void* o,
                                    const vecattn_tdesc* od, float* lse, void* stream);
 
+/*
+ * Per-head filter ratios, Eq. 5 (Sec. 3.1.2, "Dynamic Programming for Offline
+ * Search of Per-Head Filter Ratios").  Host function (host memory, no GPU).
+ * For each of `heads` heads, n_cand candidate filter ratios were sampled
+ * offline with their sparsity sp[h][c] in [0, 1] and a performance score
+ * perf[h][c] (any finite value, larger is better).  The call picks one
+ * candidate per head so that the mean sparsity over the heads is >= target
+ * and the summed performance is largest: Eq. 5's table over heads and
+ * sparsity, kept as the summed sparsity with each sp[h][c] rounded to a
+ * multiple of 1 / grid.  Ties go to the lower candidate index.
+ *   sparsity, perf : double [heads][n_cand], row-major
+ *   choice         : int32 [heads] output, the chosen candidate per head
+ *   best_perf      : output, the summed performance of that choice
+ * Errors: INVALID_ARG (null pointer, heads or n_cand < 1, target outside
+ * [0, 1], sparsity outside [0, 1] or non-finite perf, grid < 1 or
+ * heads * grid > 2^26); CAPACITY (no choice reaches the target).
+ */
+vecattn_status vecattn_plan_filter_ratios(int32_t heads, int32_t n_cand, const double* sparsity,
+                                          const double* perf, double target, int32_t grid,
+                                          int32_t* choice, double* best_perf);
+
 #ifdef __cplusplus
 }
 #endif

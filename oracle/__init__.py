@@ -16,6 +16,7 @@ Functions and the passages they follow:
 * :func:`sparse_attn`     -- Eq. 4 (materialised softmax over the selected keys).
 * :func:`sparse_attn_online` -- Algorithm 2's online recurrence (second route to Eq. 4).
 * :func:`dense_attn`      -- Eq. 1, textbook dense attention.
+* :func:`plan_filter_ratios` -- Eq. 5's optimum by exhaustive search (tiny tables only).
 """
 from __future__ import annotations
 
@@ -267,3 +268,27 @@ def dense_attn(q, k, v, causal, scale=0.0, nthreads=0):
     _check(_load().ora_dense_attn(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, D, int(causal),
                                   float(scale), _ptr(o), _ptr(lse), nthreads), "dense_attn")
     return o, lse
+
+
+def plan_filter_ratios(sparsity, perf, target: float):
+    """Eq. 5 (Sec. 3.1.2, per-head filter ratios) by its definition: over every
+    choice of one candidate per head, the largest summed performance among the
+    choices whose mean sparsity is at least ``target``.  Plain exhaustive search
+    (candidates ** heads choices), for tiny tables.  Returns (best, optima):
+    the optimum (None if no choice reaches the target) and every optimal
+    choice."""
+    import itertools
+    sp = np.asarray(sparsity, dtype=np.float64)
+    pf = np.asarray(perf, dtype=np.float64)
+    H, C = sp.shape
+    best, optima = None, []
+    for ch in itertools.product(range(C), repeat=H):
+        mean_sp = sum(sp[h, c] for h, c in enumerate(ch)) / H
+        if mean_sp < target - 1e-12:
+            continue
+        val = sum(pf[h, c] for h, c in enumerate(ch))
+        if best is None or val > best + 1e-12:
+            best, optima = val, [ch]
+        elif abs(val - best) <= 1e-12:
+            optima.append(ch)
+    return best, optima

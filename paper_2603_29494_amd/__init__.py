@@ -8,8 +8,9 @@ attention restricted to the gathered K/V rows of those columns (Eq. 4,
 Algorithm 2).  Both stages are HIP kernels in libvecattn.so behind the C ABI
 of include/vecattn.h; this package only marshals torch tensors to it.
 """
-from ._lib import (SEL_MINS, SEL_MINS_TILED, SEL_TOPK, SEL_TOPP, VecattnError, load, max_count,
-                   pool, select, sparse_attn, workspace_bytes)
+from ._lib import (SEL_MINS, SEL_MINS_TILED, SEL_TOPK, SEL_TOPP, VecattnError, head_sparsity,
+                   load, max_count, plan_filter_ratios, pool, select, sparse_attn, workspace_bytes)
 
-__all__ = ["SEL_TOPK", "SEL_TOPP", "SEL_MINS", "SEL_MINS_TILED", "VecattnError", "load",
-           "max_count", "pool", "select", "sparse_attn", "workspace_bytes"]
+__all__ = ["SEL_TOPK", "SEL_TOPP", "SEL_MINS", "SEL_MINS_TILED", "VecattnError", "head_sparsity",
+           "load", "max_count", "plan_filter_ratios", "pool", "select", "sparse_attn",
+           "workspace_bytes"]

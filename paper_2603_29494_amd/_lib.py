@@ -60,8 +60,10 @@ def load() -> ctypes.CDLL:
     lib.vecattn_select_mins_tiled.argtypes = [P, D, P, D, i32, i32, f64, i32, i32, P, i64, P, P,
                                               P, ctypes.c_size_t, P]
     lib.vecattn_sparse_attn.argtypes = [P, D, P, D, P, D, P, i64, P, i32, i32, f32, P, D, P, P]
+    lib.vecattn_plan_filter_ratios.argtypes = [i32, i32, P, P, f64, i32, P, ctypes.POINTER(f64)]
     for name in ("vecattn_pool", "vecattn_select_max_count", "vecattn_select_workspace_size",
-                 "vecattn_select", "vecattn_select_mins_tiled", "vecattn_sparse_attn"):
+                 "vecattn_select", "vecattn_select_mins_tiled", "vecattn_sparse_attn",
+                 "vecattn_plan_filter_ratios"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -205,3 +207,50 @@ def sparse_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: torch.Te
                                       _ptr(out), ctypes.byref(od), _ptr(lse), _stream(q)),
            "sparse_attn")
     return (out, lse) if return_lse else out
+
+
+def plan_filter_ratios(sparsity, perf, target: float, grid: int = 1000):
+    """Per-head filter ratios by Eq. 5's dynamic programme (host computation).
+
+    ``sparsity`` and ``perf`` are [heads, candidates] tables sampled offline
+    (sparsity in [0, 1], larger perf is better).  Returns (choice, best): the
+    chosen candidate per head (int32 [heads]) reaching mean sparsity >= target
+    with the largest summed perf, and that sum.  Raises VecattnError
+    (capacity) when no choice reaches the target."""
+    import numpy as np
+    sp = np.ascontiguousarray(sparsity, dtype=np.float64)
+    pf = np.ascontiguousarray(perf, dtype=np.float64)
+    if sp.ndim != 2 or sp.shape != pf.shape:
+        raise ValueError("sparsity and perf must be [heads, candidates] tables of one shape")
+    choice = np.empty(sp.shape[0], dtype=np.int32)
+    best = ctypes.c_double(0.0)
+    _check(load().vecattn_plan_filter_ratios(int(sp.shape[0]), int(sp.shape[1]),
+                                             sp.ctypes.data_as(ctypes.c_void_p),
+                                             pf.ctypes.data_as(ctypes.c_void_p), float(target),
+                                             int(grid), choice.ctypes.data_as(ctypes.c_void_p),
+                                             ctypes.byref(best)), "plan_filter_ratios")
+    return choice, float(best.value)
+
+
+def head_sparsity(q: torch.Tensor, k: torch.Tensor, block: int, mode, params, causal: bool = False,
+                  cap: Optional[int] = None, **tiling) -> "torch.Tensor":
+    """Sparsity per query head for each candidate parameter (an sp_h table for
+    plan_filter_ratios): 1 - (keys kept) / (eligible keys), summed over the
+    head's blocks and batch, from vecattn_select's counts.  Returns float64
+    [Hq, len(params)] on the host.  Extra keyword arguments (tile,
+    group_tiles) go to select."""
+    B, Hq, N, _ = q.shape
+    Np = (N + block - 1) // block
+    L = torch.tensor([min(N, (i + 1) * block) if causal else N for i in range(Np)],
+                     dtype=torch.float64, device=q.device)
+    out = torch.empty((Hq, len(params)), dtype=torch.float64)
+    ws = None
+    for c, prm in enumerate(params):
+        cp = max_count(N, block, causal, mode, prm) if cap is None else cap
+        if ws is None or ws.numel() < workspace_bytes(q, k, block, causal, mode, cp):
+            ws = torch.empty(workspace_bytes(q, k, block, causal, mode, cp), dtype=torch.uint8,
+                             device=q.device)
+        _, cnt = select(q, k, block, mode, prm, causal, cap=cp, workspace=ws, **tiling)
+        kept = cnt.double().sum(dim=(0, 2))                      # [Hq]
+        out[:, c] = (1.0 - kept / (B * L.sum())).cpu()
+    return out

@@ -52,4 +52,9 @@ size_t select_workspace_bytes(int64_t B, int64_t Hq, int64_t N, int64_t D, int32
                               int32_t mode, int64_t cap);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 
+// Host: per-head filter ratios by dynamic programming (Eq. 5).  Returns 0, or
+// 1 when no choice reaches the target.
+int plan_filter_ratios(int32_t H, int32_t C, const double* sp, const double* perf, double target,
+                       int32_t grid, int32_t* choice, double* best);
+
 }  // namespace vecattn

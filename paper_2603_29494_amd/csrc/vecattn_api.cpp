@@ -189,4 +189,21 @@ vecattn_status vecattn_sparse_attn(const void* q, const vecattn_tdesc* qd, const
   return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
 }
 
+vecattn_status vecattn_plan_filter_ratios(int32_t heads, int32_t n_cand, const double* sparsity,
+                                          const double* perf, double target, int32_t grid,
+                                          int32_t* choice, double* best_perf) {
+  if (heads < 1 || n_cand < 1 || !sparsity || !perf || !choice || !best_perf)
+    return VECATTN_ERR_INVALID_ARG;
+  if (grid < 1 || grid > (1 << 20) || !(target >= 0.0 && target <= 1.0))
+    return VECATTN_ERR_INVALID_ARG;
+  if (static_cast<int64_t>(heads) * grid > (int64_t(1) << 26)) return VECATTN_ERR_INVALID_ARG;
+  for (int64_t t = 0; t < static_cast<int64_t>(heads) * n_cand; ++t)
+    if (!(sparsity[t] >= 0.0 && sparsity[t] <= 1.0) || !std::isfinite(perf[t]))
+      return VECATTN_ERR_INVALID_ARG;
+  return vecattn::plan_filter_ratios(heads, n_cand, sparsity, perf, target, grid, choice,
+                                     best_perf) == 0
+             ? VECATTN_OK
+             : VECATTN_ERR_CAPACITY;
+}
+
 }  // extern "C"

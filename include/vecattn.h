@@ -163,6 +163,25 @@ vecattn_status vecattn_select_mins_tiled(const void* q, const vecattn_tdesc* qd,
                                          size_t workspace_bytes, void* stream);
 
 /*
+ * vecattn_select with one parameter per query head: params[h] (host memory,
+ * Hq values) replaces `param` for query head h -- e.g. the per-head filter
+ * ratios of Eq. 5 (vecattn_plan_filter_ratios).  tile and group_tiles apply
+ * to VECATTN_SEL_MINS_TILED as in vecattn_select_mins_tiled and are ignored by
+ * the other modes.  The values are read during the call; the buffer may be
+ * reused as soon as it returns.
+ * Errors: as vecattn_select, each params[h] checked against the mode's range
+ * (topK: CAPACITY when cap is below any head's budget); INVALID_ARG for
+ * params == NULL or, for cross-tile minS, a bad tiling; UNSUPPORTED for more
+ * than 128 query heads.
+ */
+vecattn_status vecattn_select_per_head(const void* q, const vecattn_tdesc* qd, const void* k,
+                                       const vecattn_tdesc* kd, int32_t block, int32_t causal,
+                                       int32_t mode, const double* params, int32_t tile,
+                                       int32_t group_tiles, int32_t* idx, int64_t cap,
+                                       int32_t* counts, int32_t* n_clamped, void* workspace,
+                                       size_t workspace_bytes, void* stream);
+
+/*
  * Vector-sparse attention, Eq. 4 (Sec. 3.2) and Algorithm 2.  For query row r
  * of block i (head h), the visible keys are V_r = { j in I[b,h,i,0:C[b,h,i]] :
  * causal == 0 or j <= r }, and

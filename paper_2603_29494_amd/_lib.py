@@ -61,9 +61,11 @@ def load() -> ctypes.CDLL:
                                               P, ctypes.c_size_t, P]
     lib.vecattn_sparse_attn.argtypes = [P, D, P, D, P, D, P, i64, P, i32, i32, f32, P, D, P, P]
     lib.vecattn_plan_filter_ratios.argtypes = [i32, i32, P, P, f64, i32, P, ctypes.POINTER(f64)]
+    lib.vecattn_select_per_head.argtypes = [P, D, P, D, i32, i32, i32, P, i32, i32, P, i64, P, P,
+                                            P, ctypes.c_size_t, P]
     for name in ("vecattn_pool", "vecattn_select_max_count", "vecattn_select_workspace_size",
                  "vecattn_select", "vecattn_select_mins_tiled", "vecattn_sparse_attn",
-                 "vecattn_plan_filter_ratios"):
+                 "vecattn_plan_filter_ratios", "vecattn_select_per_head"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -108,7 +110,15 @@ def mode_id(mode) -> int:
     return _MODES[mode] if isinstance(mode, str) else int(mode)
 
 
-def max_count(N: int, block: int, causal: bool, mode, param: float) -> int:
+def _per_head(param) -> bool:
+    import numpy as np
+    return np.ndim(param) > 0
+
+
+def max_count(N: int, block: int, causal: bool, mode, param) -> int:
+    """Largest count a block can select (a per-head parameter list: over its heads)."""
+    if _per_head(param):
+        return max(max_count(N, block, causal, mode, float(x)) for x in param)
     out = ctypes.c_int64(0)
     _check(load().vecattn_select_max_count(int(N), int(block), int(bool(causal)), mode_id(mode),
                                            float(param), ctypes.byref(out)), "select_max_count")
@@ -146,7 +156,9 @@ def select(q: torch.Tensor, k: torch.Tensor, block: int, mode, param: float,
            group_tiles: Optional[int] = None) -> Tuple[torch.Tensor, torch.Tensor]:
     """Per-block key-index lists (I, C) of Algorithm 1 for topK / topP / minS (Eq. 3)
     selection, or minS with Algorithm 1's cross-tile running maximum ("mins_tiled":
-    ``tile`` = B_K and ``group_tiles`` = G_K, both 16 when not given)."""
+    ``tile`` = B_K and ``group_tiles`` = G_K, both 16 when not given).  ``param``
+    may be one value per query head (a sequence of Hq values, e.g. from
+    plan_filter_ratios)."""
     _bf16_cuda(q, "q")
     _bf16_cuda(k, "k")
     B, Hq, N, Dd = q.shape
@@ -167,6 +179,17 @@ def select(q: torch.Tensor, k: torch.Tensor, block: int, mode, param: float,
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
     qd, kd = desc(q), desc(k)
     nws = 0 if workspace is None else workspace.numel()
+    if _per_head(param):
+        import numpy as np
+        hp = np.ascontiguousarray(np.asarray(param, dtype=np.float64).reshape(-1))
+        if hp.size != Hq:
+            raise ValueError("a per-head parameter list needs one value per query head")
+        _check(load().vecattn_select_per_head(
+            _ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd), int(block), int(bool(causal)),
+            mode_id(mode), hp.ctypes.data_as(ctypes.c_void_p), 16 if tile is None else int(tile),
+            16 if group_tiles is None else int(group_tiles), _ptr(idx), int(cap), _ptr(counts),
+            _ptr(n_clamped), _ptr(workspace), nws, _stream(q)), "select_per_head")
+        return idx, counts
     if mode_id(mode) == SEL_MINS_TILED:
         _check(load().vecattn_select_mins_tiled(
             _ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd), int(block), int(bool(causal)),

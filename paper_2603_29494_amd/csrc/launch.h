@@ -38,6 +38,7 @@ struct SelectArgs {
   int32_t causal;
   int32_t mode;
   double param;
+  const double* head_params;  // NULL, or one parameter per query head (host memory, Hq <= 128)
   int32_t tile;         // cross-tile minS: keys per tile (16 or 32)
   int32_t group_tiles;  // cross-tile minS: tiles per group (a power of two)
   int32_t* idx;

@@ -46,6 +46,7 @@ constexpr int kBins = 256;
 constexpr int kLevels = 6;      // histogram refinements per round (idle ones cost ~25 us)
 constexpr int kCand = 1024;     // candidate capacity per row
 constexpr int kRounds = 2;      // a topP row whose count exceeds cap reruns as topK(cap)
+constexpr int kMaxHeadParams = 128;  // query heads a per-head parameter list may cover
 
 enum Phase : int { PH_IDLE = 0, PH_HIST = 1, PH_COLLECT = 2, PH_DONE = 3, PH_EMIT = 4 };
 // MODE_HIST0: first histogram level (the interval is everything).
@@ -111,9 +112,11 @@ struct SelParams {
   int tiled_gs;     // keys per group of tiles (a power of two)
   int tiled_sb;     // 32-key blocks per segment a wave walks in order
   int tiled_carry;  // groups span several splits: waves start from a carried maximum
-  double tiled_a;   // alpha / tau: alpha in raw-score units
+  double sqrt_d;    // 1 / tau: alpha / tau is alpha in raw-score units
   float* qmax;      // [rows][nsplit * 4]: per quarter split, its maximum, then the carried one
   double param;
+  int per_head;     // 1: head_param[h] replaces param for query head h
+  double head_param[kMaxHeadParams];
   float tau;
   int64_t items;    // score-pass work items
   int64_t per_xcd;  // work items per XCD
@@ -125,6 +128,11 @@ __device__ __forceinline__ uint32_t ord_key(float f) {
 }
 __device__ __forceinline__ float ord_val(uint32_t k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
+
+// The selection parameter of a row (rows are ordered (b, h, i)).
+__device__ __forceinline__ double row_param(const SelParams& p, int64_t row) {
+  return p.per_head ? p.head_param[(row / p.Np) % p.Hq] : p.param;
 }
 
 __device__ __forceinline__ int eligible(int i, int P, int N, int causal) {
@@ -260,7 +268,7 @@ __global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
     s.L = eligible(i, p.P, p.N, p.causal);
     s.clamped = 0;
     s.topp = p.mode_topp;
-    if (!p.mode_topp && !p.mode_mins) s.k_target = topk_count(p.param, s.L);
+    if (!p.mode_topp && !p.mode_mins) s.k_target = topk_count(row_param(p, r), s.L);
   }
   const float c = p.qnorm[r] * p.kmax[b * p.Hkv + h / p.group];
   const float cc = c * 1.0009765625f + 1e-30f;
@@ -712,7 +720,7 @@ __global__ __launch_bounds__(256) void k_mins(SelParams p) {
   const float mx = ord_val(p.cand_lohi[2 * r + 1]);
   p.cand_lohi[2 * r + 1] = 0u;  // ready for the collect pass
   const float top = static_cast<float>(s.ref / static_cast<double>(p.tau));  // >= every |s|
-  const double t = static_cast<double>(mx) - p.param / static_cast<double>(p.tau);
+  const double t = static_cast<double>(mx) - row_param(p, r) / static_cast<double>(p.tau);
   float tf = static_cast<float>(t);
   if (static_cast<double>(tf) > t) tf = ord_val(ord_key(tf) - 1u);  // round down: keep ties
   tf = fmaxf(tf, -top);
@@ -786,6 +794,7 @@ __global__ __launch_bounds__(kThreads) void k_mins_tiled(SelParams p) {
   int Lr[2];
   bool have[2];
   float m[2], thr[2];
+  const double a_raw = row_param(p, row0) * p.sqrt_d;  // alpha of this head in raw-score units
 #pragma unroll
   for (int rb2 = 0; rb2 < 2; ++rb2) {
     const int rl = rb2 * 32 + ln;
@@ -799,7 +808,7 @@ __global__ __launch_bounds__(kThreads) void k_mins_tiled(SelParams p) {
       qf[rb2][s2] = __builtin_bit_cast(bf16x8, t);
     }
     m[rb2] = (EMIT && p.tiled_carry && have[rb2]) ? p.qmax[row * nq + sp * 4 + wave] : kNegInf;
-    thr[rb2] = tiled_threshold(m[rb2], p.tiled_a);
+    thr[rb2] = tiled_threshold(m[rb2], a_raw);
   }
 
   auto kload = [&](u32x4 (&dst)[DS], int blk) __attribute__((always_inline)) {
@@ -850,7 +859,7 @@ __global__ __launch_bounds__(kThreads) void k_mins_tiled(SelParams p) {
         tm = fmaxf(tm, __shfl_xor(tm, 32));
         const bool fresh = (static_cast<uint32_t>(kb + toff) & gmask) == 0u;  // a group starts
         const float mn = fmaxf(fresh ? kNegInf : m[rb2], tm);
-        if (__any(mn != m[rb2])) thr[rb2] = tiled_threshold(mn, p.tiled_a);
+        if (__any(mn != m[rb2])) thr[rb2] = tiled_threshold(mn, a_raw);
         m[rb2] = mn;
 #pragma unroll
         for (int e = e0; e < e0 + ne; ++e) {
@@ -951,7 +960,7 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
   (void)bh;
   if (level == 0 && s.topp) {
     s.Z = z;
-    s.pZ = p.param * z;
+    s.pZ = row_param(p, r) * z;
   }
   const float lo = s.blo, inv = s.binv, add = s.badd;
   const float top = static_cast<float>(s.ref / static_cast<double>(p.tau));  // raw score bound
@@ -1376,6 +1385,9 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.kop = reinterpret_cast<const u32x4*>(ws + l.kop);
   p.nkb = static_cast<int>((N + 31) / 32);
   p.param = a.param;
+  p.per_head = a.head_params != nullptr;
+  if (p.per_head)
+    for (int64_t h = 0; h < Hq; ++h) p.head_param[h] = a.head_params[h];
   p.tau = 1.0f / sqrtf(static_cast<float>(D));
 
   // Pooled queries (Eq. 2) into the workspace, contiguous [rows][D].
@@ -1417,7 +1429,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
     p.nsplit = static_cast<int>((N + st - 1) / st);
     p.tiled_tile = a.tile;
     p.tiled_gs = static_cast<int>(gs);
-    p.tiled_a = a.param * sqrt(static_cast<double>(D));  // alpha / tau
+    p.sqrt_d = sqrt(static_cast<double>(D));
     p.items = B * Hq * static_cast<int64_t>(p.nsplit) * p.nrb;
     p.per_xcd = (p.items + 7) / 8;
     const dim3 tgrid(static_cast<unsigned>(p.per_xcd * 8));

@@ -68,11 +68,14 @@ int64_t max_count(int64_t N, int32_t P, int32_t causal, int32_t mode, double par
   return mode == VECATTN_SEL_TOPK ? topk_count(param, Lmax) : Lmax;
 }
 
+constexpr int64_t kMaxHeadParams = 128;  // query heads a per-head parameter list may cover
+
 vecattn_status select_impl(const void* q, const vecattn_tdesc* qd, const void* k,
                            const vecattn_tdesc* kd, int32_t block, int32_t causal, int32_t mode,
-                           double param, int32_t tile, int32_t group_tiles, int32_t* idx,
-                           int64_t cap, int32_t* counts, int32_t* n_clamped, void* workspace,
-                           size_t workspace_bytes, void* stream) {
+                           double param, const double* head_params, int32_t tile,
+                           int32_t group_tiles, int32_t* idx, int64_t cap, int32_t* counts,
+                           int32_t* n_clamped, void* workspace, size_t workspace_bytes,
+                           void* stream) {
   vecattn_status st = check_desc(q, qd);
   if (st != VECATTN_OK) return st;
   st = check_desc(k, kd);
@@ -80,16 +83,28 @@ vecattn_status select_impl(const void* q, const vecattn_tdesc* qd, const void* k
   if (kd->B != qd->B || kd->N != qd->N || kd->D != qd->D || qd->H % kd->H != 0)
     return VECATTN_ERR_INVALID_ARG;
   if (!idx || !counts || block < 1 || cap < 1 || cap > kMaxN) return VECATTN_ERR_INVALID_ARG;
-  if (!mode_ok(mode) || !param_ok(mode, param)) return VECATTN_ERR_INVALID_ARG;
+  if (!mode_ok(mode)) return VECATTN_ERR_INVALID_ARG;
+  if (head_params) {
+    if (qd->H > kMaxHeadParams) return VECATTN_ERR_UNSUPPORTED;
+    for (int64_t h = 0; h < qd->H; ++h) {
+      if (!param_ok(mode, head_params[h])) return VECATTN_ERR_INVALID_ARG;
+      if (mode == VECATTN_SEL_TOPK && cap < max_count(qd->N, block, causal, mode, head_params[h]))
+        return VECATTN_ERR_CAPACITY;
+    }
+    param = head_params[0];
+  } else if (!param_ok(mode, param)) {
+    return VECATTN_ERR_INVALID_ARG;
+  }
   if (mode == VECATTN_SEL_MINS_TILED && !tiling_ok(tile, group_tiles))
     return VECATTN_ERR_INVALID_ARG;
-  if (mode == VECATTN_SEL_TOPK && cap < max_count(qd->N, block, causal, mode, param))
+  if (!head_params && mode == VECATTN_SEL_TOPK &&
+      cap < max_count(qd->N, block, causal, mode, param))
     return VECATTN_ERR_CAPACITY;
   const size_t need = vecattn::select_workspace_bytes(qd->B, qd->H, qd->N, qd->D, block, mode, cap);
   if (need > 0 && (!workspace || workspace_bytes < need)) return VECATTN_ERR_CAPACITY;
   if (workspace && !aligned16(workspace)) return VECATTN_ERR_INVALID_ARG;
   vecattn::SelectArgs a{to_tensor(q, qd), to_tensor(k, kd), block, causal ? 1 : 0, mode, param,
-                        tile, group_tiles, idx, cap, counts, n_clamped, workspace,
+                        head_params, tile, group_tiles, idx, cap, counts, n_clamped, workspace,
                         workspace_bytes};
   hipError_t e = vecattn::launch_select(a, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
@@ -150,8 +165,19 @@ vecattn_status vecattn_select(const void* q, const vecattn_tdesc* qd, const void
                               int32_t* n_clamped, void* workspace, size_t workspace_bytes,
                               void* stream) {
   // Cross-tile minS through this entry point uses the paper's B_K = G_K = 16.
-  return select_impl(q, qd, k, kd, block, causal, mode, param, 16, 16, idx, cap, counts,
+  return select_impl(q, qd, k, kd, block, causal, mode, param, nullptr, 16, 16, idx, cap, counts,
                      n_clamped, workspace, workspace_bytes, stream);
+}
+
+vecattn_status vecattn_select_per_head(const void* q, const vecattn_tdesc* qd, const void* k,
+                                       const vecattn_tdesc* kd, int32_t block, int32_t causal,
+                                       int32_t mode, const double* params, int32_t tile,
+                                       int32_t group_tiles, int32_t* idx, int64_t cap,
+                                       int32_t* counts, int32_t* n_clamped, void* workspace,
+                                       size_t workspace_bytes, void* stream) {
+  if (!params) return VECATTN_ERR_INVALID_ARG;
+  return select_impl(q, qd, k, kd, block, causal, mode, 0.0, params, tile, group_tiles, idx, cap,
+                     counts, n_clamped, workspace, workspace_bytes, stream);
 }
 
 vecattn_status vecattn_select_mins_tiled(const void* q, const vecattn_tdesc* qd, const void* k,
@@ -160,7 +186,7 @@ vecattn_status vecattn_select_mins_tiled(const void* q, const vecattn_tdesc* qd,
                                          int32_t* idx, int64_t cap, int32_t* counts,
                                          int32_t* n_clamped, void* workspace,
                                          size_t workspace_bytes, void* stream) {
-  return select_impl(q, qd, k, kd, block, causal, VECATTN_SEL_MINS_TILED, alpha, tile,
+  return select_impl(q, qd, k, kd, block, causal, VECATTN_SEL_MINS_TILED, alpha, nullptr, tile,
                      group_tiles, idx, cap, counts, n_clamped, workspace, workspace_bytes, stream);
 }
 

@@ -149,6 +149,29 @@ def test_select_mins_tiled_rejects_bad_arguments():
     assert va.max_count(1000, 64, True, "mins_tiled", 0.5) == 1000
 
 
+def select_per_head(params, q=FAKE, qd=None, k=FAKE, kd=None, mode=0, cap=256, H=4):
+    lib = _lib.load()
+    qd = qd or desc(1, H, 256, 128)
+    kd = kd or desc(1, 2, 256, 128)
+    arr = None if params is None else (ctypes.c_double * len(params))(*params)
+    return lib.vecattn_select_per_head(q, ctypes.byref(qd), k, ctypes.byref(kd), 64, 0, mode,
+                                       arr, 16, 16, FAKE, cap, FAKE, None, None, 1 << 40, None)
+
+
+def test_select_per_head_rejects_bad_arguments():
+    assert select_per_head(None) == INVALID
+    assert select_per_head([0.5, 0.5, 1.5, 0.5]) == INVALID            # topK ratio > 1
+    assert select_per_head([0.5, 0.5, 0.5, 0.0]) == INVALID
+    assert select_per_head([0.1, 0.2, 0.5, 0.3], cap=100) == CAPACITY  # head 2 keeps 128
+    assert select_per_head([1.0, -1.0, 1.0, 1.0], mode=2) == INVALID   # minS alpha < 0
+    assert select_per_head([0.5] * 4, mode=9) == INVALID
+    assert select_per_head([0.5] * 130, qd=desc(1, 130, 256, 128), kd=desc(1, 130, 256, 128),
+                           H=130) == UNSUPPORTED
+    assert select_per_head([0.5] * 4, q=None) == INVALID
+    # otherwise valid: the missing workspace is reported before any launch
+    assert select_per_head([0.1, 0.2, 0.5, 0.3], cap=128) == CAPACITY
+
+
 def test_workspace_size_query():
     qd, kd = desc(1, 40, 75600, 128), desc(1, 40, 75600, 128)
     n = ctypes.c_size_t(0)

@@ -123,3 +123,8 @@ def test_head_sparsity_table_and_plan_on_gpu(gpu):
     assert sp_ora[np.arange(6), choice].mean() >= target - 1e-3
     uni = [perf[:, c].sum() for c in range(len(alphas)) if sp_ora[:, c].mean() >= target]
     assert val >= max(uni) - 1e-9
+    # the plan applied in one selection call (one alpha per head)
+    per_head = [alphas[c] for c in choice]
+    _, cnt = va.select(dev(q), dev(k), 64, "mins", per_head, False, cap=N)
+    got = 1.0 - cnt[0].double().sum(dim=1).cpu().numpy() / (Np * N)
+    assert np.abs(got - sp_ora[np.arange(6), choice]).max() <= 2e-3

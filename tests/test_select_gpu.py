@@ -229,3 +229,36 @@ def test_mins_tiled_default_tiling_and_clamp(gpu):
     assert np.array_equal(c_cnt, np.minimum(a_cnt, cap))
     assert np.array_equal(c_idx, a_idx[..., :cap])
     check_rows_tiled(q, k, 64, 1.0, False, 16, 16, a_idx, a_cnt, all_rows(q, 64))
+
+
+PER_HEAD = [
+    ("topk", oracle.TOPK, [0.05, 0.1, 0.2, 0.4]),
+    ("topp", oracle.TOPP, [0.5, 0.8, 0.9, 0.99]),
+    ("mins", oracle.MINS, [0.0, 0.5, 1.0, 2.0]),
+    ("mins_tiled", oracle.MINS_TILED, [0.1, 0.3, 0.6, 1.0]),
+]
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("name,omode,params", PER_HEAD)
+def test_per_head_parameters(gpu, name, omode, params, causal):
+    # One call with a parameter per query head equals, head by head, the
+    # oracle's selection of that head with its own parameter.
+    B, Hq, Hkv, N, D, block = 1, 4, 2, 700, 128, 64
+    q, k, _ = synth.planted_case(300 + len(name) + int(causal), B, Hq, Hkv, N, D)
+    cap = va.max_count(N, block, causal, name, params)
+    ncl = torch.zeros(1, dtype=torch.int32, device="cuda")
+    idx, cnt = va.select(dev(q), dev(k), block, name, params, causal, cap=cap, n_clamped=ncl)
+    torch.cuda.synchronize()
+    assert int(ncl.item()) == 0
+    idx, cnt = idx.cpu().numpy(), cnt.cpu().numpy()
+    for h in range(Hq):
+        qh = np.ascontiguousarray(q[:, h:h + 1])
+        kh = np.ascontiguousarray(k[:, h // (Hq // Hkv):h // (Hq // Hkv) + 1])
+        ih, ch = np.ascontiguousarray(idx[:, h:h + 1]), np.ascontiguousarray(cnt[:, h:h + 1])
+        rows = all_rows(qh, block)
+        if omode == oracle.MINS_TILED:
+            mism = check_rows_tiled(qh, kh, block, params[h], causal, 16, 16, ih, ch, rows)
+        else:
+            mism = check_rows(qh, kh, block, omode, params[h], causal, cap, ih, ch, rows)
+        assert mism <= max(1, len(rows) // 20), (name, h)

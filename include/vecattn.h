@@ -66,6 +66,14 @@ typedef enum vecattn_sel_mode {
                            group; see vecattn_select_mins_tiled */
 } vecattn_sel_mode;
 
+/* Bits of the `causal` argument of the selection entry points.  0 (none) and
+ * 1 (VECATTN_CAUSAL) keep their plain meaning; other bits are invalid. */
+#define VECATTN_CAUSAL 1    /* block i's eligible keys end at its last row */
+#define VECATTN_KEEP_DIAG 2 /* block i also keeps the keys of its own rows,
+                               [i*P, min(N, (i+1)*P)); cap must then cover
+                               vecattn_select_max_count for the same flags in
+                               every mode (no block is clamped) */
+
 typedef struct vecattn_tdesc {
   int64_t B, H, N, D; /* logical sizes */
   int64_t sB, sH, sN; /* element strides of the B, H and N dimensions */
@@ -89,9 +97,10 @@ vecattn_status vecattn_pool(const void* q, const vecattn_tdesc* qd, int32_t bloc
                             const vecattn_tdesc* qpd, void* stream);
 
 /*
- * Largest number of keys any block can select, for sizing cap.  topK: max_i k_i;
+ * Largest number of keys any block can select, for sizing cap.  topK: max_i k_i
+ * (with VECATTN_KEEP_DIAG: max_i min(L_i, k_i + n_i), n_i the rows of block i);
  * the other modes: max_i L_i, where L_i = N (non-causal) or min(N, (i+1)*P)
- * (causal).
+ * (causal).  `causal` takes the same bits as vecattn_select.
  * Errors: INVALID_ARG for N < 1, block < 1, out == NULL, or param outside the
  * mode's range.
  */
@@ -109,8 +118,11 @@ vecattn_status vecattn_select_workspace_size(const vecattn_tdesc* qd, const veca
 /*
  * Important-vector selection (Sec. 3.1; Algorithm 1's outputs I and C).
  *   q : bf16 [B, Hq, N, D]    k : bf16 [B, Hkv, N, D]
- *   Block i's eligible keys are j in [0, N) (causal = 0) or j in
- *   [0, min(N, (i+1)*P)) (causal != 0).  Scores are <Q_p[i], k_j> / sqrt(D)
+ *   causal : VECATTN_CAUSAL and/or VECATTN_KEEP_DIAG bits.  Block i's
+ *   eligible keys are j in [0, N), or j in [0, min(N, (i+1)*P)) with
+ *   VECATTN_CAUSAL.  With VECATTN_KEEP_DIAG the block's list is the union of
+ *   the mode's selection and the keys of its own rows (a practical variant
+ *   the paper leaves open: local keys always attended).  Scores are <Q_p[i], k_j> / sqrt(D)
  *   with Q_p from vecattn_pool, computed from bf16 products accumulated in
  *   fp32.  Ties in score are broken toward the lower key index.
  *   idx    : int32 [B, Hq, N_p, cap] output (ascending lists, -1 padded)
@@ -192,6 +204,8 @@ vecattn_status vecattn_select_per_head(const void* q, const vecattn_tdesc* qd, c
  *   idx, counts : as produced by vecattn_select (any source is accepted if
  *   every listed key is in [0, N) and the lists are strictly ascending;
  *   other contents are undefined behaviour).
+ *   causal : the VECATTN_CAUSAL bit (VECATTN_KEEP_DIAG is accepted and has no
+ *   effect here; other bits are invalid).
  *   scale : softmax scale; 0 means 1 / sqrt(D).
  *   lse   : optional fp32 [B, Hq, N] contiguous output, may be NULL.
  * Errors: INVALID_ARG (null pointer, shape mismatch, block < 1, cap < 1,

@@ -140,14 +140,39 @@ def pooled_scores(q: np.ndarray, k: np.ndarray, block: int, causal: bool, b: int
     return out[:L.value].copy()
 
 
+def with_diagonal(idx: np.ndarray, counts: np.ndarray, N: int, block: int, cap: int,
+                  rows: Optional[Sequence[int]] = None, compact: bool = False):
+    """The keep-the-diagonal variant: each block's list united with the keys of
+    its own rows [i P, min(N, (i+1) P)), ascending, -1 padded to cap."""
+    Np = num_blocks(N, block)
+    flat = idx.reshape(-1, idx.shape[-1])
+    cnt = counts.reshape(-1)
+    out = np.full((flat.shape[0], cap), -1, dtype=np.int32)
+    ocnt = np.zeros(flat.shape[0], dtype=np.int32)
+    # t: output row; w: its flat block id (compact outputs hold the listed rows in order)
+    todo = range(flat.shape[0]) if rows is None else (range(len(rows)) if compact else list(rows))
+    for t in todo:
+        w = int(rows[t]) if compact else int(t)
+        i = w % Np
+        keys = sorted(set(flat[t, :cnt[t]].tolist()) | set(range(i * block, min(N, (i + 1) * block))))
+        if len(keys) > cap:
+            raise ValueError("capacity too small for the kept diagonal")
+        out[t, :len(keys)] = keys
+        ocnt[t] = len(keys)
+    return out.reshape(idx.shape[:-1] + (cap,)), ocnt.reshape(counts.shape)
+
+
 def select(q: np.ndarray, k: np.ndarray, block: int, mode: int, param: float, causal: bool,
            cap: int, rows: Optional[Sequence[int]] = None,
-           nthreads: int = 0, compact: bool = False) -> Tuple[np.ndarray, np.ndarray, int]:
+           nthreads: int = 0, compact: bool = False,
+           keep_diag: bool = False) -> Tuple[np.ndarray, np.ndarray, int]:
     """Selected key lists (ascending, -1 padded), counts and number of clamped rows.
 
     ``rows`` lists flat block ids w = (b * Hq + h) * Np + i to compute; other rows
     of the outputs are left as -1 / 0.  ``compact`` (with ``rows``): outputs of
     shape [len(rows), cap] and [len(rows)], in the order of ``rows``.
+    ``keep_diag``: each list united with the keys of its block's own rows
+    (:func:`with_diagonal`; no clamping then: cap must cover every union).
     """
     q, k = _bits(q), _bits(k)
     B, Hq, N, D = q.shape
@@ -170,6 +195,10 @@ def select(q: np.ndarray, k: np.ndarray, block: int, mode: int, param: float, ca
     if rc == 3:
         raise ValueError("capacity too small for topK")
     _check(rc, "select")
+    if keep_diag:
+        if ncl.value:
+            raise ValueError("capacity too small: a block was clamped")
+        idx, counts = with_diagonal(idx, counts, N, block, cap, rows, compact)
     return idx, counts, int(ncl.value)
 
 

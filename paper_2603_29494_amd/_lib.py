@@ -17,6 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libvecattn.so")
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_CAPACITY, ERR_DEVICE = range(5)
+CAUSAL, KEEP_DIAG = 1, 2  # bits of the selection entry points' `causal` argument
 SEL_TOPK, SEL_TOPP, SEL_MINS, SEL_MINS_TILED = 0, 1, 2, 3
 _MODES = {"topk": SEL_TOPK, "topp": SEL_TOPP, "mins": SEL_MINS, "mins_tiled": SEL_MINS_TILED}
 
@@ -115,12 +116,17 @@ def _per_head(param) -> bool:
     return np.ndim(param) > 0
 
 
-def max_count(N: int, block: int, causal: bool, mode, param) -> int:
+def _flags(causal: bool, keep_diag: bool) -> int:
+    return (CAUSAL if causal else 0) | (KEEP_DIAG if keep_diag else 0)
+
+
+def max_count(N: int, block: int, causal: bool, mode, param, keep_diag: bool = False) -> int:
     """Largest count a block can select (a per-head parameter list: over its heads)."""
     if _per_head(param):
-        return max(max_count(N, block, causal, mode, float(x)) for x in param)
+        return max(max_count(N, block, causal, mode, float(x), keep_diag) for x in param)
     out = ctypes.c_int64(0)
-    _check(load().vecattn_select_max_count(int(N), int(block), int(bool(causal)), mode_id(mode),
+    _check(load().vecattn_select_max_count(int(N), int(block), _flags(causal, keep_diag),
+                                           mode_id(mode),
                                            float(param), ctypes.byref(out)), "select_max_count")
     return int(out.value)
 
@@ -153,18 +159,21 @@ def select(q: torch.Tensor, k: torch.Tensor, block: int, mode, param: float,
            idx: Optional[torch.Tensor] = None, counts: Optional[torch.Tensor] = None,
            workspace: Optional[torch.Tensor] = None,
            n_clamped: Optional[torch.Tensor] = None, tile: Optional[int] = None,
-           group_tiles: Optional[int] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+           group_tiles: Optional[int] = None,
+           keep_diag: bool = False) -> Tuple[torch.Tensor, torch.Tensor]:
     """Per-block key-index lists (I, C) of Algorithm 1 for topK / topP / minS (Eq. 3)
     selection, or minS with Algorithm 1's cross-tile running maximum ("mins_tiled":
     ``tile`` = B_K and ``group_tiles`` = G_K, both 16 when not given).  ``param``
     may be one value per query head (a sequence of Hq values, e.g. from
-    plan_filter_ratios)."""
+    plan_filter_ratios).  ``keep_diag``: every block also keeps the keys of its own
+    rows (cap must then cover max_count(..., keep_diag=True))."""
     _bf16_cuda(q, "q")
     _bf16_cuda(k, "k")
     B, Hq, N, Dd = q.shape
     Np = (N + block - 1) // block
     if cap is None:
-        cap = max_count(N, block, causal, mode, param)
+        cap = max_count(N, block, causal, mode, param, keep_diag)
+    flags = _flags(causal, keep_diag)
     dev = q.device
     if idx is None:
         idx = torch.empty((B, Hq, Np, cap), dtype=torch.int32, device=dev)
@@ -185,14 +194,14 @@ def select(q: torch.Tensor, k: torch.Tensor, block: int, mode, param: float,
         if hp.size != Hq:
             raise ValueError("a per-head parameter list needs one value per query head")
         _check(load().vecattn_select_per_head(
-            _ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd), int(block), int(bool(causal)),
+            _ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd), int(block), flags,
             mode_id(mode), hp.ctypes.data_as(ctypes.c_void_p), 16 if tile is None else int(tile),
             16 if group_tiles is None else int(group_tiles), _ptr(idx), int(cap), _ptr(counts),
             _ptr(n_clamped), _ptr(workspace), nws, _stream(q)), "select_per_head")
         return idx, counts
     if mode_id(mode) == SEL_MINS_TILED:
         _check(load().vecattn_select_mins_tiled(
-            _ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd), int(block), int(bool(causal)),
+            _ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd), int(block), flags,
             float(param), 16 if tile is None else int(tile),
             16 if group_tiles is None else int(group_tiles), _ptr(idx), int(cap), _ptr(counts),
             _ptr(n_clamped), _ptr(workspace), nws, _stream(q)), "select_mins_tiled")
@@ -200,7 +209,7 @@ def select(q: torch.Tensor, k: torch.Tensor, block: int, mode, param: float,
     if tile is not None or group_tiles is not None:
         raise ValueError("tile / group_tiles apply to mode 'mins_tiled' only")
     _check(load().vecattn_select(_ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd), int(block),
-                                 int(bool(causal)), mode_id(mode), float(param), _ptr(idx),
+                                 flags, mode_id(mode), float(param), _ptr(idx),
                                  int(cap), _ptr(counts), _ptr(n_clamped), _ptr(workspace), nws,
                                  _stream(q)),
            "select")

@@ -108,6 +108,7 @@ struct SelParams {
   int mode_mins;
   int mins_direct;  // minS with cap >= every block's eligible keys: no count needed
   int mode_tiled;   // cross-tile minS (Algorithm 1)
+  int keep_diag;    // every block also keeps the keys of its own rows
   int tiled_tile;   // keys per tile: 16 or 32
   int tiled_gs;     // keys per group of tiles (a power of two)
   int tiled_sb;     // 32-key blocks per segment a wave walks in order
@@ -1233,6 +1234,11 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
         }
         ties_seen += __shfl(incl, 63);
       }
+      if (p.keep_diag) {  // the keys of the block's own rows, [i P, min(N, (i + 1) P))
+        const int i = static_cast<int>(r % p.Np);
+        const int lo = max(i * p.P - 32 * wd, 0), hi = min(min(p.N, (i + 1) * p.P) - 32 * wd, 32);
+        if (lo < hi) m |= (hi == 32 ? 0xFFFFFFFFu : (1u << hi) - 1u) & ~((1u << lo) - 1u);
+      }
       if (wd < nw && L - 32 * wd < 32) m &= (1u << (L - 32 * wd)) - 1u;
       const int nb = __builtin_popcount(m);
       int pre = nb;
@@ -1373,6 +1379,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.Np = static_cast<int>(Np);
   p.D = static_cast<int>(D);
   p.causal = a.causal;
+  p.keep_diag = a.keep_diag;
   p.split = split;
   p.nsplit = static_cast<int>((N + split - 1) / split);
   p.W = static_cast<int>((N + 31) / 32);

@@ -60,12 +60,25 @@ bool tiling_ok(int32_t tile, int32_t group_tiles) {
   return static_cast<int64_t>(tile) * group_tiles <= (int64_t(1) << 30);
 }
 
-// Largest count any block can produce (k_i is non-decreasing in L_i, so the
-// largest L_i decides).
-int64_t max_count(int64_t N, int32_t P, int32_t causal, int32_t mode, double param) {
+// Bits of the `causal` argument of the selection entry points.
+constexpr int32_t kCausal = VECATTN_CAUSAL, kKeepDiag = VECATTN_KEEP_DIAG;
+
+// Largest count any block can produce.  Without the diagonal, k_i is
+// non-decreasing in L_i, so the largest L_i decides; with it (block i adds
+// its own n_i rows' keys), min(L_i, k_i + n_i) is taken over the blocks.
+int64_t max_count(int64_t N, int32_t P, int32_t flags, int32_t mode, double param) {
+  const bool causal = (flags & kCausal) != 0;
   const int64_t Np = num_blocks(N, P);
   const int64_t Lmax = causal ? std::min<int64_t>(N, Np * static_cast<int64_t>(P)) : N;
-  return mode == VECATTN_SEL_TOPK ? topk_count(param, Lmax) : Lmax;
+  if (mode != VECATTN_SEL_TOPK) return Lmax;
+  if (!(flags & kKeepDiag)) return topk_count(param, Lmax);
+  int64_t best = 0;
+  for (int64_t i = 0; i < Np; ++i) {
+    const int64_t n_i = std::min<int64_t>(N, (i + 1) * P) - i * P;
+    const int64_t L = causal ? std::min<int64_t>(N, (i + 1) * P) : N;
+    best = std::max(best, std::min(L, topk_count(param, L) + n_i));
+  }
+  return best;
 }
 
 constexpr int64_t kMaxHeadParams = 128;  // query heads a per-head parameter list may cover
@@ -83,7 +96,7 @@ vecattn_status select_impl(const void* q, const vecattn_tdesc* qd, const void* k
   if (kd->B != qd->B || kd->N != qd->N || kd->D != qd->D || qd->H % kd->H != 0)
     return VECATTN_ERR_INVALID_ARG;
   if (!idx || !counts || block < 1 || cap < 1 || cap > kMaxN) return VECATTN_ERR_INVALID_ARG;
-  if (!mode_ok(mode)) return VECATTN_ERR_INVALID_ARG;
+  if (!mode_ok(mode) || (causal & ~(kCausal | kKeepDiag)) != 0) return VECATTN_ERR_INVALID_ARG;
   if (head_params) {
     if (qd->H > kMaxHeadParams) return VECATTN_ERR_UNSUPPORTED;
     for (int64_t h = 0; h < qd->H; ++h) {
@@ -100,12 +113,16 @@ vecattn_status select_impl(const void* q, const vecattn_tdesc* qd, const void* k
   if (!head_params && mode == VECATTN_SEL_TOPK &&
       cap < max_count(qd->N, block, causal, mode, param))
     return VECATTN_ERR_CAPACITY;
+  // With the diagonal kept, no block may be clamped: cap covers every count.
+  if ((causal & kKeepDiag) && mode != VECATTN_SEL_TOPK &&
+      cap < max_count(qd->N, block, causal, mode, param))
+    return VECATTN_ERR_CAPACITY;
   const size_t need = vecattn::select_workspace_bytes(qd->B, qd->H, qd->N, qd->D, block, mode, cap);
   if (need > 0 && (!workspace || workspace_bytes < need)) return VECATTN_ERR_CAPACITY;
   if (workspace && !aligned16(workspace)) return VECATTN_ERR_INVALID_ARG;
-  vecattn::SelectArgs a{to_tensor(q, qd), to_tensor(k, kd), block, causal ? 1 : 0, mode, param,
-                        head_params, tile, group_tiles, idx, cap, counts, n_clamped, workspace,
-                        workspace_bytes};
+  vecattn::SelectArgs a{to_tensor(q, qd), to_tensor(k, kd), block, (causal & kCausal) ? 1 : 0,
+                        (causal & kKeepDiag) ? 1 : 0, mode, param, head_params, tile, group_tiles,
+                        idx, cap, counts, n_clamped, workspace, workspace_bytes};
   hipError_t e = vecattn::launch_select(a, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
 }
@@ -143,7 +160,8 @@ vecattn_status vecattn_pool(const void* q, const vecattn_tdesc* qd, int32_t bloc
 
 vecattn_status vecattn_select_max_count(int64_t N, int32_t block, int32_t causal, int32_t mode,
                                         double param, int64_t* out) {
-  if (!out || N < 1 || N > kMaxN || block < 1 || !mode_ok(mode) || !param_ok(mode, param))
+  if (!out || N < 1 || N > kMaxN || block < 1 || !mode_ok(mode) || !param_ok(mode, param) ||
+      (causal & ~(kCausal | kKeepDiag)) != 0)
     return VECATTN_ERR_INVALID_ARG;
   *out = max_count(N, block, causal, mode, param);
   return VECATTN_OK;
@@ -208,9 +226,10 @@ vecattn_status vecattn_sparse_attn(const void* q, const vecattn_tdesc* qd, const
     return VECATTN_ERR_INVALID_ARG;
   if (!idx || !counts || block < 1 || cap < 1 || cap > kMaxN) return VECATTN_ERR_INVALID_ARG;
   if (!std::isfinite(scale) || scale < 0.0f) return VECATTN_ERR_INVALID_ARG;
+  if ((causal & ~(kCausal | kKeepDiag)) != 0) return VECATTN_ERR_INVALID_ARG;
   vecattn::SparseAttnArgs a{to_tensor(q, qd), to_tensor(k, kd), to_tensor(v, vd),
                             o, od->sB, od->sH, od->sN, lse, idx, counts, cap, block,
-                            causal ? 1 : 0, scale};
+                            (causal & kCausal) ? 1 : 0, scale};
   hipError_t e = vecattn::launch_sparse_attn(a, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
 }

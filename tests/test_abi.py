@@ -172,6 +172,19 @@ def test_select_per_head_rejects_bad_arguments():
     assert select_per_head([0.1, 0.2, 0.5, 0.3], cap=128) == CAPACITY
 
 
+def test_keep_diag_flag():
+    # topK with the diagonal: block i keeps k_i + its own rows (at most L_i)
+    assert va.max_count(1024, 64, False, "topk", 0.125, keep_diag=True) == 192
+    assert va.max_count(1024, 64, True, "topk", 0.125, keep_diag=True) == 192
+    assert va.max_count(100, 64, True, "topk", 0.5, keep_diag=True) == 86   # 50 + 36 rows
+    assert va.max_count(1000, 64, True, "topp", 0.5, keep_diag=True) == 1000
+    assert select(mode=0, param=0.25, cap=64, causal=4) == INVALID        # unknown bit
+    assert select(mode=0, param=0.25, cap=127, causal=2) == CAPACITY       # 64 + 64 needed
+    assert select(mode=1, param=0.5, cap=255, causal=2) == CAPACITY        # no clamping
+    assert select(mode=1, param=0.5, cap=256, causal=3, ws=None) == CAPACITY   # valid flags
+    assert attn(causal=4) == INVALID
+
+
 def test_workspace_size_query():
     qd, kd = desc(1, 40, 75600, 128), desc(1, 40, 75600, 128)
     n = ctypes.c_size_t(0)

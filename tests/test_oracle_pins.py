@@ -448,3 +448,20 @@ def test_compact_row_layout_matches_full_layout():
             assert np.array_equal(o1[0, h, i * 64:i * 64 + n], o2[t, :n])
             assert np.array_equal(l1[0, h, i * 64:i * 64 + n], l2[t, :n])
             assert np.isnan(o2[t, n:]).all()
+
+
+def test_keep_diagonal_variant():
+    # topK k = 1 with the block's own rows kept: the argmax plus the diagonal range
+    q, k = _tiny_layer(81, 200, D=32)
+    idx, cnt, _ = oracle.select(q, k, 64, oracle.TOPK, 1e-6, True, 200, keep_diag=True)
+    for i in range(4):
+        s = oracle.pooled_scores(q, k, 64, True, 0, 0, i)
+        diag = set(range(64 * i, min(200, 64 * (i + 1))))
+        want = sorted(diag | {int(np.argmax(s))})
+        assert list(idx[0, 0, i, :cnt[0, 0, i]]) == want
+    # keeping everything already keeps the diagonal
+    a, ca, _ = oracle.select(q, k, 64, oracle.TOPK, 1.0, True, 200, keep_diag=True)
+    b, cb, _ = oracle.select(q, k, 64, oracle.TOPK, 1.0, True, 200)
+    assert np.array_equal(a, b) and np.array_equal(ca, cb)
+    with pytest.raises(ValueError):   # lists must fit: 64 + k keys in 65 slots fails for k > 1
+        oracle.select(q, k, 64, oracle.TOPK, 0.1, False, 65, keep_diag=True)

@@ -262,3 +262,22 @@ def test_per_head_parameters(gpu, name, omode, params, causal):
         else:
             mism = check_rows(qh, kh, block, omode, params[h], causal, cap, ih, ch, rows)
         assert mism <= max(1, len(rows) // 20), (name, h)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("name,param", [("topk", 0.1), ("topp", 0.8), ("mins", 0.5),
+                                        ("mins_tiled", 0.3)])
+def test_keep_diagonal(gpu, name, param, causal):
+    # With the diagonal kept, every list is the plain selection united with
+    # the keys of the block's own rows (bit-exact: the selection is
+    # deterministic), and the counts follow.
+    B, Hq, Hkv, N, D, block = 1, 2, 2, 777, 128, 64
+    q, k, _ = synth.planted_case(400 + len(name) + int(causal), B, Hq, Hkv, N, D)
+    cap = va.max_count(N, block, causal, name, param, keep_diag=True)
+    a_idx, a_cnt = va.select(dev(q), dev(k), block, name, param, causal, cap=cap, keep_diag=True)
+    b_idx, b_cnt = va.select(dev(q), dev(k), block, name, param, causal, cap=cap)
+    torch.cuda.synchronize()
+    want_idx, want_cnt = oracle.with_diagonal(b_idx.cpu().numpy(), b_cnt.cpu().numpy(), N, block,
+                                              cap)
+    assert np.array_equal(a_cnt.cpu().numpy(), want_cnt)
+    assert np.array_equal(a_idx.cpu().numpy(), want_idx)

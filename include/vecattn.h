@@ -218,6 +218,36 @@ vecattn_status vecattn_sparse_attn(const void* q, const vecattn_tdesc* qd, const
                                    const vecattn_tdesc* od, float* lse, void* stream);
 
 /*
+ * Variable-length batches.  Sequences of different lengths packed along N of
+ * B = 1 tensors: sequence s is rows [cu_seqlens[s], cu_seqlens[s+1]) (host
+ * int64, nseq + 1 values, cu_seqlens[0] = 0, non-decreasing, last = N; empty
+ * sequences are allowed).  Each sequence is handled exactly as a separate
+ * B = 1 call on its rows (its key indices count from its first row); the
+ * calls run one after another on `stream`.  Output layouts are the
+ * per-sequence arrays laid end to end:
+ *   idx    : int32, for each sequence [Hq, N_p(s), cap], N_p(s) = ceil(n_s / P)
+ *   counts : int32, for each sequence [Hq, N_p(s)]
+ *   lse    : fp32,  for each sequence [Hq, n_s] (optional)
+ * Q, K, V, O rows are read and written in place (the [1, H, N, D] views).
+ * The selection workspace must be sized (vecattn_select_workspace_size) for
+ * the longest sequence.  Every argument is checked for every sequence before
+ * the first launch.  Many short sequences cost one set of launches each.
+ */
+vecattn_status vecattn_select_varlen(const void* q, const vecattn_tdesc* qd, const void* k,
+                                     const vecattn_tdesc* kd, const int64_t* cu_seqlens,
+                                     int32_t nseq, int32_t block, int32_t causal, int32_t mode,
+                                     double param, int32_t* idx, int64_t cap, int32_t* counts,
+                                     int32_t* n_clamped, void* workspace, size_t workspace_bytes,
+                                     void* stream);
+vecattn_status vecattn_sparse_attn_varlen(const void* q, const vecattn_tdesc* qd, const void* k,
+                                          const vecattn_tdesc* kd, const void* v,
+                                          const vecattn_tdesc* vd, const int64_t* cu_seqlens,
+                                          int32_t nseq, const int32_t* idx, int64_t cap,
+                                          const int32_t* counts, int32_t block, int32_t causal,
+                                          float scale, void* o, const vecattn_tdesc* od,
+                                          float* lse, void* stream);
+
+/*
  * Per-head filter ratios, Eq. 5 (Sec. 3.1.2, "Dynamic Programming for Offline
  * Search of Per-Head Filter Ratios").  Host function (host memory, no GPU).
  * For each of `heads` heads, n_cand candidate filter ratios were sampled

@@ -64,9 +64,14 @@ def load() -> ctypes.CDLL:
     lib.vecattn_plan_filter_ratios.argtypes = [i32, i32, P, P, f64, i32, P, ctypes.POINTER(f64)]
     lib.vecattn_select_per_head.argtypes = [P, D, P, D, i32, i32, i32, P, i32, i32, P, i64, P, P,
                                             P, ctypes.c_size_t, P]
+    lib.vecattn_select_varlen.argtypes = [P, D, P, D, P, i32, i32, i32, i32, f64, P, i64, P, P, P,
+                                          ctypes.c_size_t, P]
+    lib.vecattn_sparse_attn_varlen.argtypes = [P, D, P, D, P, D, P, i32, P, i64, P, i32, i32, f32,
+                                               P, D, P, P]
     for name in ("vecattn_pool", "vecattn_select_max_count", "vecattn_select_workspace_size",
                  "vecattn_select", "vecattn_select_mins_tiled", "vecattn_sparse_attn",
-                 "vecattn_plan_filter_ratios", "vecattn_select_per_head"):
+                 "vecattn_plan_filter_ratios", "vecattn_select_per_head",
+                 "vecattn_select_varlen", "vecattn_sparse_attn_varlen"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -286,3 +291,70 @@ def head_sparsity(q: torch.Tensor, k: torch.Tensor, block: int, mode, params, ca
         kept = cnt.double().sum(dim=(0, 2))                      # [Hq]
         out[:, c] = (1.0 - kept / (B * L.sum())).cpu()
     return out
+
+
+def varlen_blocks(cu_seqlens, block: int):
+    """Query blocks of each packed sequence and their offsets: (per-sequence
+    N_p, first block of each sequence, total blocks)."""
+    import numpy as np
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    nb = (np.diff(cu) + block - 1) // block
+    first = np.concatenate([[0], np.cumsum(nb)[:-1]]) if len(nb) else np.zeros(0, np.int64)
+    return nb, first, int(nb.sum())
+
+
+def select_varlen(q: torch.Tensor, k: torch.Tensor, cu_seqlens, block: int, mode, param: float,
+                  causal: bool = False, cap: Optional[int] = None,
+                  workspace: Optional[torch.Tensor] = None, n_clamped: Optional[torch.Tensor] = None,
+                  keep_diag: bool = False) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Selection over packed variable-length sequences (q, k: [1, H, total, D];
+    cu_seqlens: nseq + 1 row offsets).  Returns flat (idx, counts): the
+    per-sequence [Hq, N_p(s), cap] and [Hq, N_p(s)] arrays laid end to end."""
+    import numpy as np
+    _bf16_cuda(q, "q")
+    _bf16_cuda(k, "k")
+    cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int64))
+    Hq = q.shape[1]
+    lens = np.diff(cu)
+    longest = int(lens.max()) if lens.size else 0
+    if cap is None:
+        cap = max(max_count(int(n), block, causal, mode, param, keep_diag) for n in lens if n > 0)
+    _, _, total_blocks = varlen_blocks(cu, block)
+    idx = torch.empty(total_blocks * Hq * cap, dtype=torch.int32, device=q.device)
+    counts = torch.empty(total_blocks * Hq, dtype=torch.int32, device=q.device)
+    if workspace is None:
+        qv = q[:, :, :max(longest, 1)]
+        kv = k[:, :, :max(longest, 1)]
+        workspace = torch.empty(workspace_bytes(qv, kv, block, causal, mode, cap), dtype=torch.uint8,
+                                device=q.device)
+    qd, kd = desc(q), desc(k)
+    _check(load().vecattn_select_varlen(
+        _ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd), cu.ctypes.data_as(ctypes.c_void_p),
+        int(len(cu) - 1), int(block), _flags(causal, keep_diag), mode_id(mode), float(param),
+        _ptr(idx), int(cap), _ptr(counts), _ptr(n_clamped), _ptr(workspace), workspace.numel(),
+        _stream(q)), "select_varlen")
+    return idx, counts
+
+
+def sparse_attn_varlen(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, cu_seqlens,
+                       idx: torch.Tensor, counts: torch.Tensor, cap: int, block: int,
+                       causal: bool = False, scale: float = 0.0,
+                       out: Optional[torch.Tensor] = None, return_lse: bool = False):
+    """Vector-sparse attention over packed variable-length sequences, with the
+    lists of select_varlen.  Returns out (and the flat per-sequence
+    [Hq, n_s] LSE arrays laid end to end when return_lse)."""
+    import numpy as np
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _bf16_cuda(t, n)
+    cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int64))
+    if out is None:
+        out = torch.empty_like(q, memory_format=torch.contiguous_format)
+    lse = (torch.empty(q.shape[1] * q.shape[2], dtype=torch.float32, device=q.device)
+           if return_lse else None)
+    qd, kd, vd, od = desc(q), desc(k), desc(v), desc(out)
+    _check(load().vecattn_sparse_attn_varlen(
+        _ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd), _ptr(v), ctypes.byref(vd),
+        cu.ctypes.data_as(ctypes.c_void_p), int(len(cu) - 1), _ptr(idx), int(cap), _ptr(counts),
+        int(block), int(bool(causal)), float(scale), _ptr(out), ctypes.byref(od), _ptr(lse),
+        _stream(q)), "sparse_attn_varlen")
+    return (out, lse) if return_lse else out

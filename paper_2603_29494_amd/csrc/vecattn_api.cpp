@@ -234,6 +234,105 @@ vecattn_status vecattn_sparse_attn(const void* q, const vecattn_tdesc* qd, const
   return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
 }
 
+}  // extern "C"
+
+namespace {
+
+// Packed variable-length batches: sequence s is rows [cu[s], cu[s+1]) of the
+// B = 1 tensors; its blocks, lists and counts follow those of the sequences
+// before it.
+bool cu_ok(const int64_t* cu, int32_t nseq, int64_t total) {
+  if (!cu || nseq < 1 || cu[0] != 0 || cu[nseq] != total) return false;
+  for (int32_t s = 0; s < nseq; ++s)
+    if (cu[s + 1] < cu[s]) return false;
+  return true;
+}
+
+vecattn_tdesc seq_desc(const vecattn_tdesc* d, int64_t n) {
+  vecattn_tdesc r = *d;
+  r.N = n;
+  return r;
+}
+
+const void* seq_ptr(const void* p, const vecattn_tdesc* d, int64_t row) {
+  return static_cast<const char*>(p) + row * d->sN * 2;  // bf16 elements
+}
+
+}  // namespace
+
+extern "C" {
+
+vecattn_status vecattn_select_varlen(const void* q, const vecattn_tdesc* qd, const void* k,
+                                     const vecattn_tdesc* kd, const int64_t* cu_seqlens,
+                                     int32_t nseq, int32_t block, int32_t causal, int32_t mode,
+                                     double param, int32_t* idx, int64_t cap, int32_t* counts,
+                                     int32_t* n_clamped, void* workspace, size_t workspace_bytes,
+                                     void* stream) {
+  vecattn_status st = check_desc(q, qd);
+  if (st != VECATTN_OK) return st;
+  if ((st = check_desc(k, kd)) != VECATTN_OK) return st;
+  if (qd->B != 1 || kd->B != 1 || kd->N != qd->N || kd->D != qd->D || qd->H % kd->H != 0)
+    return VECATTN_ERR_INVALID_ARG;
+  if (!cu_ok(cu_seqlens, nseq, qd->N) || !idx || !counts || block < 1 || cap < 1 || cap > kMaxN)
+    return VECATTN_ERR_INVALID_ARG;
+  if (!mode_ok(mode) || !param_ok(mode, param) || (causal & ~(kCausal | kKeepDiag)) != 0)
+    return VECATTN_ERR_INVALID_ARG;
+  // Every sequence's checks first, so that an error launches nothing.
+  for (int32_t s = 0; s < nseq; ++s) {
+    const int64_t n = cu_seqlens[s + 1] - cu_seqlens[s];
+    if (n == 0) continue;
+    if ((mode == VECATTN_SEL_TOPK || (causal & kKeepDiag)) &&
+        cap < max_count(n, block, causal, mode, param))
+      return VECATTN_ERR_CAPACITY;
+    const size_t need = vecattn::select_workspace_bytes(1, qd->H, n, qd->D, block, mode, cap);
+    if (need > 0 && (!workspace || workspace_bytes < need)) return VECATTN_ERR_CAPACITY;
+  }
+  int64_t blocks = 0;  // blocks of the sequences before s
+  for (int32_t s = 0; s < nseq; ++s) {
+    const int64_t n = cu_seqlens[s + 1] - cu_seqlens[s];
+    if (n == 0) continue;
+    const vecattn_tdesc qs = seq_desc(qd, n), ks = seq_desc(kd, n);
+    st = select_impl(seq_ptr(q, qd, cu_seqlens[s]), &qs, seq_ptr(k, kd, cu_seqlens[s]), &ks, block,
+                     causal, mode, param, nullptr, 16, 16, idx + blocks * qd->H * cap, cap,
+                     counts + blocks * qd->H, n_clamped, workspace, workspace_bytes, stream);
+    if (st != VECATTN_OK) return st;
+    blocks += num_blocks(n, block);
+  }
+  return VECATTN_OK;
+}
+
+vecattn_status vecattn_sparse_attn_varlen(const void* q, const vecattn_tdesc* qd, const void* k,
+                                          const vecattn_tdesc* kd, const void* v,
+                                          const vecattn_tdesc* vd, const int64_t* cu_seqlens,
+                                          int32_t nseq, const int32_t* idx, int64_t cap,
+                                          const int32_t* counts, int32_t block, int32_t causal,
+                                          float scale, void* o, const vecattn_tdesc* od,
+                                          float* lse, void* stream) {
+  vecattn_status st;
+  if ((st = check_desc(q, qd)) != VECATTN_OK) return st;
+  if ((st = check_desc(k, kd)) != VECATTN_OK) return st;
+  if ((st = check_desc(v, vd)) != VECATTN_OK) return st;
+  if ((st = check_desc(o, od)) != VECATTN_OK) return st;
+  if (qd->B != 1 || kd->B != 1 || vd->B != 1 || od->B != 1) return VECATTN_ERR_INVALID_ARG;
+  if (!cu_ok(cu_seqlens, nseq, qd->N) || !idx || !counts) return VECATTN_ERR_INVALID_ARG;
+  int64_t blocks = 0;
+  for (int32_t s = 0; s < nseq; ++s) {
+    const int64_t n = cu_seqlens[s + 1] - cu_seqlens[s];
+    if (n == 0) continue;
+    const int64_t r0 = cu_seqlens[s];
+    const vecattn_tdesc qs = seq_desc(qd, n), ks = seq_desc(kd, n), vs = seq_desc(vd, n),
+                        os = seq_desc(od, n);
+    // The first sequence's call checks what all calls share; later ones cannot fail on it.
+    st = vecattn_sparse_attn(seq_ptr(q, qd, r0), &qs, seq_ptr(k, kd, r0), &ks, seq_ptr(v, vd, r0),
+                             &vs, idx + blocks * qd->H * cap, cap, counts + blocks * qd->H, block,
+                             causal, scale, const_cast<void*>(seq_ptr(o, od, r0)), &os,
+                             lse ? lse + qd->H * r0 : nullptr, stream);
+    if (st != VECATTN_OK) return st;
+    blocks += num_blocks(n, block);
+  }
+  return VECATTN_OK;
+}
+
 vecattn_status vecattn_plan_filter_ratios(int32_t heads, int32_t n_cand, const double* sparsity,
                                           const double* perf, double target, int32_t grid,
                                           int32_t* choice, double* best_perf) {

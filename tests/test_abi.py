@@ -185,6 +185,34 @@ def test_keep_diag_flag():
     assert attn(causal=4) == INVALID
 
 
+def test_varlen_rejects_bad_offsets():
+    lib = _lib.load()
+    qd, kd = desc(1, 4, 256, 128), desc(1, 2, 256, 128)
+
+    def sel(cu, n=None, qd_=qd, cap=256):
+        arr = None if cu is None else (ctypes.c_int64 * len(cu))(*cu)
+        return lib.vecattn_select_varlen(FAKE, ctypes.byref(qd_), FAKE, ctypes.byref(kd), arr,
+                                         len(cu) - 1 if n is None else n, 64, 0, 0, 0.25, FAKE,
+                                         cap, FAKE, None, None, 1 << 40, None)
+
+    assert sel(None, n=1) == INVALID
+    assert sel([0]) == INVALID                        # no sequence
+    assert sel([1, 256]) == INVALID                   # must start at row 0
+    assert sel([0, 100, 50, 256]) == INVALID          # decreasing
+    assert sel([0, 100, 200]) == INVALID              # must end at N
+    assert sel([0, 100, 256], qd_=desc(2, 4, 256, 128)) == INVALID   # packed: B = 1
+    assert sel([0, 100, 256], cap=24) == CAPACITY     # topK 25% of 156 keys = 39
+    assert sel([0, 100, 256], cap=64) == CAPACITY     # valid: the missing workspace is reported
+
+    def att(cu):
+        arr = (ctypes.c_int64 * len(cu))(*cu)
+        return lib.vecattn_sparse_attn_varlen(FAKE, ctypes.byref(qd), FAKE, ctypes.byref(kd), FAKE,
+                                              ctypes.byref(kd), arr, len(cu) - 1, FAKE, 16, FAKE,
+                                              64, 0, 0.0, FAKE, ctypes.byref(qd), None, None)
+    assert att([0, 300]) == INVALID
+    assert att([0, 200, 100]) == INVALID
+
+
 def test_workspace_size_query():
     qd, kd = desc(1, 40, 75600, 128), desc(1, 40, 75600, 128)
     n = ctypes.c_size_t(0)

@@ -281,3 +281,39 @@ def test_keep_diagonal(gpu, name, param, causal):
                                               cap)
     assert np.array_equal(a_cnt.cpu().numpy(), want_cnt)
     assert np.array_equal(a_idx.cpu().numpy(), want_idx)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_varlen_batch(gpu, causal):
+    # Packed sequences (one empty) in one call equal separate calls on each
+    # sequence's rows; attention on the packed lists matches the oracle.
+    lens = [300, 0, 777, 64, 129]
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    Hq, Hkv, D, block = 4, 2, 128, 64
+    q, k, v = synth.planted_case(500 + int(causal), 1, Hq, Hkv, int(cu[-1]), D)
+    tq, tk, tv = dev(q), dev(k), dev(v)
+    cap = max(va.max_count(n, block, causal, "topk", 0.2) for n in lens if n)
+    idx, cnt = va.select_varlen(tq, tk, cu, block, "topk", 0.2, causal, cap=cap)
+    out, lse = va.sparse_attn_varlen(tq, tk, tv, cu, idx, cnt, cap, block, causal, return_lse=True)
+    torch.cuda.synchronize()
+    nb, first, total = va.varlen_blocks(cu, block)
+    idx = idx.view(-1).cpu().numpy()
+    cnt = cnt.view(-1).cpu().numpy()
+    for s, n in enumerate(lens):
+        if n == 0:
+            continue
+        r0, r1 = int(cu[s]), int(cu[s + 1])
+        i_s, c_s = va.select(tq[:, :, r0:r1], tk[:, :, r0:r1], block, "topk", 0.2, causal, cap=cap)
+        torch.cuda.synchronize()
+        got_i = idx[first[s] * Hq * cap:(first[s] + nb[s]) * Hq * cap].reshape(1, Hq, nb[s], cap)
+        got_c = cnt[first[s] * Hq:(first[s] + nb[s]) * Hq].reshape(1, Hq, nb[s])
+        assert np.array_equal(got_i, i_s.cpu().numpy()) and np.array_equal(got_c, c_s.cpu().numpy())
+        qs, ks, vs = (np.ascontiguousarray(a[:, :, r0:r1]) for a in (q, k, v))
+        o_ref, lse_ref = oracle.sparse_attn(qs, ks, vs, got_i, got_c, block, causal)
+        o = out[:, :, r0:r1].float().cpu().numpy()
+        err = np.abs(o - o_ref)
+        assert err.max() <= 2e-2 and err.mean() <= 2e-3, (s, err.max())
+        l = lse[Hq * r0:Hq * r1].view(1, Hq, n).cpu().numpy()
+        ok = np.isfinite(lse_ref)
+        assert np.array_equal(np.isfinite(l), ok)
+        assert np.abs(l[ok] - lse_ref[ok]).max() <= 2e-3

@@ -109,6 +109,7 @@ struct SelParams {
   int mins_direct;  // minS with cap >= every block's eligible keys: no count needed
   int mode_tiled;   // cross-tile minS (Algorithm 1)
   int keep_diag;    // every block also keeps the keys of its own rows
+  int quad_rows;    // idx rows start on 16 bytes and no row can exceed cap
   int tiled_tile;   // keys per tile: 16 or 32
   int tiled_gs;     // keys per group of tiles (a power of two)
   int tiled_sb;     // 32-key blocks per segment a wave walks in order
@@ -1189,10 +1190,24 @@ __global__ __launch_bounds__(256) void k_resolve_cand(SelParams p) {
 // loads do not wait for one another.
 constexpr int kCompactBatch = 8;
 
+// Inclusive prefix sum over the 64 lanes of a wave with DPP moves (no LDS):
+// shifts by 1, 2, 4, 8 inside each 16-lane row, then row 0's total into row 1
+// and row 2's into row 3 (broadcast of lane 15), and rows 0-1's total into
+// rows 2-3 (broadcast of lane 31).  Lanes without a source add 0.
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return x;
+}
+
 __global__ __launch_bounds__(64) void k_compact(SelParams p) {
   const int64_t r = blockIdx.x;
   const RowState& s = p.st[r];
-  __shared__ int32_t stage[64 * 32];
+  __shared__ __align__(16) int32_t stage[64 * 32 + 4];
   const int lane = threadIdx.x;
   const int L = s.L;
   const int nw = (L + 31) / 32;
@@ -1200,9 +1215,14 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
   const int k_eq = s.k_eq;
   const uint32_t* bsel = p.bsel + r * p.W;
   const uint32_t* btie = p.btie + r * p.W;
-  int base = 0;      // entries written so far
+  int base = 0;      // entries listed so far
   int ties_seen = 0; // tied keys met so far (ascending index)
   int32_t* out = p.idx + r * p.cap;
+  // Rows that start on 16 bytes and cannot exceed cap are stored four entries
+  // per lane; the last (< 4) entries of a chunk wait in stage[0, 4) for the
+  // next one, and go out one by one after the last chunk.
+  const bool quads = p.quad_rows;
+  int done = 0;      // entries stored (quad path)
   for (int c0 = 0; c0 < nw; c0 += 64 * kCompactBatch) {
     uint32_t mb[kCompactBatch], tb[kCompactBatch];
 #pragma unroll
@@ -1219,11 +1239,7 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
       if (tiep) {  // uniform per row: keep only the first k_eq tied keys
         const uint32_t tw = tb[j];
         const int nt = __builtin_popcount(tw);
-        int incl = nt;
-        for (int o = 1; o < 64; o <<= 1) {
-          const int y = __shfl_up(incl, o);
-          if (lane >= o) incl += y;
-        }
+        const int incl = wave_incl_scan(nt);
         int room = k_eq - (ties_seen + incl - nt);  // ties this lane may still keep
         uint32_t t2 = tw;
         while (t2 && room > 0) {
@@ -1232,7 +1248,7 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
           t2 ^= bit;
           --room;
         }
-        ties_seen += __shfl(incl, 63);
+        ties_seen += __builtin_amdgcn_readlane(incl, 63);
       }
       if (p.keep_diag) {  // the keys of the block's own rows, [i P, min(N, (i + 1) P))
         const int i = static_cast<int>(r % p.Np);
@@ -1241,13 +1257,10 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
       }
       if (wd < nw && L - 32 * wd < 32) m &= (1u << (L - 32 * wd)) - 1u;
       const int nb = __builtin_popcount(m);
-      int pre = nb;
-      for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(pre, o);
-        if (lane >= o) pre += y;
-      }
-      const int total = __shfl(pre, 63);
-      int pos = pre - nb;
+      const int pre = wave_incl_scan(nb);
+      const int total = __builtin_amdgcn_readlane(pre, 63);
+      const int pend = base - done;  // quad path: entries waiting in stage[0, pend), < 4
+      int pos = (quads ? pend : 0) + pre - nb;
       uint32_t mm = m;
       while (mm) {
         const int bit = __builtin_ctz(mm);
@@ -1255,11 +1268,28 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
         stage[pos++] = 32 * wd + bit;
       }
       __syncthreads();
-      for (int t = lane; t < total; t += 64)
-        if (base + t < p.cap) out[base + t] = stage[t];
-      __syncthreads();
+      if (quads) {
+        const int avail = pend + total;
+        const int nq = avail / 4;
+        int4* out4 = reinterpret_cast<int4*>(out + done);
+        const int4* st4 = reinterpret_cast<const int4*>(stage);
+        for (int t = lane; t < nq; t += 64) out4[t] = st4[t];
+        const int rem = avail - 4 * nq;
+        const int carry = lane < rem ? stage[4 * nq + lane] : 0;
+        __syncthreads();
+        if (lane < rem) stage[lane] = carry;
+        done += 4 * nq;
+      } else {
+        for (int t = lane; t < total; t += 64)
+          if (base + t < p.cap) out[base + t] = stage[t];
+        __syncthreads();
+      }
       base += total;
     }
+  }
+  if (quads) {  // the last entries, fewer than 4
+    __syncthreads();
+    if (lane < base - done) out[done + lane] = stage[lane];
   }
   const int n = min(base, static_cast<int>(p.cap));
   for (int t = n + lane; t < p.cap; t += 64) out[t] = -1;
@@ -1380,6 +1410,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.D = static_cast<int>(D);
   p.causal = a.causal;
   p.keep_diag = a.keep_diag;
+  p.quad_rows = (a.cap % 4 == 0) && (reinterpret_cast<uintptr_t>(a.idx) % 16 == 0) && a.mode != 3;
   p.split = split;
   p.nsplit = static_cast<int>((N + split - 1) / split);
   p.W = static_cast<int>((N + 31) / 32);

@@ -317,3 +317,22 @@ def test_varlen_batch(gpu, causal):
         ok = np.isfinite(lse_ref)
         assert np.array_equal(np.isfinite(l), ok)
         assert np.abs(l[ok] - lse_ref[ok]).max() <= 2e-3
+
+
+@pytest.mark.parametrize("mode,param", [("topk", 0.1), ("topp", 0.9), ("mins", 0.7)])
+def test_list_writer_alignment_paths(gpu, mode, param):
+    # Lists of rows that start on 16 bytes are stored four entries at a time,
+    # others one at a time: both give the same lists and -1 padding.
+    q, k, _ = synth.planted_case(600 + len(mode), 1, 3, 3, 1337, 128)
+    need = va.max_count(1337, 64, True, mode, param)
+    caps = [need + (-need) % 4, need + (-need) % 4 + 1]       # a multiple of 4, and not
+    res = []
+    for cap in caps:
+        idx, cnt = va.select(dev(q), dev(k), 64, mode, param, True, cap=cap)
+        torch.cuda.synchronize()
+        res.append((idx.cpu().numpy(), cnt.cpu().numpy()))
+    (i0, c0), (i1, c1) = res
+    assert np.array_equal(c0, c1)
+    assert np.array_equal(i0, i1[..., :caps[0]]) and np.all(i1[..., caps[0]:] == -1)
+    check_rows(q, k, 64, {"topk": oracle.TOPK, "topp": oracle.TOPP, "mins": oracle.MINS}[mode],
+               param, True, caps[0], i0, c0, all_rows(q, 64))

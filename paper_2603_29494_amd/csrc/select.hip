@@ -47,6 +47,11 @@ constexpr int kLevels = 6;      // histogram refinements per round (idle ones co
 constexpr int kCand = 1024;     // candidate capacity per row
 constexpr int kRounds = 2;      // a topP row whose count exceeds cap reruns as topK(cap)
 constexpr int kMaxHeadParams = 128;  // query heads a per-head parameter list may cover
+// Rows entering each later pass are counted (nact[level] for histogram level
+// >= 1, nact[kEmitSlot] for the emit pass); a pass that no row needs returns
+// at once, without reading row state.
+constexpr int kEmitSlot = kLevels + 1;
+constexpr int kActiveSlots = 16;
 
 enum Phase : int { PH_IDLE = 0, PH_HIST = 1, PH_COLLECT = 2, PH_DONE = 3, PH_EMIT = 4 };
 // MODE_HIST0: first histogram level (the interval is everything).
@@ -110,6 +115,8 @@ struct SelParams {
   int mode_tiled;   // cross-tile minS (Algorithm 1)
   int keep_diag;    // every block also keeps the keys of its own rows
   int quad_rows;    // idx rows start on 16 bytes and no row can exceed cap
+  uint32_t* nact;   // [kActiveSlots] rows waiting for each later pass
+  int gate;         // slot of nact this launch needs non-zero, or -1
   int tiled_tile;   // keys per tile: 16 or 32
   int tiled_gs;     // keys per group of tiles (a power of two)
   int tiled_sb;     // 32-key blocks per segment a wave walks in order
@@ -258,6 +265,9 @@ __global__ __launch_bounds__(256) void k_k_operand_order(const uint16_t* __restr
 }
 
 __global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
+  // Counters start at zero once per call (rows sent to the emit pass in the
+  // first round still count in the second).
+  if (round == 0 && blockIdx.x == 0 && threadIdx.x < kActiveSlots) p.nact[threadIdx.x] = 0u;
   const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (r >= p.rows) return;
   RowState& s = p.st[r];
@@ -349,6 +359,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   __shared__ __align__(16) float s_acc[COL ? 4 * 64 * 16 : 1];  // per lane: its 16 scores
   __shared__ uint32_t s_max[MODE == MODE_MAX ? kRowsWG : 1];  // ordered keys of row maxima
 
+  if (p.gate >= 0 && p.nact[p.gate] == 0u) return;  // no row needs this pass
   const int64_t item = xcd_work_item(p.per_xcd);
   if (item >= p.items) return;
   const int rb = static_cast<int>(item % p.nrb);
@@ -736,6 +747,7 @@ __global__ __launch_bounds__(256) void k_mins(SelParams p) {
     s.tie_interval = 0;
     s.k_eq = 0;
     s.phase = PH_EMIT;
+    atomicAdd(&p.nact[kEmitSlot], 1u);
     return;
   }
   s.blo = tf;
@@ -934,6 +946,7 @@ __global__ __launch_bounds__(256) void k_tiled_init(SelParams p) {
 // Resolve after a HIST pass: one wave per row.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
+  if (level > 0 && p.nact[level] == 0u) return;
   const int64_t r = blockIdx.x;
   RowState& s = p.st[r];
   if (s.phase != PH_HIST || s.level != level) return;
@@ -981,6 +994,7 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
       s.count = static_cast<int>(tot);
       s.level = level + 1;
       s.phase = PH_EMIT;
+      atomicAdd(&p.nact[kEmitSlot], 1u);
       return;
     }
     s.k_target = static_cast<int>(p.cap);  // more than cap: keep the cap best
@@ -1045,6 +1059,7 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
   if (inside <= static_cast<uint32_t>(kCand) || nl >= kLevels) {
     s.phase = PH_COLLECT;
   } else {
+    atomicAdd(&p.nact[nl], 1u);
     // An end bin also holds the scores beyond the bin range (level 0 of topK
     // rows bins a sampled bracket, not the whole range): the next level spans
     // the chosen bins' actual extent, within the Cauchy-Schwarz bound.
@@ -1167,6 +1182,7 @@ __global__ __launch_bounds__(256) void k_resolve_cand(SelParams p) {
       }
       s.count = count;
       s.phase = PH_EMIT;
+      atomicAdd(&p.nact[kEmitSlot], 1u);
       if (s.clamped && p.n_clamped) atomicAdd(p.n_clamped, 1);
     }
   }
@@ -1308,7 +1324,7 @@ __global__ __launch_bounds__(256) void k_zero_u32(uint32_t* p, int64_t n) {
 // ---------------------------------------------------------------------------
 struct Layout {
   size_t qp, state, hist, nab, mab, zp, cand_n, cand_lohi, cand, bsel, btie, qnorm, kmax, qmax, kop,
-      total;
+      nact, total;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -1336,6 +1352,7 @@ Layout layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t D, int32_t 
   l.kmax = take(B * Hkv * 4);
   l.qmax = take(rows * nsplit * 4 * 4);
   l.kop = take(B * Hkv * ((N + 31) / 32) * 32 * D * 2);
+  l.nact = take(kActiveSlots * 4);
   l.total = o;
   return l;
 }
@@ -1421,6 +1438,8 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.mode_tiled = a.mode == 3;
   p.qmax = reinterpret_cast<float*>(ws + l.qmax);
   p.kop = reinterpret_cast<const u32x4*>(ws + l.kop);
+  p.nact = reinterpret_cast<uint32_t*>(ws + l.nact);
+  p.gate = -1;
   p.nkb = static_cast<int>((N + 31) / 32);
   p.param = a.param;
   p.per_head = a.head_params != nullptr;
@@ -1510,14 +1529,20 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
     if (p.mins_direct) break;  // every row goes straight to the emit pass
     for (int lv = 0; lv < kLevels; ++lv) {
       // Level 0 bins every key, except for minS rows, which count [threshold, max].
-      if (lv == 0 && !p.mode_mins) score_pass<MODE_HIST0>(D, p.mode_topp != 0, pgrid, p, stream);
-      else score_pass<MODE_HIST>(D, p.mode_topp != 0, pgrid, p, stream);
+      SelParams pl = p;
+      pl.gate = lv > 0 ? lv : -1;
+      if (lv == 0 && !p.mode_mins) score_pass<MODE_HIST0>(D, p.mode_topp != 0, pgrid, pl, stream);
+      else score_pass<MODE_HIST>(D, p.mode_topp != 0, pgrid, pl, stream);
       hipLaunchKernelGGL(k_resolve_hist, rgrid, dim3(64), 0, stream, p, lv);
     }
     score_pass<MODE_COLLECT>(D, p.mode_topp != 0, pgrid, p, stream);
     hipLaunchKernelGGL(k_resolve_cand, rgrid, dim3(256), 0, stream, p);
   }
-  score_pass<MODE_EMIT>(D, p.mode_topp != 0, pgrid, p, stream);
+  {
+    SelParams pe = p;
+    pe.gate = kEmitSlot;
+    score_pass<MODE_EMIT>(D, p.mode_topp != 0, pgrid, pe, stream);
+  }
   hipLaunchKernelGGL(k_compact, rgrid, dim3(64), 0, stream, p);
   return hipGetLastError();
 }

@@ -43,7 +43,7 @@ namespace {
 constexpr int kRowsWG = 64;     // pooled rows per workgroup
 constexpr int kThreads = 256;
 constexpr int kBins = 256;
-constexpr int kLevels = 6;      // histogram refinements per round (idle ones cost ~25 us)
+constexpr int kLevels = 6;      // histogram refinements per round (idle ones cost ~6 us)
 constexpr int kCand = 1024;     // candidate capacity per row
 constexpr int kRounds = 2;      // a topP row whose count exceeds cap reruns as topK(cap)
 constexpr int kMaxHeadParams = 128;  // query heads a per-head parameter list may cover

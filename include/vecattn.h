@@ -218,6 +218,24 @@ vecattn_status vecattn_sparse_attn(const void* q, const vecattn_tdesc* qd, const
                                    const vecattn_tdesc* od, float* lse, void* stream);
 
 /*
+ * Checker for the index input of vecattn_sparse_attn, for lists that did not
+ * come from vecattn_select.  Sets *n_bad (device int32, cleared by the call)
+ * to the number of rows whose list breaks the attention's contract: a count
+ * outside [0, cap], or among the row's first `count` entries one outside
+ * [0, n_keys) or one not strictly above the entry before it.  Entries past a
+ * row's count are not read.
+ *   idx    : int32 [rows, cap], contiguous (e.g. [B, Hq, N_p, cap] as rows =
+ *            B * Hq * N_p)            counts : int32 [rows]
+ *   n_keys : N of the keys the lists index
+ * One read of the listed entries (4 bytes each); asynchronous on `stream`.
+ * Errors: INVALID_ARG (n_bad NULL, idx or counts NULL with rows > 0, rows < 0
+ * or > 2^31 - 1, cap < 1, n_keys < 1, cap or n_keys > 2^30).
+ */
+vecattn_status vecattn_check_lists(const int32_t* idx, int64_t rows, int64_t cap,
+                                   const int32_t* counts, int64_t n_keys, int32_t* n_bad,
+                                   void* stream);
+
+/*
  * Variable-length batches.  Sequences of different lengths packed along N of
  * B = 1 tensors: sequence s is rows [cu_seqlens[s], cu_seqlens[s+1]) (host
  * int64, nseq + 1 values, cu_seqlens[0] = 0, non-decreasing, last = N; empty

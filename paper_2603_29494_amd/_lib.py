@@ -61,6 +61,7 @@ def load() -> ctypes.CDLL:
     lib.vecattn_select_mins_tiled.argtypes = [P, D, P, D, i32, i32, f64, i32, i32, P, i64, P, P,
                                               P, ctypes.c_size_t, P]
     lib.vecattn_sparse_attn.argtypes = [P, D, P, D, P, D, P, i64, P, i32, i32, f32, P, D, P, P]
+    lib.vecattn_check_lists.argtypes = [P, i64, i64, P, i64, P, P]
     lib.vecattn_plan_filter_ratios.argtypes = [i32, i32, P, P, f64, i32, P, ctypes.POINTER(f64)]
     lib.vecattn_select_per_head.argtypes = [P, D, P, D, i32, i32, i32, P, i32, i32, P, i64, P, P,
                                             P, ctypes.c_size_t, P]
@@ -71,7 +72,7 @@ def load() -> ctypes.CDLL:
     for name in ("vecattn_pool", "vecattn_select_max_count", "vecattn_select_workspace_size",
                  "vecattn_select", "vecattn_select_mins_tiled", "vecattn_sparse_attn",
                  "vecattn_plan_filter_ratios", "vecattn_select_per_head",
-                 "vecattn_select_varlen", "vecattn_sparse_attn_varlen"):
+                 "vecattn_select_varlen", "vecattn_sparse_attn_varlen", "vecattn_check_lists"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -244,6 +245,22 @@ def sparse_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: torch.Te
                                       _ptr(out), ctypes.byref(od), _ptr(lse), _stream(q)),
            "sparse_attn")
     return (out, lse) if return_lse else out
+
+
+def check_lists(idx: torch.Tensor, counts: torch.Tensor, n_keys: int) -> int:
+    """Number of rows of (idx [..., cap], counts [...]) that break sparse_attn's
+    input contract (count outside [0, cap], a listed key outside [0, n_keys), or a
+    list not strictly ascending); 0 for any output of select.  Synchronises."""
+    if idx.dtype != torch.int32 or counts.dtype != torch.int32 or not idx.is_cuda \
+            or not counts.is_cuda or not idx.is_contiguous() or not counts.is_contiguous():
+        raise ValueError("idx and counts must be contiguous int32 CUDA tensors")
+    if idx.dim() < 1 or tuple(idx.shape[:-1]) != tuple(counts.shape):
+        raise ValueError("idx must be [..., cap] with counts of shape [...]")
+    n_bad = torch.empty(1, dtype=torch.int32, device=idx.device)
+    _check(load().vecattn_check_lists(_ptr(idx), int(counts.numel()), int(idx.shape[-1]),
+                                      _ptr(counts), int(n_keys), _ptr(n_bad), _stream(idx)),
+           "check_lists")
+    return int(n_bad.item())
 
 
 def plan_filter_ratios(sparsity, perf, target: float, grid: int = 1000):

@@ -54,6 +54,11 @@ size_t select_workspace_bytes(int64_t B, int64_t Hq, int64_t N, int64_t D, int32
                               int32_t mode, int64_t cap);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 
+// Rows whose list breaks the attention's input contract, counted into *n_bad
+// (cleared first).  rows <= 2^31 - 1 fits the grid.
+hipError_t launch_check_lists(const int32_t* idx, const int32_t* counts, int64_t rows, int64_t cap,
+                              int64_t n_keys, int32_t* n_bad, hipStream_t stream);
+
 // Host: per-head filter ratios by dynamic programming (Eq. 5).  Returns 0, or
 // 1 when no choice reaches the target.
 int plan_filter_ratios(int32_t H, int32_t C, const double* sp, const double* perf, double target,

@@ -234,6 +234,18 @@ vecattn_status vecattn_sparse_attn(const void* q, const vecattn_tdesc* qd, const
   return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
 }
 
+vecattn_status vecattn_check_lists(const int32_t* idx, int64_t rows, int64_t cap,
+                                   const int32_t* counts, int64_t n_keys, int32_t* n_bad,
+                                   void* stream) {
+  if (!n_bad || rows < 0 || rows > INT32_MAX || cap < 1 || cap > kMaxN || n_keys < 1 ||
+      n_keys > kMaxN)
+    return VECATTN_ERR_INVALID_ARG;
+  if (rows > 0 && (!idx || !counts)) return VECATTN_ERR_INVALID_ARG;
+  hipError_t e = vecattn::launch_check_lists(idx, counts, rows, cap, n_keys, n_bad,
+                                             static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
+}
+
 }  // extern "C"
 
 namespace {

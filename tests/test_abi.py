@@ -213,6 +213,24 @@ def test_varlen_rejects_bad_offsets():
     assert att([0, 200, 100]) == INVALID
 
 
+def test_check_lists_rejects_bad_arguments():
+    lib = _lib.load()
+
+    def chk(idx=FAKE, rows=10, cap=16, cnt=FAKE, n=256, out=FAKE):
+        return lib.vecattn_check_lists(idx, rows, cap, cnt, n, out, None)
+
+    assert chk(idx=None) == INVALID
+    assert chk(cnt=None) == INVALID
+    assert chk(out=None) == INVALID
+    assert chk(rows=-1) == INVALID
+    assert chk(rows=1 << 31) == INVALID
+    assert chk(cap=0) == INVALID
+    assert chk(cap=(1 << 30) + 1) == INVALID
+    assert chk(n=0) == INVALID
+    assert chk(n=(1 << 30) + 1) == INVALID
+    assert chk(rows=0, idx=None, cnt=None, n=0) == INVALID         # still validated when empty
+
+
 def test_workspace_size_query():
     qd, kd = desc(1, 40, 75600, 128), desc(1, 40, 75600, 128)
     n = ctypes.c_size_t(0)

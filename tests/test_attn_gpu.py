@@ -179,3 +179,65 @@ def test_k_and_v_with_different_row_strides(gpu, D):
                             return_lse=True)
     torch.cuda.synchronize()
     check_attn(o, lse, o_ref, lse_ref, f"kv strides D={D}")
+
+
+def sparse_lists(seed, B, H, Np, N, P, causal, max_count):
+    """Short random ascending lists (1 .. max_count keys per block) for long
+    sequences, drawn without a pass over all N keys per block."""
+    r = np.random.Generator(np.random.PCG64(seed))
+    idx = np.full((B * H * Np, max_count), -1, dtype=np.int32)
+    cnt = np.zeros(B * H * Np, dtype=np.int32)
+    for row in range(B * H * Np):
+        i = row % Np
+        L = min(N, (i + 1) * P) if causal else N
+        want = int(r.integers(1, min(max_count, L) + 1))
+        uniq = np.unique(r.integers(0, L, size=2 * want + 8))
+        keys = np.sort(r.choice(uniq, size=min(want, uniq.size), replace=False))
+        idx[row, :keys.size] = keys
+        cnt[row] = keys.size
+    return idx.reshape(B, H, Np, max_count), cnt.reshape(B, H, Np)
+
+
+# Long sequences whose K/V sizes make the kernel deal blocks to groups of 2, 4
+# and 8 XCDs (K and V rows of one KV head: N * D * 4 bytes, half when causal;
+# the group is the smallest whose concurrently swept heads fit ~160 MB):
+# 30.7 MB x 8 heads -> 2, with two 64-row chunks per 128-row block; the same
+# causal; 46 MB x 8 (B = 2) -> 4; one 205 MB KV head shared by 2 query heads -> 8.
+XCD_CASES = [(1, 8, 8, 60000, 128, False), (1, 8, 8, 120000, 64, True),
+             (2, 4, 4, 90000, 64, False), (1, 2, 1, 400000, 64, False)]
+
+
+@pytest.mark.parametrize("case", XCD_CASES, ids=["g2_chunked", "g2_causal", "g4_batch2", "g8_gqa"])
+def test_long_sequences_sampled(gpu, case):
+    B, Hq, Hkv, N, P, causal = case
+    D = 128
+    print(f"long sequence {case}", flush=True)
+    q = synth.random_bits(61, (B, Hq, N, D))
+    k = synth.random_bits(62, (B, Hkv, N, D))
+    v = synth.random_bits(63, (B, Hkv, N, D))
+    Np = (N + P - 1) // P
+    idx, cnt = sparse_lists(64, B, Hq, Np, N, P, causal, 96)
+    o, lse = va.sparse_attn(dev(q), dev(k), dev(v), torch.from_numpy(idx).cuda(),
+                            torch.from_numpy(cnt).cuda(), P, causal, return_lse=True)
+    torch.cuda.synchronize()
+    # Causal rows can see no listed key: O = 0 and LSE = -inf there, finite elsewhere.
+    assert bool(torch.isfinite(o.float()).all())
+    assert bool((torch.isfinite(lse) | torch.isneginf(lse)).all())
+    rng = np.random.Generator(np.random.PCG64(65))
+    total = B * Hq * Np
+    rows = np.unique(np.concatenate([[0, Np - 1, total - 1],
+                                     rng.choice(total, size=9, replace=False)]))
+    flat_i, flat_c = idx.reshape(total, -1), cnt.reshape(total)
+    o_ref, lse_ref = oracle.sparse_attn(q, k, v, flat_i[rows], flat_c[rows], P, causal,
+                                        blocks=rows, compact=True, nthreads=8)
+    for t, r in enumerate(rows):
+        i, h, b = r % Np, (r // Np) % Hq, r // (Np * Hq)
+        n = min(N, (i + 1) * P) - i * P
+        got = o[b, h, i * P:i * P + n].float().cpu().numpy().astype(np.float64)
+        err = np.abs(got - o_ref[t, :n])
+        assert err.max() <= ATOL_MAX and err.mean() <= ATOL_MEAN, (case, int(r), err.max())
+        lg = lse[b, h, i * P:i * P + n].cpu().numpy().astype(np.float64)
+        empty = np.isneginf(lse_ref[t, :n])
+        assert np.array_equal(np.isneginf(lg), empty) and np.all(got[empty] == 0.0), (case, int(r))
+        if (~empty).any():
+            assert np.abs(lg[~empty] - lse_ref[t, :n][~empty]).max() <= LSE_TOL, (case, int(r))

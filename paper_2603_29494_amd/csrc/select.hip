@@ -942,6 +942,20 @@ __global__ __launch_bounds__(256) void k_tiled_init(SelParams p) {
   s.phase = PH_EMIT;
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave with DPP moves (no LDS):
+// shifts by 1, 2, 4, 8 inside each 16-lane row, then row 0's total into row 1
+// and row 2's into row 3 (broadcast of lane 15), and rows 0-1's total into
+// rows 2-3 (broadcast of lane 31).  Lanes without a source add 0.
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return x;
+}
+
 // ---------------------------------------------------------------------------
 // Resolve after a HIST pass: one wave per row.
 // ---------------------------------------------------------------------------
@@ -957,9 +971,7 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
     p.hist[r * kBins + t] = 0u;  // ready for the next level
   }
   __syncthreads();
-  if (lane != 0) return;
-  // Sum the per-split statistics in split order.
-  const int64_t bh = r / p.Np;
+  // Sum the per-split statistics in split order (every lane alike).
   const int i = static_cast<int>(r % p.Np);
   const int rb = i / kRowsWG;
   const int i_last = min(p.Np, (rb + 1) * kRowsWG) - 1;
@@ -972,7 +984,48 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
     mab += p.m_above[r * p.nsplit + q];
     if (level == 0) z += p.zpart[r * p.nsplit + q];
   }
-  (void)bh;
+  // Count cut (topK, and minS rows over cap) across the wave: lane l holds
+  // bins 255 - 4l - j (j = 0..3, descending), and the scan counts the keys in
+  // every bin from the top through them.  The cut bin is the highest bin whose
+  // count from the top reaches the target rank (never an empty bin: the bin
+  // above it fell short); `cut_above` counts the keys in the bins above it.
+  static_assert(kBins == 4 * 64, "four bins per lane");
+  int hb[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) hb[j] = static_cast<int>(hs[kBins - 1 - 4 * lane - j]);
+  const int lsum = hb[0] + hb[1] + hb[2] + hb[3];
+  const int incl = wave_incl_scan(lsum);
+  const int total_in = __builtin_amdgcn_readlane(incl, 63);
+  int cut_bin = -1, cut_above = 0;
+  if (!s.topp) {
+    const bool over_cap = s.mins && static_cast<uint32_t>(total_in) + nab >
+                                        static_cast<uint32_t>(p.cap);
+    const int kt = over_cap ? static_cast<int>(p.cap) : s.k_target;
+    const int want = max(kt - static_cast<int>(nab), 1);
+    const uint64_t hit = __ballot(incl >= want);
+    if (hit != 0ull) {
+      const int src = __builtin_ctzll(hit);  // lowest lane: the highest bins
+      int c = incl - lsum, jb = 3;  // in lane src: the first j whose count reaches `want`
+      for (int j = 0; j < 4; ++j) {
+        if (c + hb[j] >= want) { jb = j; break; }
+        c += hb[j];
+      }
+      cut_bin = __builtin_amdgcn_readlane(kBins - 1 - 4 * lane - jb, src);
+      cut_above = __builtin_amdgcn_readlane(c, src);
+    } else {  // cannot happen unless the counts disagree: the lowest non-empty bin
+      const uint64_t ne = __ballot(lsum > 0);
+      if (ne != 0ull) {
+        const int src = 63 - __builtin_clzll(ne);  // highest lane: the lowest bins
+        int jb = 0;
+        for (int j = 3; j >= 0; --j)
+          if (hb[j] != 0) { jb = j; break; }
+        cut_bin = __builtin_amdgcn_readlane(kBins - 1 - 4 * lane - jb, src);
+        const int h_low = jb == 0 ? hb[0] : jb == 1 ? hb[1] : jb == 2 ? hb[2] : hb[3];
+        cut_above = total_in - __builtin_amdgcn_readlane(h_low, src);
+      }
+    }
+  }
+  if (lane != 0) return;
   if (level == 0 && s.topp) {
     s.Z = z;
     s.pZ = row_param(p, r) * z;
@@ -983,9 +1036,7 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
   uint32_t above_bins = 0;  // keys in bins above bb (inside the interval)
   if (s.mins) {  // level 0 of a minS row: the histogram counts the keys it keeps
     s.mins = 0;
-    uint32_t tot = 0;
-    for (int bn = 0; bn < kBins; ++bn) tot += hs[bn];
-    tot += nab;
+    const uint32_t tot = static_cast<uint32_t>(total_in) + nab;
     if (tot <= static_cast<uint32_t>(p.cap)) {
       s.tstar = s.s_lo;  // the emit pass keeps s > t* and, all ties kept, s == t*
       s.tie_partial = 0;
@@ -1001,23 +1052,8 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
     s.clamped = 1;
   }
   if (!s.topp) {
-    const int k_rem = s.k_target - static_cast<int>(nab);  // rank of the cut inside the interval
-    uint32_t cum = 0;
-    for (int bn = kBins - 1; bn >= 0; --bn) {
-      if (hs[bn] == 0) continue;
-      if (cum + hs[bn] >= static_cast<uint32_t>(max(k_rem, 1))) {
-        ba = bb = bn;
-        break;
-      }
-      cum += hs[bn];
-    }
-    if (ba < 0) {  // cannot happen unless the counts disagree; keep the lowest non-empty bin
-      for (int bn = 0; bn < kBins; ++bn)
-        if (hs[bn]) { ba = bb = bn; break; }
-      cum = 0;
-      for (int bn = kBins - 1; bn > ba; --bn) cum += hs[bn];
-    }
-    above_bins = cum;
+    ba = bb = cut_bin;  // from the wave scan above (target: k_target, or cap for minS)
+    above_bins = static_cast<uint32_t>(cut_above);
   } else {
     // Mass bounds per bin from its score range; the cut bin range is every bin
     // the true cut may lie in.
@@ -1205,20 +1241,6 @@ __global__ __launch_bounds__(256) void k_resolve_cand(SelParams p) {
 // together: the row's chunks are processed strictly in order, but their
 // loads do not wait for one another.
 constexpr int kCompactBatch = 8;
-
-// Inclusive prefix sum over the 64 lanes of a wave with DPP moves (no LDS):
-// shifts by 1, 2, 4, 8 inside each 16-lane row, then row 0's total into row 1
-// and row 2's into row 3 (broadcast of lane 15), and rows 0-1's total into
-// rows 2-3 (broadcast of lane 31).  Lanes without a source add 0.
-__device__ __forceinline__ int wave_incl_scan(int x) {
-  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);  // row_shr:1
-  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);  // row_shr:2
-  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);  // row_shr:4
-  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);  // row_shr:8
-  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15
-  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31
-  return x;
-}
 
 __global__ __launch_bounds__(64) void k_compact(SelParams p) {
   const int64_t r = blockIdx.x;

@@ -284,7 +284,8 @@ def test_keep_diagonal(gpu, name, param, causal):
 
 
 @pytest.mark.parametrize("causal", [False, True])
-def test_varlen_batch(gpu, causal):
+@pytest.mark.parametrize("mode,param", [("topk", 0.2), ("topp", 0.9), ("mins", 0.5)])
+def test_varlen_batch(gpu, causal, mode, param):
     # Packed sequences (one empty) in one call equal separate calls on each
     # sequence's rows; attention on the packed lists matches the oracle.
     lens = [300, 0, 777, 64, 129]
@@ -292,8 +293,8 @@ def test_varlen_batch(gpu, causal):
     Hq, Hkv, D, block = 4, 2, 128, 64
     q, k, v = synth.planted_case(500 + int(causal), 1, Hq, Hkv, int(cu[-1]), D)
     tq, tk, tv = dev(q), dev(k), dev(v)
-    cap = max(va.max_count(n, block, causal, "topk", 0.2) for n in lens if n)
-    idx, cnt = va.select_varlen(tq, tk, cu, block, "topk", 0.2, causal, cap=cap)
+    cap = max(va.max_count(n, block, causal, mode, param) for n in lens if n)
+    idx, cnt = va.select_varlen(tq, tk, cu, block, mode, param, causal, cap=cap)
     out, lse = va.sparse_attn_varlen(tq, tk, tv, cu, idx, cnt, cap, block, causal, return_lse=True)
     torch.cuda.synchronize()
     nb, first, total = va.varlen_blocks(cu, block)
@@ -303,7 +304,7 @@ def test_varlen_batch(gpu, causal):
         if n == 0:
             continue
         r0, r1 = int(cu[s]), int(cu[s + 1])
-        i_s, c_s = va.select(tq[:, :, r0:r1], tk[:, :, r0:r1], block, "topk", 0.2, causal, cap=cap)
+        i_s, c_s = va.select(tq[:, :, r0:r1], tk[:, :, r0:r1], block, mode, param, causal, cap=cap)
         torch.cuda.synchronize()
         got_i = idx[first[s] * Hq * cap:(first[s] + nb[s]) * Hq * cap].reshape(1, Hq, nb[s], cap)
         got_c = cnt[first[s] * Hq:(first[s] + nb[s]) * Hq].reshape(1, Hq, nb[s])
@@ -316,7 +317,7 @@ def test_varlen_batch(gpu, causal):
         l = lse[Hq * r0:Hq * r1].view(1, Hq, n).cpu().numpy()
         ok = np.isfinite(lse_ref)
         assert np.array_equal(np.isfinite(l), ok)
-        assert np.abs(l[ok] - lse_ref[ok]).max() <= 2e-3
+        assert np.abs(l[ok] - lse_ref[ok]).max() <= 4e-3  # log(1 + 2^-8): bf16 weights in the sum
 
 
 @pytest.mark.parametrize("mode,param", [("topk", 0.1), ("topp", 0.9), ("mins", 0.7)])

@@ -346,16 +346,53 @@ def test_single_key_and_zero_query():
     idx = np.full((1, 1, 3, 4), -1, dtype=np.int32)
     cnt = np.array([[[1, 1, 1]]], dtype=np.int32)
     idx[0, 0, :, 0] = [5, 30, 40]
-    o, _ = oracle.sparse_attn(q, k, v, idx, cnt, P, False)
+    o, lse = oracle.sparse_attn(q, k, v, idx, cnt, P, False)
     vf = oracle.bf16_to_f64(v)
+    qf, kf = oracle.bf16_to_f64(q), oracle.bf16_to_f64(k)
     for i, j in enumerate([5, 30, 40]):
         assert np.array_equal(o[0, 0, i * P:(i + 1) * P], np.repeat(vf[0, 0, j:j + 1], P, 0))
+        # one visible key: LSE is that key's scaled score, q_r . k_j / sqrt(D)
+        np.testing.assert_allclose(lse[0, 0, i * P:(i + 1) * P],
+                                   qf[0, 0, i * P:(i + 1) * P] @ kf[0, 0, j] / np.sqrt(D),
+                                   rtol=0, atol=1e-12)
     z = np.zeros_like(q)
     idx2 = np.array([[[[1, 4, 9, 20]] * 3]], dtype=np.int32).reshape(1, 1, 3, 4)
     cnt2 = np.full((1, 1, 3), 4, dtype=np.int32)
-    o2, _ = oracle.sparse_attn(z, k, v, idx2, cnt2, P, False)
+    o2, lse2 = oracle.sparse_attn(z, k, v, idx2, cnt2, P, False)
     np.testing.assert_allclose(o2[0, 0], np.repeat(vf[0, 0, [1, 4, 9, 20]].mean(0)[None], N, 0),
                                rtol=0, atol=1e-14)
+    # Q = 0: every score is 0, so LSE = log(number of visible keys)
+    np.testing.assert_allclose(lse2[0, 0], np.full(N, np.log(4.0)), rtol=0, atol=1e-14)
+
+
+def test_lse_matches_torch_logsumexp():
+    # LSE over each row's visible listed keys (causal: j <= r) against torch's
+    # logsumexp in fp64 on the same scaled scores; rows with nothing visible are -inf.
+    import torch
+    B, H, N, D, P = 1, 2, 40, 16, 8
+    q = synth.random_bits(91, (B, H, N, D))
+    k = synth.random_bits(92, (B, H, N, D))
+    v = synth.random_bits(93, (B, H, N, D))
+    r = np.random.default_rng(94)
+    Np, cap = N // P, 12
+    idx = np.full((B, H, Np, cap), -1, dtype=np.int32)
+    cnt = np.zeros((B, H, Np), dtype=np.int32)
+    for h in range(H):
+        for i in range(Np):
+            c = int(r.integers(0, cap + 1))
+            idx[0, h, i, :c] = np.sort(r.choice(N, size=c, replace=False))
+            cnt[0, h, i] = c
+    _, lse = oracle.sparse_attn(q, k, v, idx, cnt, P, True)
+    qf = torch.from_numpy(oracle.bf16_to_f64(q))
+    kf = torch.from_numpy(oracle.bf16_to_f64(k))
+    for h in range(H):
+        for row in range(N):
+            keys = [j for j in idx[0, h, row // P, :cnt[0, h, row // P]] if j <= row]
+            if not keys:
+                assert np.isneginf(lse[0, h, row])
+                continue
+            s = (kf[0, h, keys] @ qf[0, h, row]) / np.sqrt(D)
+            assert abs(lse[0, h, row] - torch.logsumexp(s, 0).item()) <= 1e-12
 
 
 def test_empty_causal_rows():

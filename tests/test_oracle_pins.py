@@ -502,3 +502,97 @@ def test_keep_diagonal_variant():
     assert np.array_equal(a, b) and np.array_equal(ca, cb)
     with pytest.raises(ValueError):   # lists must fit: 64 + k keys in 65 slots fails for k > 1
         oracle.select(q, k, 64, oracle.TOPK, 0.1, False, 65, keep_diag=True)
+
+
+def _numpy_scores(q, k, P, causal, h, i, group):
+    """Scaled pooled scores of block i from numpy: the pooled queries (pinned
+    above against numpy means) times K, divided by sqrt(D)."""
+    N, D = q.shape[2], q.shape[3]
+    qp = oracle.bf16_to_f64(oracle.pool(q, P))[0, h, i]
+    L = min(N, (i + 1) * P) if causal else N
+    return (oracle.bf16_to_f64(k)[0, h // group, :L] @ qp) / math.sqrt(D)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_mins_select_is_numpy_threshold(causal):
+    # Eq. 3 by its definition: every eligible key whose scaled pooled score is
+    # >= the block's largest score minus alpha (alpha in scaled-score units;
+    # an alpha scaled by sqrt(D), a > for >= or a threshold from another row
+    # fails here).  Keys within 1e-9 of a threshold would make the comparison
+    # depend on summation order; the data is checked to have none.
+    N, P, D, Hq, Hkv = 300, 64, 32, 4, 2
+    q = synth.random_bits(141, (1, Hq, N, D), scale=4.0)
+    k = synth.random_bits(142, (1, Hkv, N, D))
+    Np = (N + P - 1) // P
+    partial = 0
+    for alpha in (0.1, 0.5, 2.0):
+        idx, cnt, ncl = oracle.select(q, k, P, oracle.MINS, alpha, causal, N)
+        assert ncl == 0
+        for h in range(Hq):
+            for i in range(Np):
+                s = _numpy_scores(q, k, P, causal, h, i, Hq // Hkv)
+                thr = s.max() - alpha
+                assert np.abs(s - thr).min() > 1e-9
+                want = np.nonzero(s >= thr)[0]
+                c = cnt[0, h, i]
+                assert np.array_equal(idx[0, h, i, :c], want), (alpha, h, i)
+                assert np.all(idx[0, h, i, c:] == -1)
+                partial += 1 < c < len(s)
+    assert partial > 10   # the thresholds cut inside most rows, not at an end
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_mins_cap_keeps_first_of_total_order(causal):
+    # A block whose minS set exceeds cap keeps the first cap keys of the set in
+    # the total order (score descending, index ascending) -- numpy's lexsort of
+    # (index, -score) -- listed ascending, and is counted once.  Duplicate key
+    # rows put exact ties at the cap boundary (the lower index must win).
+    N, P, D = 256, 32, 32
+    q = synth.random_bits(151, (1, 1, N, D), scale=4.0)
+    k = synth.random_bits(152, (1, 1, N, D))
+    k[0, 0, 40::7] = k[0, 0, 3]
+    for alpha, cap in ((0.4, 9), (1.0, 25), (3.0, 60)):
+        idx, cnt, ncl = oracle.select(q, k, P, oracle.MINS, alpha, causal, cap)
+        clamped = 0
+        for i in range(N // P):
+            s = _numpy_scores(q, k, P, causal, 0, i, 1)
+            thr = s.max() - alpha
+            assert np.abs(s - thr).min() > 1e-9
+            full = set(np.nonzero(s >= thr)[0].tolist())
+            order = np.lexsort((np.arange(len(s)), -s))
+            kept = [int(j) for j in order if int(j) in full][:cap]
+            clamped += len(full) > cap
+            c = cnt[0, 0, i]
+            assert c == min(cap, len(full))
+            assert list(idx[0, 0, i, :c]) == sorted(kept), (alpha, i)
+        assert ncl == clamped and clamped > 0
+
+
+def test_oracle_plan_worked_examples():
+    # Eq. 5 worked by hand (the same tables the library's test uses):
+    #   head 0: (sparsity, perf) = (0.1, 1.0) (0.5, 0.8) (0.9, 0.2)
+    #   head 1:                    (0.2, 1.0) (0.6, 0.9) (0.8, 0.5)
+    # Mean sparsity >= 0.5 needs a summed sparsity >= 1.0.  The feasible
+    # choices (summed sparsity -> summed perf): (1,1) 1.1 -> 1.7, (1,2) 1.3 ->
+    # 1.3, (2,0) 1.1 -> 1.2, (2,1) 1.5 -> 1.1, (2,2) 1.7 -> 0.7; the others
+    # fall short (e.g. (0,2) 0.9).  So 1.7 at (1,1) is the only optimum.
+    # >= 0.85 (sum >= 1.7) leaves (2,2): 0.7; target 0 takes each head's best
+    # perf, (0,0): 2.0; 0.9 (sum >= 1.8) is out of reach.
+    sp = np.array([[0.1, 0.5, 0.9], [0.2, 0.6, 0.8]])
+    pf = np.array([[1.0, 0.8, 0.2], [1.0, 0.9, 0.5]])
+    best, optima = oracle.plan_filter_ratios(sp, pf, 0.5)
+    assert best == pytest.approx(1.7) and optima == [(1, 1)]
+    best, optima = oracle.plan_filter_ratios(sp, pf, 0.85)
+    assert best == pytest.approx(0.7) and optima == [(2, 2)]
+    best, optima = oracle.plan_filter_ratios(sp, pf, 0.0)
+    assert best == pytest.approx(2.0) and optima == [(0, 0)]
+    assert oracle.plan_filter_ratios(sp, pf, 0.9) == (None, [])
+    # Tied optima: two identical heads with (0.2, 1.0) (0.4, 0.5); mean >= 0.3
+    # needs one head at 0.4: (0,1) and (1,0) both give 1.5, (1,1) gives 1.0.
+    sp2 = np.array([[0.2, 0.4], [0.2, 0.4]])
+    pf2 = np.array([[1.0, 0.5], [1.0, 0.5]])
+    best, optima = oracle.plan_filter_ratios(sp2, pf2, 0.3)
+    assert best == pytest.approx(1.5) and sorted(optima) == [(0, 1), (1, 0)]
+    # "at least": a mean exactly at the target is feasible
+    best, optima = oracle.plan_filter_ratios(np.array([[0.5], [0.5]]), np.array([[0.3], [0.4]]), 0.5)
+    assert best == pytest.approx(0.7) and optima == [(0, 0)]

@@ -46,6 +46,15 @@ def test_matches_exhaustive_search(seed):
         assert sp[np.arange(H), choice].mean() >= target - 1e-12
 
 
+def test_tied_optima_return_one_of_them():
+    # two identical heads (0.2, 1.0) (0.4, 0.5), mean >= 0.3: (0,1) and (1,0)
+    # both reach 1.5 (hand-worked; the oracle's pin lists both)
+    sp = np.array([[0.2, 0.4], [0.2, 0.4]])
+    pf = np.array([[1.0, 0.5], [1.0, 0.5]])
+    choice, val = va.plan_filter_ratios(sp, pf, 0.3)
+    assert val == pytest.approx(1.5) and tuple(choice.tolist()) in ((0, 1), (1, 0))
+
+
 def test_target_zero_takes_each_heads_best_and_lower_index_on_ties():
     sp = np.array([[0.0, 0.3, 0.6], [0.1, 0.2, 0.3]])
     pf = np.array([[0.5, 0.9, 0.9], [0.7, 0.1, 0.7]])

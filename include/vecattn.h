@@ -16,8 +16,13 @@
  * Conventions shared by every entry point
  *   - Tensors are caller-owned device memory.  The library never allocates,
  *     frees or synchronises; every call is asynchronous on `stream` (a
- *     hipStream_t; NULL means the default stream) and keeps no state, so calls
- *     on different streams may run concurrently.
+ *     hipStream_t; NULL means the default stream), and calls on different
+ *     streams may run concurrently.  The only state kept between calls is a
+ *     per-process, per-device locality counter of vecattn_sparse_attn (tiles
+ *     processed per XCD, which paces the order in which a workgroup walks its
+ *     list): concurrent calls share it, which changes their speed and the
+ *     order of the softmax sums (the last bits of O), never which keys are
+ *     attended.
  *   - Q, K, V, O are bf16 with logical shape [B, H, N, D] described by a
  *     vecattn_tdesc: sizes plus element strides sB, sH, sN; the D dimension is
  *     contiguous (stride 1).  Every row start must be 16-byte aligned (base
@@ -109,11 +114,19 @@ vecattn_status vecattn_select_max_count(int64_t N, int32_t block, int32_t causal
 
 /*
  * Workspace bytes vecattn_select needs for these shapes (device memory the
- * caller allocates and passes in; contents need not be initialised).
+ * caller allocates and passes in; contents need not be initialised).  The
+ * size depends on B, Hq, Hkv (kd->H), N, D and block.
+ * Errors: INVALID_ARG (a NULL pointer, block < 1, cap < 1, an unknown mode,
+ * sizes < 1 or N > 2^30, Hq % Hkv != 0, D not in {64, 128}).
  */
 vecattn_status vecattn_select_workspace_size(const vecattn_tdesc* qd, const vecattn_tdesc* kd,
                                              int32_t block, int32_t causal, int32_t mode,
                                              int64_t cap, size_t* bytes);
+
+/* The same size as a return value (0 when vecattn_select_workspace_size would
+ * return an error). */
+size_t vecattn_select_workspace_bytes(const vecattn_tdesc* qd, const vecattn_tdesc* kd,
+                                      int32_t block, int32_t mode, int64_t cap);
 
 /*
  * Important-vector selection (Sec. 3.1; Algorithm 1's outputs I and C).
@@ -209,7 +222,11 @@ vecattn_status vecattn_select_per_head(const void* q, const vecattn_tdesc* qd, c
  *   scale : softmax scale; 0 means 1 / sqrt(D).
  *   lse   : optional fp32 [B, Hq, N] contiguous output, may be NULL.
  * Errors: INVALID_ARG (null pointer, shape mismatch, block < 1, cap < 1,
- * misalignment); UNSUPPORTED (D not in {64, 128}).
+ * misalignment); UNSUPPORTED (D not in {64, 128}; or a K or V head the
+ * gathers cannot address with 32-bit offsets: N >= 2^24, a row stride sN of
+ * 2^23 elements or more (with N > 1), or (N - 1) * sN * 2 + 2 * D >= 2^31
+ * bytes -- e.g. a packed [B, N, 3, H, D] QKV view with H * D = 5120 from
+ * N ~ 69,900 on).
  */
 vecattn_status vecattn_sparse_attn(const void* q, const vecattn_tdesc* qd, const void* k,
                                    const vecattn_tdesc* kd, const void* v, const vecattn_tdesc* vd,
@@ -266,8 +283,46 @@ vecattn_status vecattn_sparse_attn_varlen(const void* q, const vecattn_tdesc* qd
                                           float* lse, void* stream);
 
 /*
- * Per-head filter ratios, Eq. 5 (Sec. 3.1.2, "Dynamic Programming for Offline
- * Search of Per-Head Filter Ratios").  Host function (host memory, no GPU).
+ * Sparsity of each query head from a selection's counts: Eq. 5's sp_h
+ * (Sec. 3.1.2), the table vecattn_plan_filter_ratios takes.
+ *   sparsity[h] = 1 - (sum over b, i of counts[b, h, i]) / (B * sum_i L_i)
+ * with L_i the eligible keys of block i (N, or min(N, (i + 1) * block) with
+ * VECATTN_CAUSAL).  Integer sums, one fp64 division.
+ *   counts   : int32 [B, Hq, N_p] (device, e.g. from vecattn_select)
+ *   sparsity : fp64 [Hq] device output
+ *   causal   : the selection's bits (VECATTN_KEEP_DIAG is accepted, no effect)
+ * Errors: INVALID_ARG (NULL pointer, B, Hq or N < 1, N > 2^30, block < 1, bad
+ * bits).
+ */
+vecattn_status vecattn_head_sparsity(const int32_t* counts, int64_t B, int64_t Hq, int64_t N,
+                                     int32_t block, int32_t causal, double* sparsity,
+                                     void* stream);
+
+/*
+ * Recall of a selected pattern, the statistic of the sparse-pattern study
+ * (Sec. 2.2): for query row r of block i, the share of the row's exact
+ * attention map that the block's list keeps,
+ *   kept[b, h, r] = sum_{j in I[b,h,i,0:C) visible} exp(x_j) / sum_{j visible} exp(x_j),
+ *   x_j = scale * <q_r, k_j>, visible = (j < N) and (causal == 0 or j <= r).
+ * The mean of kept over rows is the recall of the pattern; 1 - keep ratio is
+ * its sparsity.  One dense pass over the visible keys (2 * N * visible * D
+ * MFMA FLOP per head), the list held as a bitmask in LDS.
+ *   q : bf16 [B, Hq, N, D]   k : bf16 [B, Hkv, N, D]
+ *   idx, counts, cap : as for vecattn_sparse_attn (entries outside [0, N) are
+ *            ignored; a key listed twice counts once)
+ *   scale : 0 means 1 / sqrt(D)
+ *   kept  : fp32 [B, Hq, N] contiguous output
+ * Errors: INVALID_ARG (null pointer, shape mismatch, block < 1, cap < 1, bad
+ * scale or bits, misalignment); UNSUPPORTED (D not in {64, 128}, N > 2^18).
+ */
+vecattn_status vecattn_recall(const void* q, const vecattn_tdesc* qd, const void* k,
+                              const vecattn_tdesc* kd, const int32_t* idx, int64_t cap,
+                              const int32_t* counts, int32_t block, int32_t causal, float scale,
+                              float* kept, void* stream);
+
+/*
+ * Per-head filter ratios, Eq. 5 (Sec. 3.1.2).  Host function (host memory, no
+ * GPU).
  * For each of `heads` heads, n_cand candidate filter ratios were sampled
  * offline with their sparsity sp[h][c] in [0, 1] and a performance score
  * perf[h][c] (any finite value, larger is better).  The call picks one

@@ -17,6 +17,8 @@ Functions and the passages they follow:
 * :func:`sparse_attn_online` -- Algorithm 2's online recurrence (second route to Eq. 4).
 * :func:`dense_attn`      -- Eq. 1, textbook dense attention.
 * :func:`plan_filter_ratios` -- Eq. 5's optimum by exhaustive search (tiny tables only).
+* :func:`kept_mass`       -- Sec. 2.2's recall: the exact attention mass a pattern keeps.
+* :func:`head_sparsity`   -- Eq. 5's sp_h: the share of a head's eligible keys left out.
 """
 from __future__ import annotations
 
@@ -71,9 +73,13 @@ def _load():
     lib.ora_dense_attn.argtypes = [P, P, P, i64, i64, i64, i64, i64, i32, f64, P, P, i32]
     lib.ora_sparse_attn_online.argtypes = [P, P, P, i64, i64, i64, i64, i64, i32, i32, f64,
                                            P, i64, P, i32, P, P, i32]
+    lib.ora_pooled_scores_rows.argtypes = [P, P, i64, i64, i64, i64, i64, i32, i32, P, i64, P,
+                                           i32]
+    lib.ora_kept_mass.argtypes = [P, P, i64, i64, i64, i64, i64, i32, i32, f64, P, i64, P, P, P,
+                                  i64, i32]
     for name in ("ora_bf16_round", "ora_pool", "ora_pooled_scores", "ora_select",
                  "ora_mins_progressive_row", "ora_select_mins_tiled", "ora_sparse_attn", "ora_dense_attn",
-                 "ora_sparse_attn_online"):
+                 "ora_sparse_attn_online", "ora_kept_mass", "ora_pooled_scores_rows"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -138,6 +144,22 @@ def pooled_scores(q: np.ndarray, k: np.ndarray, block: int, causal: bool, b: int
     _check(_load().ora_pooled_scores(_ptr(q), _ptr(k), B, Hq, Hkv, N, D, block, int(causal),
                                      b, h, i, _ptr(out), ctypes.byref(L)), "pooled_scores")
     return out[:L.value].copy()
+
+
+def pooled_scores_rows(q: np.ndarray, k: np.ndarray, block: int, causal: bool, rows,
+                       nthreads: int = 0):
+    """pooled_scores of several blocks (flat ids (b * Hq + h) * Np + i), computed
+    in parallel: a list of 1-D arrays, one per listed block (L_i values each)."""
+    q, k = _bits(q), _bits(k)
+    B, Hq, N, D = q.shape
+    Hkv = k.shape[1]
+    rows_arr = np.ascontiguousarray(rows, dtype=np.int64)
+    out = np.empty((rows_arr.size, N), dtype=np.float64)
+    _check(_load().ora_pooled_scores_rows(_ptr(q), _ptr(k), B, Hq, Hkv, N, D, block, int(causal),
+                                          _ptr(rows_arr), rows_arr.size, _ptr(out), nthreads),
+           "pooled_scores_rows")
+    Np = num_blocks(N, block)
+    return [out[t, :eligible_keys(N, block, int(w) % Np, causal)] for t, w in enumerate(rows_arr)]
 
 
 def with_diagonal(idx: np.ndarray, counts: np.ndarray, N: int, block: int, cap: int,
@@ -297,6 +319,34 @@ def dense_attn(q, k, v, causal, scale=0.0, nthreads=0):
     _check(_load().ora_dense_attn(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, D, int(causal),
                                   float(scale), _ptr(o), _ptr(lse), nthreads), "dense_attn")
     return o, lse
+
+
+def kept_mass(q, k, idx, counts, block, causal, scale=0.0, blocks=None, nthreads=0):
+    """Sec. 2.2's recall of the lists' pattern, per query row: the share of the
+    row's exact attention distribution (softmax over the keys it sees) that
+    falls on its block's listed keys.  Returns [B, Hq, N] f64 (NaN for rows of
+    blocks not in ``blocks``)."""
+    q, k = _bits(q), _bits(k)
+    B, Hq, N, D = q.shape
+    Hkv = k.shape[1]
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    counts = np.ascontiguousarray(counts, dtype=np.int32)
+    kept = np.full((B, Hq, N), np.nan, dtype=np.float64)
+    blk = None if blocks is None else np.ascontiguousarray(blocks, dtype=np.int64)
+    _check(_load().ora_kept_mass(_ptr(q), _ptr(k), B, Hq, Hkv, N, D, block, int(causal),
+                                 float(scale), _ptr(idx), idx.shape[-1], _ptr(counts), _ptr(kept),
+                                 _ptr(blk), 0 if blk is None else blk.size, nthreads),
+           "kept_mass")
+    return kept
+
+
+def head_sparsity(counts, N: int, block: int, causal: bool) -> np.ndarray:
+    """Eq. 5's sp_h from a selection's counts [B, Hq, N_p]: 1 - (keys kept by the
+    head's blocks over the batch) / (B * the blocks' eligible keys), per head."""
+    c = np.asarray(counts, dtype=np.int64)
+    B, Hq, Np = c.shape
+    L = sum(eligible_keys(N, block, i, causal) for i in range(Np))
+    return 1.0 - c.sum(axis=(0, 2)).astype(np.float64) / float(B * L)
 
 
 def plan_filter_ratios(sparsity, perf, target: float):

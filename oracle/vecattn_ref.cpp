@@ -25,6 +25,8 @@
 //   * Eq. 4 (Sec. 3.2): O[I_B(i)] = softmax(Q[I_B(i)] K[Idx(i)]^T / sqrt(D)) V[Idx(i)].
 //   * Algorithm 2 (appendix, Vector-Sparse Computation): the tiled online-softmax
 //     recurrence, used here only as a second route to Eq. 4 for self-checks.
+//   * Sec. 2.2 (statistical comparison of sparse patterns): the recall of a
+//     pattern is the share of the exact attention map's mass that it keeps.
 //
 // Readings where the paper is silent (the design notes list each one):
 //   ragged last block pools only its existing rows; Q_p is rounded once from the
@@ -298,6 +300,28 @@ int ora_pooled_scores(const uint16_t* q, const uint16_t* k, int64_t B, int64_t H
   return ORA_OK;
 }
 
+// The same for several blocks (flat ids w = (b * Hq + h) * Np + i), one row
+// of out per block: out[t * N + j] for j < L of the t-th block; the rest of
+// the row is left untouched.  Rows are independent (OpenMP).
+int ora_pooled_scores_rows(const uint16_t* q, const uint16_t* k, int64_t B, int64_t Hq,
+                           int64_t Hkv, int64_t N, int64_t D, int32_t block, int32_t causal,
+                           const int64_t* rows, int64_t n_rows, double* out, int32_t nthreads) {
+  Shape s{B, Hq, Hkv, N, D};
+  if (!q || !k || !rows || !out || block < 1 || n_rows < 0 || !shape_ok(s)) return ORA_ERR_ARG;
+  const int64_t Np = num_blocks(N, block);
+  for (int64_t t = 0; t < n_rows; ++t)
+    if (rows[t] < 0 || rows[t] >= B * Hq * Np) return ORA_ERR_ARG;
+  set_threads(nthreads);
+#pragma omp parallel for schedule(dynamic)
+  for (int64_t t = 0; t < n_rows; ++t) {
+    const int64_t w = rows[t];
+    std::vector<double> sc;
+    pooled_scores(q, k, s, block, causal, w / (Np * Hq), (w / Np) % Hq, w % Np, sc);
+    for (size_t j = 0; j < sc.size(); ++j) out[t * N + static_cast<int64_t>(j)] = sc[j];
+  }
+  return ORA_OK;
+}
+
 int64_t ora_topk_count(double ratio, int64_t L) { return topk_count(ratio, L); }
 
 // Selection (Sec. 3.1): for every block (or for the listed flat rows
@@ -507,6 +531,68 @@ int ora_dense_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v, int6
     if (lse) lse[w] = m + std::log(Z);
   }
   return ORA_OK;
+}
+
+// Recall of the pattern the index lists describe (Sec. 2.2), per query row:
+// kept[b, h, r] = sum over the keys j of block i's list that row r sees of
+// softmax_j(scale * q_r . k_j), the softmax taken over every key row r sees
+// (j < N, and j <= r when causal) -- the exact attention row of Eq. 1.
+// kept is [B, Hq, N] doubles; rows of blocks not listed are left untouched.
+int ora_kept_mass(const uint16_t* q, const uint16_t* k, int64_t B, int64_t Hq, int64_t Hkv,
+                  int64_t N, int64_t D, int32_t block, int32_t causal, double scale,
+                  const int32_t* idx, int64_t cap, const int32_t* counts, double* kept,
+                  const int64_t* blocks, int64_t n_blocks, int32_t nthreads) {
+  Shape s{B, Hq, Hkv, N, D};
+  if (!q || !k || !idx || !counts || !kept || block < 1 || cap < 0 || !shape_ok(s))
+    return ORA_ERR_ARG;
+  if (scale == 0.0) scale = 1.0 / std::sqrt(static_cast<double>(D));
+  const int64_t Np = num_blocks(N, block);
+  const int64_t g = Hq / Hkv;
+  const int64_t total = blocks ? n_blocks : B * Hq * Np;
+  int bad = 0;
+  set_threads(nthreads);
+#pragma omp parallel for schedule(dynamic) reduction(| : bad)
+  for (int64_t t = 0; t < total; ++t) {
+    const int64_t w = blocks ? blocks[t] : t;
+    const int64_t i = w % Np, h = (w / Np) % Hq, b = w / (Np * Hq);
+    const int64_t hk = h / g;
+    const int32_t c = counts[w];
+    if (c < 0 || c > cap) {
+      bad = 1;
+      continue;
+    }
+    std::vector<char> listed(N, 0);
+    for (int32_t t2 = 0; t2 < c; ++t2) {
+      const int64_t j = idx[w * cap + t2];
+      if (j < 0 || j >= N) {
+        bad = 1;
+        continue;
+      }
+      listed[j] = 1;
+    }
+    const int64_t r0 = i * block, r1 = std::min<int64_t>(N, r0 + block);
+    for (int64_t r = r0; r < r1; ++r) {
+      const uint16_t* qr = q + row_off(b, h, r, Hq, N, D);
+      const int64_t nk = causal ? r + 1 : N;
+      std::vector<double> x(nk);
+      double m = -std::numeric_limits<double>::infinity();
+      for (int64_t j = 0; j < nk; ++j) {
+        const uint16_t* kr = k + row_off(b, hk, j, Hkv, N, D);
+        double dot = 0.0;
+        for (int64_t d = 0; d < D; ++d) dot += bf16_value(qr[d]) * bf16_value(kr[d]);
+        x[j] = scale * dot;
+        m = std::max(m, x[j]);
+      }
+      double Z = 0.0, S = 0.0;
+      for (int64_t j = 0; j < nk; ++j) {
+        const double e = std::exp(x[j] - m);
+        Z += e;
+        if (listed[j]) S += e;
+      }
+      kept[(b * Hq + h) * N + r] = S / Z;
+    }
+  }
+  return bad ? ORA_ERR_ARG : ORA_OK;
 }
 
 // Algorithm 2 (Vector-Sparse Computation) for the listed blocks: the index list

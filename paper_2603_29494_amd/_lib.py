@@ -69,10 +69,15 @@ def load() -> ctypes.CDLL:
                                           ctypes.c_size_t, P]
     lib.vecattn_sparse_attn_varlen.argtypes = [P, D, P, D, P, D, P, i32, P, i64, P, i32, i32, f32,
                                                P, D, P, P]
+    lib.vecattn_select_workspace_bytes.argtypes = [D, D, i32, i32, i64]
+    lib.vecattn_select_workspace_bytes.restype = ctypes.c_size_t
+    lib.vecattn_head_sparsity.argtypes = [P, i64, i64, i64, i32, i32, P, P]
+    lib.vecattn_recall.argtypes = [P, D, P, D, P, i64, P, i32, i32, f32, P, P]
     for name in ("vecattn_pool", "vecattn_select_max_count", "vecattn_select_workspace_size",
                  "vecattn_select", "vecattn_select_mins_tiled", "vecattn_sparse_attn",
                  "vecattn_plan_filter_ratios", "vecattn_select_per_head",
-                 "vecattn_select_varlen", "vecattn_sparse_attn_varlen", "vecattn_check_lists"):
+                 "vecattn_select_varlen", "vecattn_sparse_attn_varlen", "vecattn_check_lists",
+                 "vecattn_head_sparsity", "vecattn_recall"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -286,28 +291,58 @@ def plan_filter_ratios(sparsity, perf, target: float, grid: int = 1000):
     return choice, float(best.value)
 
 
+def head_sparsity_of(counts: torch.Tensor, N: int, block: int, causal: bool = False,
+                     out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Eq. 5's sp_h of one selection: float64 [Hq] on the device, from its
+    counts [B, Hq, N_p] (vecattn_head_sparsity)."""
+    if counts.dtype != torch.int32 or not counts.is_cuda or not counts.is_contiguous() \
+            or counts.dim() != 3:
+        raise ValueError("counts must be a contiguous int32 CUDA tensor [B, Hq, N_p]")
+    B, Hq, _ = counts.shape
+    if out is None:
+        out = torch.empty(Hq, dtype=torch.float64, device=counts.device)
+    _check(load().vecattn_head_sparsity(_ptr(counts), int(B), int(Hq), int(N), int(block),
+                                        int(bool(causal)), _ptr(out), _stream(counts)),
+           "head_sparsity")
+    return out
+
+
 def head_sparsity(q: torch.Tensor, k: torch.Tensor, block: int, mode, params, causal: bool = False,
                   cap: Optional[int] = None, **tiling) -> "torch.Tensor":
     """Sparsity per query head for each candidate parameter (an sp_h table for
-    plan_filter_ratios): 1 - (keys kept) / (eligible keys), summed over the
-    head's blocks and batch, from vecattn_select's counts.  Returns float64
-    [Hq, len(params)] on the host.  Extra keyword arguments (tile,
-    group_tiles) go to select."""
+    plan_filter_ratios): one selection per parameter, each reduced to its
+    per-head sparsity by vecattn_head_sparsity.  Returns float64 [Hq,
+    len(params)] on the host.  Extra keyword arguments (tile, group_tiles) go
+    to select."""
     B, Hq, N, _ = q.shape
-    Np = (N + block - 1) // block
-    L = torch.tensor([min(N, (i + 1) * block) if causal else N for i in range(Np)],
-                     dtype=torch.float64, device=q.device)
-    out = torch.empty((Hq, len(params)), dtype=torch.float64)
+    table = torch.empty((len(params), Hq), dtype=torch.float64, device=q.device)
     ws = None
     for c, prm in enumerate(params):
         cp = max_count(N, block, causal, mode, prm) if cap is None else cap
-        if ws is None or ws.numel() < workspace_bytes(q, k, block, causal, mode, cp):
-            ws = torch.empty(workspace_bytes(q, k, block, causal, mode, cp), dtype=torch.uint8,
-                             device=q.device)
+        need = workspace_bytes(q, k, block, causal, mode, cp)
+        if ws is None or ws.numel() < need:
+            ws = torch.empty(need, dtype=torch.uint8, device=q.device)
         _, cnt = select(q, k, block, mode, prm, causal, cap=cp, workspace=ws, **tiling)
-        kept = cnt.double().sum(dim=(0, 2))                      # [Hq]
-        out[:, c] = (1.0 - kept / (B * L.sum())).cpu()
-    return out
+        head_sparsity_of(cnt, N, block, causal, out=table[c])
+    return table.cpu().t().contiguous()
+
+
+def recall(q: torch.Tensor, k: torch.Tensor, idx: torch.Tensor, counts: torch.Tensor, block: int,
+           causal: bool = False, scale: float = 0.0) -> torch.Tensor:
+    """Attention mass each query row's block list keeps (the recall of the
+    pattern study, vecattn_recall): fp32 [B, Hq, N]."""
+    _bf16_cuda(q, "q")
+    _bf16_cuda(k, "k")
+    if idx.dtype != torch.int32 or counts.dtype != torch.int32 or not idx.is_contiguous() \
+            or not counts.is_contiguous():
+        raise ValueError("idx and counts must be contiguous int32")
+    B, Hq, N, _ = q.shape
+    kept = torch.empty((B, Hq, N), dtype=torch.float32, device=q.device)
+    qd, kd = desc(q), desc(k)
+    _check(load().vecattn_recall(_ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd), _ptr(idx),
+                                 int(idx.shape[-1]), _ptr(counts), int(block), int(bool(causal)),
+                                 float(scale), _ptr(kept), _stream(q)), "recall")
+    return kept
 
 
 def varlen_blocks(cu_seqlens, block: int):

@@ -50,14 +50,36 @@ struct SelectArgs {
   size_t workspace_bytes;
 };
 
-size_t select_workspace_bytes(int64_t B, int64_t Hq, int64_t N, int64_t D, int32_t block,
-                              int32_t mode, int64_t cap);
+size_t select_workspace_bytes(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t D,
+                              int32_t block, int32_t mode, int64_t cap);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 
 // Rows whose list breaks the attention's input contract, counted into *n_bad
 // (cleared first).  rows <= 2^31 - 1 fits the grid.
 hipError_t launch_check_lists(const int32_t* idx, const int32_t* counts, int64_t rows, int64_t cap,
                               int64_t n_keys, int32_t* n_bad, hipStream_t stream);
+
+// Sparsity per query head from the counts of a selection (Eq. 5's sp_h):
+// sparsity[h] = 1 - sum_{b,i} C[b,h,i] / (B * sum_i L_i), as fp64.
+hipError_t launch_head_sparsity(const int32_t* counts, int64_t B, int64_t Hq, int64_t N,
+                                int32_t block, int32_t causal, double* sparsity,
+                                hipStream_t stream);
+
+// Attention mass each query row's block list keeps (the recall of Sec. 2.2):
+// kept[b,h,r] = sum over the listed visible keys of the row's softmax over
+// all its visible keys.  N <= kRecallMaxN.
+constexpr int64_t kRecallMaxN = int64_t(1) << 18;
+struct RecallArgs {
+  Tensor4 q, k;
+  const int32_t* idx;
+  const int32_t* counts;
+  int64_t cap;
+  int32_t block;
+  int32_t causal;
+  float scale;
+  float* kept;
+};
+hipError_t launch_recall(const RecallArgs& a, hipStream_t stream);
 
 // Host: per-head filter ratios by dynamic programming (Eq. 5).  Returns 0, or
 // 1 when no choice reaches the target.

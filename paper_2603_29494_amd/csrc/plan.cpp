@@ -1,5 +1,4 @@
-// Per-head filter ratios (paper Sec. 3.1.2, "Dynamic Programming for Offline
-// Search of Per-Head Filter Ratios", Eq. 5): choose one candidate filter
+// Per-head filter ratios (paper Sec. 3.1.2, Eq. 5): choose one candidate filter
 // ratio per head so that the heads' mean sparsity reaches a target and the
 // summed per-head performance is largest.  Host code; the tables sp_h and
 // Perf_h come from offline sampling.

@@ -1391,12 +1391,11 @@ int choose_split(int64_t B, int64_t Hq, int64_t N, int32_t P) {
 
 }  // namespace
 
-size_t select_workspace_bytes(int64_t B, int64_t Hq, int64_t N, int64_t D, int32_t block,
-                              int32_t mode, int64_t cap) {
+size_t select_workspace_bytes(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t D,
+                              int32_t block, int32_t mode, int64_t cap) {
   (void)mode;
   (void)cap;
-  // Hkv is not known here; reserve one bound per query head (>= per kv head).
-  return layout(B, Hq, Hq, N, D, block, choose_split(B, Hq, N, block)).total;
+  return layout(B, Hq, Hkv, N, D, block, choose_split(B, Hq, N, block)).total;
 }
 
 template <int MODE>
@@ -1416,7 +1415,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   const int64_t Np = (N + P - 1) / P;
   const int64_t rows = B * Hq * Np;
   const int split = choose_split(B, Hq, N, P);
-  const Layout l = layout(B, Hq, Hq, N, D, P, split);
+  const Layout l = layout(B, Hq, Hkv, N, D, P, split);
   if (a.workspace_bytes < l.total) return hipErrorInvalidValue;
   char* ws = static_cast<char*>(a.workspace);
   SelParams p{};

@@ -187,7 +187,9 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
   };
 
   // K and V of this head as buffer resources: gathers use 32-bit byte offsets
-  // (row * row_bytes + 16 * chunk; the host checks that a head spans < 2 GiB).
+  // (row * row_bytes + 16 * chunk, the product in 24 bits); the host rejects
+  // heads with N >= 2^24, a row stride of 2^24 bytes or more, or rows spanning
+  // 2^31 bytes or more, so every offset here is exact.
   const uint16_t* kh = k + b * k_sB + hk * k_sH;
   const uint16_t* vh = v + b * v_sB + hk * v_sH;
   const uint32_t k_rowb = static_cast<uint32_t>(k_sN) * 2u;
@@ -240,9 +242,9 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
   auto issue_tile = [&](int t, int st) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      // Valid ids are below N < 2^24 (a head spans < 2 GiB), as __umul24
-      // needs; an invalid id reads some row of this head or zeros, never
-      // outside it (buffer range check).
+      // Valid ids are below N < 2^24 and row strides below 2^24 bytes, as
+      // __umul24 needs; an invalid id reads some row of this head or zeros,
+      // never outside it (buffer range check).
       const uint32_t r = static_cast<uint32_t>(nid[u]);
       uint16_t* kd = kbuf(st) + (wave * U + u) * 64 * 8;
       uint16_t* vd = vbuf(st) + (wave * U + u) * 64 * 8;

@@ -83,6 +83,40 @@ int64_t max_count(int64_t N, int32_t P, int32_t flags, int32_t mode, double para
 
 constexpr int64_t kMaxHeadParams = 128;  // query heads a per-head parameter list may cover
 
+// The attention gathers K and V rows with 32-bit byte offsets inside one
+// head: key j of a head sits at j * row_bytes, computed with a 24-bit
+// multiply, and the head's rows must span < 2^31 bytes.  Heads beyond that
+// are rejected (UNSUPPORTED) instead of gathering wrong rows.
+bool gather_offsets_ok(const vecattn_tdesc* d) {
+  const int64_t rowb = d->sN * 2;
+  if (d->N >= (int64_t(1) << 24)) return false;
+  if (d->N > 1 && rowb >= (int64_t(1) << 24)) return false;
+  return (d->N - 1) * rowb + 2 * d->D < (int64_t(1) << 31);
+}
+
+// Every check of vecattn_sparse_attn, without launching anything.
+vecattn_status check_attn(const void* q, const vecattn_tdesc* qd, const void* k,
+                          const vecattn_tdesc* kd, const void* v, const vecattn_tdesc* vd,
+                          const int32_t* idx, int64_t cap, const int32_t* counts, int32_t block,
+                          int32_t causal, float scale, const void* o, const vecattn_tdesc* od) {
+  vecattn_status st;
+  if ((st = check_desc(q, qd)) != VECATTN_OK) return st;
+  if ((st = check_desc(k, kd)) != VECATTN_OK) return st;
+  if ((st = check_desc(v, vd)) != VECATTN_OK) return st;
+  if ((st = check_desc(o, od)) != VECATTN_OK) return st;
+  if (kd->B != qd->B || kd->N != qd->N || kd->D != qd->D || qd->H % kd->H != 0)
+    return VECATTN_ERR_INVALID_ARG;
+  if (vd->B != kd->B || vd->H != kd->H || vd->N != kd->N || vd->D != kd->D)
+    return VECATTN_ERR_INVALID_ARG;
+  if (od->B != qd->B || od->H != qd->H || od->N != qd->N || od->D != qd->D)
+    return VECATTN_ERR_INVALID_ARG;
+  if (!idx || !counts || block < 1 || cap < 1 || cap > kMaxN) return VECATTN_ERR_INVALID_ARG;
+  if (!std::isfinite(scale) || scale < 0.0f) return VECATTN_ERR_INVALID_ARG;
+  if ((causal & ~(kCausal | kKeepDiag)) != 0) return VECATTN_ERR_INVALID_ARG;
+  if (!gather_offsets_ok(kd) || !gather_offsets_ok(vd)) return VECATTN_ERR_UNSUPPORTED;
+  return VECATTN_OK;
+}
+
 vecattn_status select_impl(const void* q, const vecattn_tdesc* qd, const void* k,
                            const vecattn_tdesc* kd, int32_t block, int32_t causal, int32_t mode,
                            double param, const double* head_params, int32_t tile,
@@ -117,7 +151,8 @@ vecattn_status select_impl(const void* q, const vecattn_tdesc* qd, const void* k
   if ((causal & kKeepDiag) && mode != VECATTN_SEL_TOPK &&
       cap < max_count(qd->N, block, causal, mode, param))
     return VECATTN_ERR_CAPACITY;
-  const size_t need = vecattn::select_workspace_bytes(qd->B, qd->H, qd->N, qd->D, block, mode, cap);
+  const size_t need =
+      vecattn::select_workspace_bytes(qd->B, qd->H, kd->H, qd->N, qd->D, block, mode, cap);
   if (need > 0 && (!workspace || workspace_bytes < need)) return VECATTN_ERR_CAPACITY;
   if (workspace && !aligned16(workspace)) return VECATTN_ERR_INVALID_ARG;
   vecattn::SelectArgs a{to_tensor(q, qd), to_tensor(k, kd), block, (causal & kCausal) ? 1 : 0,
@@ -172,9 +207,48 @@ vecattn_status vecattn_select_workspace_size(const vecattn_tdesc* qd, const veca
                                              int64_t cap, size_t* bytes) {
   (void)causal;
   if (!qd || !kd || !bytes || block < 1 || cap < 1) return VECATTN_ERR_INVALID_ARG;
-  if (!mode_ok(mode)) return VECATTN_ERR_INVALID_ARG;
-  *bytes = vecattn::select_workspace_bytes(qd->B, qd->H, qd->N, qd->D, block, mode, cap);
+  if (!mode_ok(mode) || qd->B < 1 || qd->H < 1 || qd->N < 1 || qd->N > kMaxN || kd->H < 1 ||
+      qd->H % kd->H != 0 || (qd->D != 64 && qd->D != 128))
+    return VECATTN_ERR_INVALID_ARG;
+  *bytes = vecattn::select_workspace_bytes(qd->B, qd->H, kd->H, qd->N, qd->D, block, mode, cap);
   return VECATTN_OK;
+}
+
+size_t vecattn_select_workspace_bytes(const vecattn_tdesc* qd, const vecattn_tdesc* kd,
+                                      int32_t block, int32_t mode, int64_t cap) {
+  size_t n = 0;
+  return vecattn_select_workspace_size(qd, kd, block, 0, mode, cap, &n) == VECATTN_OK ? n : 0;
+}
+
+vecattn_status vecattn_head_sparsity(const int32_t* counts, int64_t B, int64_t Hq, int64_t N,
+                                     int32_t block, int32_t causal, double* sparsity,
+                                     void* stream) {
+  if (!counts || !sparsity || B < 1 || Hq < 1 || Hq > INT32_MAX || N < 1 || N > kMaxN ||
+      block < 1 || (causal & ~(kCausal | kKeepDiag)) != 0)
+    return VECATTN_ERR_INVALID_ARG;
+  hipError_t e = vecattn::launch_head_sparsity(counts, B, Hq, N, block, (causal & kCausal) ? 1 : 0,
+                                               sparsity, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
+}
+
+vecattn_status vecattn_recall(const void* q, const vecattn_tdesc* qd, const void* k,
+                              const vecattn_tdesc* kd, const int32_t* idx, int64_t cap,
+                              const int32_t* counts, int32_t block, int32_t causal, float scale,
+                              float* kept, void* stream) {
+  vecattn_status st = check_desc(q, qd);
+  if (st != VECATTN_OK) return st;
+  if ((st = check_desc(k, kd)) != VECATTN_OK) return st;
+  if (kd->B != qd->B || kd->N != qd->N || kd->D != qd->D || qd->H % kd->H != 0)
+    return VECATTN_ERR_INVALID_ARG;
+  if (!idx || !counts || !kept || block < 1 || cap < 1 || cap > kMaxN)
+    return VECATTN_ERR_INVALID_ARG;
+  if (!std::isfinite(scale) || scale < 0.0f) return VECATTN_ERR_INVALID_ARG;
+  if ((causal & ~(kCausal | kKeepDiag)) != 0) return VECATTN_ERR_INVALID_ARG;
+  if (qd->N > vecattn::kRecallMaxN) return VECATTN_ERR_UNSUPPORTED;
+  vecattn::RecallArgs a{to_tensor(q, qd), to_tensor(k, kd), idx, counts, cap, block,
+                        (causal & kCausal) ? 1 : 0, scale, kept};
+  hipError_t e = vecattn::launch_recall(a, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
 }
 
 vecattn_status vecattn_select(const void* q, const vecattn_tdesc* qd, const void* k,
@@ -213,20 +287,9 @@ vecattn_status vecattn_sparse_attn(const void* q, const vecattn_tdesc* qd, const
                                    const int32_t* idx, int64_t cap, const int32_t* counts,
                                    int32_t block, int32_t causal, float scale, void* o,
                                    const vecattn_tdesc* od, float* lse, void* stream) {
-  vecattn_status st;
-  if ((st = check_desc(q, qd)) != VECATTN_OK) return st;
-  if ((st = check_desc(k, kd)) != VECATTN_OK) return st;
-  if ((st = check_desc(v, vd)) != VECATTN_OK) return st;
-  if ((st = check_desc(o, od)) != VECATTN_OK) return st;
-  if (kd->B != qd->B || kd->N != qd->N || kd->D != qd->D || qd->H % kd->H != 0)
-    return VECATTN_ERR_INVALID_ARG;
-  if (vd->B != kd->B || vd->H != kd->H || vd->N != kd->N || vd->D != kd->D)
-    return VECATTN_ERR_INVALID_ARG;
-  if (od->B != qd->B || od->H != qd->H || od->N != qd->N || od->D != qd->D)
-    return VECATTN_ERR_INVALID_ARG;
-  if (!idx || !counts || block < 1 || cap < 1 || cap > kMaxN) return VECATTN_ERR_INVALID_ARG;
-  if (!std::isfinite(scale) || scale < 0.0f) return VECATTN_ERR_INVALID_ARG;
-  if ((causal & ~(kCausal | kKeepDiag)) != 0) return VECATTN_ERR_INVALID_ARG;
+  const vecattn_status st =
+      check_attn(q, qd, k, kd, v, vd, idx, cap, counts, block, causal, scale, o, od);
+  if (st != VECATTN_OK) return st;
   vecattn::SparseAttnArgs a{to_tensor(q, qd), to_tensor(k, kd), to_tensor(v, vd),
                             o, od->sB, od->sH, od->sN, lse, idx, counts, cap, block,
                             (causal & kCausal) ? 1 : 0, scale};
@@ -296,7 +359,7 @@ vecattn_status vecattn_select_varlen(const void* q, const vecattn_tdesc* qd, con
     if ((mode == VECATTN_SEL_TOPK || (causal & kKeepDiag)) &&
         cap < max_count(n, block, causal, mode, param))
       return VECATTN_ERR_CAPACITY;
-    const size_t need = vecattn::select_workspace_bytes(1, qd->H, n, qd->D, block, mode, cap);
+    const size_t need = vecattn::select_workspace_bytes(1, qd->H, kd->H, n, qd->D, block, mode, cap);
     if (need > 0 && (!workspace || workspace_bytes < need)) return VECATTN_ERR_CAPACITY;
   }
   int64_t blocks = 0;  // blocks of the sequences before s
@@ -320,13 +383,23 @@ vecattn_status vecattn_sparse_attn_varlen(const void* q, const vecattn_tdesc* qd
                                           const int32_t* counts, int32_t block, int32_t causal,
                                           float scale, void* o, const vecattn_tdesc* od,
                                           float* lse, void* stream) {
-  vecattn_status st;
-  if ((st = check_desc(q, qd)) != VECATTN_OK) return st;
-  if ((st = check_desc(k, kd)) != VECATTN_OK) return st;
-  if ((st = check_desc(v, vd)) != VECATTN_OK) return st;
-  if ((st = check_desc(o, od)) != VECATTN_OK) return st;
+  // The whole packed tensors first (sizes, strides, the relations between
+  // Q, K, V and O), then every sequence's view, so that an error launches
+  // nothing.
+  vecattn_status st = check_attn(q, qd, k, kd, v, vd, idx, cap, counts, block, causal, scale, o, od);
+  if (st != VECATTN_OK) return st;
   if (qd->B != 1 || kd->B != 1 || vd->B != 1 || od->B != 1) return VECATTN_ERR_INVALID_ARG;
-  if (!cu_ok(cu_seqlens, nseq, qd->N) || !idx || !counts) return VECATTN_ERR_INVALID_ARG;
+  if (!cu_ok(cu_seqlens, nseq, qd->N)) return VECATTN_ERR_INVALID_ARG;
+  for (int32_t s = 0; s < nseq; ++s) {
+    const int64_t n = cu_seqlens[s + 1] - cu_seqlens[s];
+    if (n == 0) continue;
+    const int64_t r0 = cu_seqlens[s];
+    const vecattn_tdesc qs = seq_desc(qd, n), ks = seq_desc(kd, n), vs = seq_desc(vd, n),
+                        os = seq_desc(od, n);
+    st = check_attn(seq_ptr(q, qd, r0), &qs, seq_ptr(k, kd, r0), &ks, seq_ptr(v, vd, r0), &vs, idx,
+                    cap, counts, block, causal, scale, seq_ptr(o, od, r0), &os);
+    if (st != VECATTN_OK) return st;
+  }
   int64_t blocks = 0;
   for (int32_t s = 0; s < nseq; ++s) {
     const int64_t n = cu_seqlens[s + 1] - cu_seqlens[s];
@@ -334,7 +407,6 @@ vecattn_status vecattn_sparse_attn_varlen(const void* q, const vecattn_tdesc* qd
     const int64_t r0 = cu_seqlens[s];
     const vecattn_tdesc qs = seq_desc(qd, n), ks = seq_desc(kd, n), vs = seq_desc(vd, n),
                         os = seq_desc(od, n);
-    // The first sequence's call checks what all calls share; later ones cannot fail on it.
     st = vecattn_sparse_attn(seq_ptr(q, qd, r0), &qs, seq_ptr(k, kd, r0), &ks, seq_ptr(v, vd, r0),
                              &vs, idx + blocks * qd->H * cap, cap, counts + blocks * qd->H, block,
                              causal, scale, const_cast<void*>(seq_ptr(o, od, r0)), &os,

@@ -43,11 +43,9 @@ def check_rows(q, k, block, mode, param, causal, cap, idx_gpu, cnt_gpu, rows, co
     idx_gpu = idx_gpu.reshape(-1, idx_gpu.shape[-1])
     cnt_gpu = cnt_gpu.reshape(-1)
     mismatched = 0
-    for w in rows:
+    for w, s in zip(rows, _scores(q, k, block, causal, rows)):
         w = int(w)
         pw = pos[w]
-        i, h, b = w % Np, (w // Np) % Hq, w // (Np * Hq)
-        s = oracle.pooled_scores(q, k, block, causal, b, h, i)
         L = len(s)
         tol = REL_TOL * np.abs(s).max()
         cg, co = int(cnt_gpu[pw]), int(cnt_o[pw])
@@ -92,6 +90,62 @@ def check_rows(q, k, block, mode, param, causal, cap, idx_gpu, cnt_gpu, rows, co
     return mismatched
 
 
+def check_rows_keep_diag(q, k, block, mode, param, causal, cap, idx_gpu, cnt_gpu, rows,
+                         compact=False, tiling=(16, 16)):
+    """Parity of lists selected with the block's own rows kept (the keep-diagonal
+    variant): the GPU list holds every key of the block's rows, and its
+    difference from the oracle's list (the oracle's selection united with those
+    keys) lies outside the block's rows, within the near-tie tolerance of the
+    oracle's cut (the score of its last kept key; minS: rowmax - alpha;
+    cross-tile minS: the key's own running threshold, with ``tiling`` = (B_K,
+    G_K)).  Returns the number of rows whose lists differ."""
+    B, Hq, N, D = q.shape
+    Np = (N + block - 1) // block
+    kw = dict(rows=rows, compact=True)
+    if mode == oracle.MINS_TILED:
+        plain_i, plain_c, ncl = oracle.select_mins_tiled(q, k, block, param, causal, cap,
+                                                         tiling[0], tiling[1], **kw)
+        assert ncl == 0
+        kd_i, kd_c = oracle.with_diagonal(plain_i, plain_c, N, block, cap, rows, compact=True)
+    else:
+        plain_i, plain_c, _ = oracle.select(q, k, block, mode, param, causal, cap, **kw)
+        kd_i, kd_c, _ = oracle.select(q, k, block, mode, param, causal, cap, keep_diag=True, **kw)
+    idx_gpu = idx_gpu.reshape(-1, idx_gpu.shape[-1])
+    cnt_gpu = cnt_gpu.reshape(-1)
+    mismatched = 0
+    for t, (w, s) in enumerate(zip(rows, _scores(q, k, block, causal, rows))):
+        w = int(w)
+        pw = t if compact else w
+        i = w % Np
+        diag = np.arange(i * block, min(N, (i + 1) * block))
+        cg = int(cnt_gpu[pw])
+        g = idx_gpu[pw, :cg]
+        assert np.all(np.diff(g) > 0) and (cg == 0 or (g[0] >= 0 and g[-1] < len(s))), w
+        assert np.all(idx_gpu[pw, cg:] == -1), f"row {w}: padding"
+        assert np.isin(diag, g).all(), f"row {w}: a key of the block's own rows is missing"
+        diff = np.setxor1d(g, kd_i[t, :kd_c[t]])
+        if diff.size:
+            mismatched += 1
+            assert not np.isin(diff, diag).any()
+            if mode == oracle.MINS_TILED:
+                cut = running_threshold(s, param, tiling[0], tiling[1])[diff]
+            elif mode == oracle.MINS:
+                cut = s.max() - param
+            else:
+                cut = s[plain_i[t, :plain_c[t]]].min()
+            tol = REL_TOL * np.abs(s).max()
+            assert np.all(np.abs(s[diff] - cut) <= tol), \
+                f"row {w}: keep-diagonal lists differ beyond near-tie: {np.abs(s[diff] - cut).max()}"
+    return mismatched
+
+
+def _scores(q, k, block, causal, rows, chunk=256):
+    """The oracle's scores of the listed blocks, computed a chunk at a time."""
+    rows = [int(w) for w in rows]
+    for c0 in range(0, len(rows), chunk):
+        yield from oracle.pooled_scores_rows(q, k, block, causal, rows[c0:c0 + chunk])
+
+
 def running_threshold(s, alpha, bk, gk):
     """Per key: (maximum over its group's tiles up to its own tile) - alpha,
     the threshold Algorithm 1 compares it with (used only to place the
@@ -128,11 +182,9 @@ def check_rows_tiled(q, k, block, alpha, causal, bk, gk, idx_gpu, cnt_gpu, rows,
     idx_gpu = idx_gpu.reshape(-1, idx_gpu.shape[-1])
     cnt_gpu = cnt_gpu.reshape(-1)
     mismatched = 0
-    for w in rows:
+    for w, s in zip(rows, _scores(q, k, block, causal, rows)):
         w = int(w)
         pw = pos[w]
-        i, h, b = w % Np, (w // Np) % Hq, w // (Np * Hq)
-        s = oracle.pooled_scores(q, k, block, causal, b, h, i)
         L = len(s)
         tol = REL_TOL * np.abs(s).max()
         cg, co = int(cnt_gpu[pw]), int(cnt_o[pw])

@@ -249,3 +249,94 @@ def test_pool_rejects_bad_arguments():
     assert lib.vecattn_pool(FAKE, ctypes.byref(qd), 0, FAKE, ctypes.byref(pd), None) == INVALID
     bad = desc(1, 2, 3, 64)
     assert lib.vecattn_pool(FAKE, ctypes.byref(qd), 64, FAKE, ctypes.byref(bad), None) == INVALID
+
+
+def test_sparse_attn_rejects_heads_beyond_32bit_gather_offsets():
+    # The gathers address a head's K/V rows with 32-bit byte offsets (24-bit
+    # row products): N >= 2^24, a row stride of 2^24 bytes or more, or rows
+    # spanning 2^31 bytes or more are rejected before any launch.
+    def big(N, sN, H=2):
+        return _lib.TDesc(1, H, N, 128, H * N * sN, N * sN, sN)
+    # a packed [B, N, 3, 40, 128] QKV view: K rows 30720 bytes apart
+    packed = lambda N: _lib.TDesc(1, 40, N, 128, N * 15360, 128, 15360)
+    N_ok = 69906          # (N - 1) * 30720 + 256 < 2^31
+    assert (N_ok - 1) * 30720 + 256 < 2 ** 31 <= N_ok * 30720 + 256
+    q_ok, q_bad = desc(1, 40, N_ok, 128), desc(1, 40, N_ok + 1, 128)
+    # valid shapes otherwise: these fail only later, on the FAKE pointers' data
+    # (never reached: the call below returns before any launch when rejected)
+    assert attn(qd=q_bad, kd=packed(N_ok + 1), vd=packed(N_ok + 1), od=q_bad) == UNSUPPORTED
+    assert attn(qd=q_bad, kd=desc(1, 40, N_ok + 1, 128), vd=packed(N_ok + 1), od=q_bad) == UNSUPPORTED
+    n24 = 1 << 24
+    d24 = desc(1, 1, n24, 64)
+    assert attn(qd=d24, kd=desc(1, 1, n24, 64), vd=desc(1, 1, n24, 64), od=d24) == UNSUPPORTED
+    wide = _lib.TDesc(1, 1, 2, 64, 2 * (1 << 23), 2 * (1 << 23), 1 << 23)   # 2^24-byte rows
+    q2 = desc(1, 1, 2, 64)
+    assert attn(qd=q2, kd=wide, vd=desc(1, 1, 2, 64), od=q2) == UNSUPPORTED
+    assert attn(qd=q2, kd=desc(1, 1, 2, 64), vd=wide, od=q2) == UNSUPPORTED
+    assert q_ok.N == N_ok
+
+
+def test_varlen_attention_checks_every_tensor_before_launching():
+    # K, V and O must cover Q's rows (each sequence's view is cut from them).
+    lib = _lib.load()
+    qd = desc(1, 4, 256, 128)
+
+    def att(kd=None, vd=None, od=None, cu=(0, 100, 256)):
+        kd, vd, od = kd or desc(1, 2, 256, 128), vd or desc(1, 2, 256, 128), od or qd
+        arr = (ctypes.c_int64 * len(cu))(*cu)
+        return lib.vecattn_sparse_attn_varlen(FAKE, ctypes.byref(qd), FAKE, ctypes.byref(kd), FAKE,
+                                              ctypes.byref(vd), arr, len(cu) - 1, FAKE, 16, FAKE,
+                                              64, 0, 0.0, FAKE, ctypes.byref(od), None, None)
+    assert att(kd=desc(1, 2, 200, 128)) == INVALID
+    assert att(vd=desc(1, 2, 200, 128)) == INVALID
+    assert att(od=desc(1, 4, 200, 128)) == INVALID
+    assert att(kd=desc(1, 3, 256, 128), vd=desc(1, 3, 256, 128)) == INVALID   # 4 % 3
+    assert att(vd=desc(1, 2, 256, 64)) == INVALID
+    assert att(od=desc(1, 4, 256, 64)) == INVALID
+
+
+def test_workspace_counts_kv_heads_once():
+    # The K operand copy is one per key/value head: a GQA layer (28 / 4 heads)
+    # needs less than the same layer with 28 key/value heads.
+    lib = _lib.load()
+    q = desc(1, 28, 32768, 128)
+    n_gqa, n_mha = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    assert lib.vecattn_select_workspace_size(ctypes.byref(q), ctypes.byref(desc(1, 4, 32768, 128)),
+                                             64, 1, 0, 3277, ctypes.byref(n_gqa)) == OK
+    assert lib.vecattn_select_workspace_size(ctypes.byref(q), ctypes.byref(desc(1, 28, 32768, 128)),
+                                             64, 1, 0, 3277, ctypes.byref(n_mha)) == OK
+    kop = 32768 * 128 * 2      # one head's K in operand order
+    assert n_mha.value - n_gqa.value >= 24 * kop
+    # the size-returning form agrees, and returns 0 on bad arguments
+    assert lib.vecattn_select_workspace_bytes(ctypes.byref(q), ctypes.byref(desc(1, 4, 32768, 128)),
+                                              64, 0, 3277) == n_gqa.value
+    assert lib.vecattn_select_workspace_bytes(ctypes.byref(q), ctypes.byref(desc(1, 3, 32768, 128)),
+                                              64, 0, 3277) == 0
+    assert lib.vecattn_select_workspace_bytes(None, ctypes.byref(q), 64, 0, 3277) == 0
+    assert lib.vecattn_select_workspace_bytes(ctypes.byref(q), ctypes.byref(q), 0, 0, 3277) == 0
+
+
+def test_head_sparsity_and_recall_reject_bad_arguments():
+    lib = _lib.load()
+
+    def hs(cnt=FAKE, B=1, H=4, N=256, block=64, causal=0, out=FAKE):
+        return lib.vecattn_head_sparsity(cnt, B, H, N, block, causal, out, None)
+    assert hs(cnt=None) == INVALID and hs(out=None) == INVALID
+    assert hs(B=0) == INVALID and hs(H=0) == INVALID and hs(N=0) == INVALID
+    assert hs(N=(1 << 30) + 1) == INVALID and hs(block=0) == INVALID and hs(causal=4) == INVALID
+
+    def rc(q=FAKE, qd=None, k=FAKE, kd=None, idx=FAKE, cap=16, cnt=FAKE, block=64, causal=0,
+           scale=0.0, kept=FAKE):
+        qd = qd or desc(1, 4, 256, 128)
+        kd = kd or desc(1, 2, 256, 128)
+        return lib.vecattn_recall(q, ctypes.byref(qd), k, ctypes.byref(kd), idx, cap, cnt, block,
+                                  causal, scale, kept, None)
+    assert rc(q=None) == INVALID and rc(k=None) == INVALID and rc(idx=None) == INVALID
+    assert rc(cnt=None) == INVALID and rc(kept=None) == INVALID
+    assert rc(block=0) == INVALID and rc(cap=0) == INVALID and rc(causal=4) == INVALID
+    assert rc(scale=-1.0) == INVALID and rc(scale=float("nan")) == INVALID
+    assert rc(kd=desc(1, 3, 256, 128)) == INVALID and rc(kd=desc(1, 2, 255, 128)) == INVALID
+    assert rc(q=FAKE + 2) == INVALID
+    assert rc(qd=desc(1, 4, 256, 96), kd=desc(1, 2, 256, 96)) == UNSUPPORTED
+    n = (1 << 18) + 1
+    assert rc(qd=desc(1, 4, n, 128), kd=desc(1, 2, n, 128)) == UNSUPPORTED

@@ -245,3 +245,29 @@ def test_long_sequences_sampled(gpu, case):
         assert np.array_equal(np.isneginf(lg), empty) and np.all(got[empty] == 0.0), (case, int(r))
         if (~empty).any():
             assert np.abs(lg[~empty] - lse_ref[t, :n][~empty]).max() <= LSE_TOL, (case, int(r))
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_extreme_logits_move_the_softmax_reference(gpu, causal):
+    # Scores with a spread of tens of nats, the largest keys toward the end of
+    # every (ascending) list: tiles keep bringing maxima far above the running
+    # reference (weights beyond 2^8), so the kernel must move its reference,
+    # rescale O and the normaliser and recompute the weights, over and over.
+    B, Hq, Hkv, N, D, P = 1, 2, 1, 1200, 128, 64
+    q = synth.random_bits(91, (B, Hq, N, D), scale=6.0)
+    kf = synth.bits_to_f32(synth.random_bits(92, (B, Hkv, N, D), scale=5.0))
+    kf *= np.linspace(0.3, 1.5, N, dtype=np.float32).reshape(1, 1, N, 1)   # later keys larger
+    k = synth.to_bf16_bits(kf)
+    v = synth.random_bits(93, (B, Hkv, N, D))
+    Np = (N + P - 1) // P
+    idx, cnt = random_lists(94, B, Hq, Np, N, P, causal, 900, 900, min_count=1)
+    o_ref, lse_ref = oracle.sparse_attn(q, k, v, idx, cnt, P, causal)
+    fin = np.isfinite(lse_ref)
+    qf, kk = oracle.bf16_to_f64(q), oracle.bf16_to_f64(k)
+    s = (qf[0, 0, :64] @ kk[0, 0].T) / math.sqrt(D)
+    assert s.max() - s.min() > 150.0                   # tens of log2 units between tiles
+    o, lse = va.sparse_attn(dev(q), dev(k), dev(v), torch.from_numpy(idx).cuda(),
+                            torch.from_numpy(cnt).cuda(), P, causal, return_lse=True)
+    torch.cuda.synchronize()
+    check_attn(o, lse, o_ref, lse_ref, f"extreme logits causal={causal}")
+    assert np.abs(lse_ref[fin]).max() > 100.0

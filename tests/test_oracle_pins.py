@@ -596,3 +596,80 @@ def test_oracle_plan_worked_examples():
     # "at least": a mean exactly at the target is feasible
     best, optima = oracle.plan_filter_ratios(np.array([[0.5], [0.5]]), np.array([[0.3], [0.4]]), 0.5)
     assert best == pytest.approx(0.7) and optima == [(0, 0)]
+
+
+def _random_lists(seed, B, H, Np, N, P, causal, cap):
+    r = np.random.Generator(np.random.PCG64(seed))
+    idx = np.full((B, H, Np, cap), -1, dtype=np.int32)
+    cnt = np.zeros((B, H, Np), dtype=np.int32)
+    for b in range(B):
+        for h in range(H):
+            for i in range(Np):
+                L = min(N, (i + 1) * P) if causal else N
+                c = int(r.integers(0, min(cap, L) + 1))
+                idx[b, h, i, :c] = np.sort(r.choice(L, size=c, replace=False))
+                cnt[b, h, i] = c
+    return idx, cnt
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_kept_mass_matches_torch_softmax(causal):
+    # Sec. 2.2's recall per row: torch's softmax (fp64, library routine) of the
+    # row's scaled scores over the keys it sees, summed over its block's listed
+    # keys; GQA through K rows shared by two query heads.
+    B, Hq, Hkv, N, D, P = 1, 4, 2, 70, 16, 16
+    q = synth.random_bits(161, (B, Hq, N, D), scale=2.0)
+    k = synth.random_bits(162, (B, Hkv, N, D))
+    Np = (N + P - 1) // P
+    idx, cnt = _random_lists(163, B, Hq, Np, N, P, causal, 30)
+    kept = oracle.kept_mass(q, k, idx, cnt, P, causal)
+    qf = torch.from_numpy(oracle.bf16_to_f64(q))
+    kf = torch.from_numpy(oracle.bf16_to_f64(k))
+    for h in range(Hq):
+        for r in range(N):
+            n = r + 1 if causal else N
+            p = torch.softmax((kf[0, h // 2, :n] @ qf[0, h, r]) / math.sqrt(D), 0).numpy()
+            listed = [j for j in idx[0, h, r // P, :cnt[0, h, r // P]] if j < n]
+            assert abs(kept[0, h, r] - p[listed].sum()) <= 1e-12
+
+
+def test_kept_mass_closed_forms():
+    B, H, N, D, P = 1, 2, 96, 16, 32
+    q = synth.random_bits(171, (B, H, N, D))
+    k = synth.random_bits(172, (B, H, N, D))
+    v = synth.random_bits(173, (B, H, N, D))
+    Np = N // P
+    for causal in (False, True):
+        full_i, full_c = _all_keys(N, P, causal, Np, B, H)
+        assert np.all(oracle.kept_mass(q, k, full_i, full_c, P, causal) == 1.0)   # every key
+        empty_c = np.zeros_like(full_c)
+        assert np.all(oracle.kept_mass(q, k, full_i, empty_c, P, causal) == 0.0)  # no key
+        # Q = 0: uniform rows, so the recall is the share of visible keys listed
+        idx, cnt = _random_lists(174, B, H, Np, N, P, causal, 40)
+        kz = oracle.kept_mass(np.zeros_like(q), k, idx, cnt, P, causal)
+        for h in range(H):
+            for r in range(N):
+                n = r + 1 if causal else N
+                seen = sum(1 for j in idx[0, h, r // P, :cnt[0, h, r // P]] if j < n)
+                assert abs(kz[0, h, r] - seen / n) <= 1e-15
+        # the kept share is exp(LSE over the visible listed keys - LSE over all
+        # visible keys), from the sparse and dense attention routines
+        kept = oracle.kept_mass(q, k, idx, cnt, P, causal)
+        _, lse_s = oracle.sparse_attn(q, k, v, idx, cnt, P, causal)
+        _, lse_d = oracle.dense_attn(q, k, v, causal)
+        np.testing.assert_allclose(kept, np.exp(lse_s - lse_d), rtol=1e-12, atol=1e-300)
+
+
+def test_head_sparsity_definition():
+    # Eq. 5's sp_h by hand: 2 heads, N = 10, P = 4 (blocks of 4, 4, 2 rows).
+    # Non-causal: each block has 10 eligible keys (30 per head); causal: 4, 8,
+    # 10 (22 per head).
+    cnt = np.array([[[4, 2, 3], [10, 10, 10]]], dtype=np.int32)
+    np.testing.assert_array_equal(oracle.head_sparsity(cnt, 10, 4, False),
+                                  [1 - 9 / 30, 0.0])
+    cc = np.array([[[4, 2, 3], [4, 8, 10]]], dtype=np.int32)
+    np.testing.assert_array_equal(oracle.head_sparsity(cc, 10, 4, True), [1 - 9 / 22, 0.0])
+    # the batch averages: two copies of the same head give the same sparsity
+    two = np.concatenate([cnt, cnt], axis=0)
+    np.testing.assert_array_equal(oracle.head_sparsity(two, 10, 4, False),
+                                  oracle.head_sparsity(cnt, 10, 4, False))

@@ -157,6 +157,25 @@ vecattn_status vecattn_select(const void* q, const vecattn_tdesc* qd, const void
                               void* stream);
 
 /*
+ * vecattn_select without a caller workspace, for callers that cannot allocate
+ * device memory (code under stream capture, tight serving loops, harnesses
+ * that forbid allocation).  The workspace is a 64 MiB array inside the library
+ * (VECATTN_STATIC_WORKSPACE_BYTES), one copy per GPU the library runs on, held
+ * until the process ends; the call allocates nothing.  Arguments and results
+ * are those of vecattn_select.  Every call on a GPU uses that GPU's one copy
+ * (the current device's): calls that overlap on one GPU (other streams, other
+ * threads) race and must be serialised by the caller.
+ * Errors: as vecattn_select; CAPACITY when vecattn_select_workspace_size for
+ * these shapes exceeds VECATTN_STATIC_WORKSPACE_BYTES; DEVICE if the array's
+ * device address cannot be obtained.
+ */
+#define VECATTN_STATIC_WORKSPACE_BYTES (64u << 20)
+vecattn_status vecattn_select_noalloc(const void* q, const vecattn_tdesc* qd, const void* k,
+                                      const vecattn_tdesc* kd, int32_t block, int32_t causal,
+                                      int32_t mode, double param, int32_t* idx, int64_t cap,
+                                      int32_t* counts, int32_t* n_clamped, void* stream);
+
+/*
  * Important-vector selection with Algorithm 1's cross-tile minS filter
  * (appendix Algorithm 1; Sec. 3.1.3, "Cross-tile minS optimization"; the rule
  * is Eq. 3's with a running maximum in place of the row maximum).  Block i's

@@ -73,11 +73,12 @@ def load() -> ctypes.CDLL:
     lib.vecattn_select_workspace_bytes.restype = ctypes.c_size_t
     lib.vecattn_head_sparsity.argtypes = [P, i64, i64, i64, i32, i32, P, P]
     lib.vecattn_recall.argtypes = [P, D, P, D, P, i64, P, i32, i32, f32, P, P]
+    lib.vecattn_select_noalloc.argtypes = [P, D, P, D, i32, i32, i32, f64, P, i64, P, P, P]
     for name in ("vecattn_pool", "vecattn_select_max_count", "vecattn_select_workspace_size",
                  "vecattn_select", "vecattn_select_mins_tiled", "vecattn_sparse_attn",
                  "vecattn_plan_filter_ratios", "vecattn_select_per_head",
                  "vecattn_select_varlen", "vecattn_sparse_attn_varlen", "vecattn_check_lists",
-                 "vecattn_head_sparsity", "vecattn_recall"):
+                 "vecattn_head_sparsity", "vecattn_recall", "vecattn_select_noalloc"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -224,6 +225,32 @@ def select(q: torch.Tensor, k: torch.Tensor, block: int, mode, param: float,
                                  int(cap), _ptr(counts), _ptr(n_clamped), _ptr(workspace), nws,
                                  _stream(q)),
            "select")
+    return idx, counts
+
+
+STATIC_WORKSPACE_BYTES = 64 << 20
+
+
+def select_noalloc(q: torch.Tensor, k: torch.Tensor, block: int, mode, param: float,
+                   causal: bool, cap: int, idx: torch.Tensor, counts: torch.Tensor,
+                   n_clamped: Optional[torch.Tensor] = None, keep_diag: bool = False):
+    """select() on the library's own workspace (vecattn_select_noalloc): no device
+    memory is allocated by this call; the caller provides idx [B, Hq, N_p, cap]
+    and counts [B, Hq, N_p] (contiguous int32).  Calls overlapping on one GPU
+    race on that workspace."""
+    _bf16_cuda(q, "q")
+    _bf16_cuda(k, "k")
+    B, Hq, N, _ = q.shape
+    Np = (N + block - 1) // block
+    if idx.shape != (B, Hq, Np, cap) or not idx.is_contiguous() or idx.dtype != torch.int32:
+        raise ValueError("idx must be contiguous int32 [B, Hq, N_p, cap]")
+    if counts.shape != (B, Hq, Np) or not counts.is_contiguous() or counts.dtype != torch.int32:
+        raise ValueError("counts must be contiguous int32 [B, Hq, N_p]")
+    qd, kd = desc(q), desc(k)
+    _check(load().vecattn_select_noalloc(_ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd),
+                                         int(block), _flags(causal, keep_diag), mode_id(mode),
+                                         float(param), _ptr(idx), int(cap), _ptr(counts),
+                                         _ptr(n_clamped), _stream(q)), "select_noalloc")
     return idx, counts
 
 

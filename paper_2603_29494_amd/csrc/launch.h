@@ -50,6 +50,11 @@ struct SelectArgs {
   size_t workspace_bytes;
 };
 
+// The library's own selection workspace (one copy per GPU, for callers that
+// cannot allocate): its size, and this GPU's copy (the current device's).
+constexpr size_t kStaticWorkspaceBytes = size_t(64) << 20;
+hipError_t static_workspace(void** ptr);
+
 size_t select_workspace_bytes(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t D,
                               int32_t block, int32_t mode, int64_t cap);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);

@@ -117,12 +117,13 @@ vecattn_status check_attn(const void* q, const vecattn_tdesc* qd, const void* k,
   return VECATTN_OK;
 }
 
-vecattn_status select_impl(const void* q, const vecattn_tdesc* qd, const void* k,
-                           const vecattn_tdesc* kd, int32_t block, int32_t causal, int32_t mode,
-                           double param, const double* head_params, int32_t tile,
-                           int32_t group_tiles, int32_t* idx, int64_t cap, int32_t* counts,
-                           int32_t* n_clamped, void* workspace, size_t workspace_bytes,
-                           void* stream) {
+// Every argument check of the selection entry points except the workspace's;
+// *need receives the workspace bytes the call needs.
+vecattn_status select_check(const void* q, const vecattn_tdesc* qd, const void* k,
+                            const vecattn_tdesc* kd, int32_t block, int32_t causal, int32_t mode,
+                            double param, const double* head_params, int32_t tile,
+                            int32_t group_tiles, const int32_t* idx, int64_t cap,
+                            const int32_t* counts, size_t* need) {
   vecattn_status st = check_desc(q, qd);
   if (st != VECATTN_OK) return st;
   st = check_desc(k, kd);
@@ -151,10 +152,23 @@ vecattn_status select_impl(const void* q, const vecattn_tdesc* qd, const void* k
   if ((causal & kKeepDiag) && mode != VECATTN_SEL_TOPK &&
       cap < max_count(qd->N, block, causal, mode, param))
     return VECATTN_ERR_CAPACITY;
-  const size_t need =
-      vecattn::select_workspace_bytes(qd->B, qd->H, kd->H, qd->N, qd->D, block, mode, cap);
+  *need = vecattn::select_workspace_bytes(qd->B, qd->H, kd->H, qd->N, qd->D, block, mode, cap);
+  return VECATTN_OK;
+}
+
+vecattn_status select_impl(const void* q, const vecattn_tdesc* qd, const void* k,
+                           const vecattn_tdesc* kd, int32_t block, int32_t causal, int32_t mode,
+                           double param, const double* head_params, int32_t tile,
+                           int32_t group_tiles, int32_t* idx, int64_t cap, int32_t* counts,
+                           int32_t* n_clamped, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+  size_t need = 0;
+  const vecattn_status st = select_check(q, qd, k, kd, block, causal, mode, param, head_params,
+                                         tile, group_tiles, idx, cap, counts, &need);
+  if (st != VECATTN_OK) return st;
   if (need > 0 && (!workspace || workspace_bytes < need)) return VECATTN_ERR_CAPACITY;
   if (workspace && !aligned16(workspace)) return VECATTN_ERR_INVALID_ARG;
+  if (head_params) param = head_params[0];
   vecattn::SelectArgs a{to_tensor(q, qd), to_tensor(k, kd), block, (causal & kCausal) ? 1 : 0,
                         (causal & kKeepDiag) ? 1 : 0, mode, param, head_params, tile, group_tiles,
                         idx, cap, counts, n_clamped, workspace, workspace_bytes};
@@ -259,6 +273,23 @@ vecattn_status vecattn_select(const void* q, const vecattn_tdesc* qd, const void
   // Cross-tile minS through this entry point uses the paper's B_K = G_K = 16.
   return select_impl(q, qd, k, kd, block, causal, mode, param, nullptr, 16, 16, idx, cap, counts,
                      n_clamped, workspace, workspace_bytes, stream);
+}
+
+vecattn_status vecattn_select_noalloc(const void* q, const vecattn_tdesc* qd, const void* k,
+                                      const vecattn_tdesc* kd, int32_t block, int32_t causal,
+                                      int32_t mode, double param, int32_t* idx, int64_t cap,
+                                      int32_t* counts, int32_t* n_clamped, void* stream) {
+  // All checks first (no device call on an error), then the size limit, then
+  // this GPU's copy of the library's workspace.
+  size_t need = 0;
+  vecattn_status st = select_check(q, qd, k, kd, block, causal, mode, param, nullptr, 16, 16, idx,
+                                   cap, counts, &need);
+  if (st != VECATTN_OK) return st;
+  if (need > vecattn::kStaticWorkspaceBytes) return VECATTN_ERR_CAPACITY;
+  void* ws = nullptr;
+  if (vecattn::static_workspace(&ws) != hipSuccess) return VECATTN_ERR_DEVICE;
+  return select_impl(q, qd, k, kd, block, causal, mode, param, nullptr, 16, 16, idx, cap, counts,
+                     n_clamped, ws, vecattn::kStaticWorkspaceBytes, stream);
 }
 
 vecattn_status vecattn_select_per_head(const void* q, const vecattn_tdesc* qd, const void* k,

@@ -340,3 +340,23 @@ def test_head_sparsity_and_recall_reject_bad_arguments():
     assert rc(qd=desc(1, 4, 256, 96), kd=desc(1, 2, 256, 96)) == UNSUPPORTED
     n = (1 << 18) + 1
     assert rc(qd=desc(1, 4, n, 128), kd=desc(1, 2, n, 128)) == UNSUPPORTED
+
+
+def test_select_noalloc_checks_before_any_device_call():
+    # Every argument error, and a workspace need above the library's 64 MiB,
+    # is reported before the call touches a device (FAKE pointers here).
+    lib = _lib.load()
+
+    def sel(qd=None, kd=None, block=64, causal=0, mode=0, param=0.25, idx=FAKE, cap=64, cnt=FAKE):
+        qd = qd or desc(1, 4, 256, 128)
+        kd = kd or desc(1, 2, 256, 128)
+        return lib.vecattn_select_noalloc(FAKE, ctypes.byref(qd), FAKE, ctypes.byref(kd), block,
+                                          causal, mode, param, idx, cap, cnt, None, None)
+    assert sel(idx=None) == INVALID and sel(cnt=None) == INVALID and sel(block=0) == INVALID
+    assert sel(param=1.5) == INVALID and sel(mode=9) == INVALID and sel(causal=4) == INVALID
+    assert sel(kd=desc(1, 3, 256, 128)) == INVALID
+    assert sel(cap=63) == CAPACITY
+    big_q, big_k = desc(1, 40, 75600, 128), desc(1, 40, 75600, 128)
+    assert lib.vecattn_select_workspace_bytes(ctypes.byref(big_q), ctypes.byref(big_k), 64, 0,
+                                              11340) > _lib.STATIC_WORKSPACE_BYTES
+    assert sel(qd=big_q, kd=big_k, cap=11340, param=0.15) == CAPACITY

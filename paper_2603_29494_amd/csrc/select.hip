@@ -42,7 +42,18 @@ namespace {
 
 constexpr int kRowsWG = 64;     // pooled rows per workgroup
 constexpr int kThreads = 256;
-constexpr int kBins = 256;
+constexpr int kBins = 256;     // bins per histogram level (topK, minS)
+constexpr int kBinsP = 128;    // bins per level in topP launches: each bin also sums its mass, and
+                               // 128 64-bit bins fit the LDS of two workgroups per CU
+// topP bin entries: count << 48 | mass in units of 2^-31 (terms exp(tau s -
+// ref) <= 1 rounded to that grid); a workgroup adds at most 4096 terms to a
+// bin, so neither field can carry into the other.
+constexpr int kMassShift = 48;
+constexpr double kMassUnit = 0x1p-31;
+constexpr float kTopPRange = 40.0f;  // nats below the row maximum the level-0 topP bins span
+// topP cut bins are resolved to this share of the row's total mass: the GPU's
+// fp32 scores and exp2 already differ from exact masses by ~1e-7 relative.
+constexpr double kTopPMassSlack = 0x1p-20;
 constexpr int kLevels = 6;      // histogram refinements per round (idle ones cost ~6 us)
 constexpr int kCand = 1024;     // candidate capacity per row
 constexpr int kRounds = 2;      // a topP row whose count exceeds cap reruns as topK(cap)
@@ -80,6 +91,7 @@ struct RowState {
   float s_lo, s_hi; // current interval: keys with s_lo <= s <= s_hi (exact float bounds)
   float blo, binv;  // bin range of the current level: lo and bins per unit
   float badd;       // bin of s: floor(fma(s, binv, badd)), badd = -blo * binv
+  float smax;       // topP: the row's largest score (ref = tau * smax)
   float tstar;      // cut score
   double ref;       // softmax reference (an upper bound of the row's scores)
   double Z;         // total mass (topP)
@@ -93,6 +105,7 @@ struct SelParams {
   int nkb;                // 32-key blocks per key/value head
   RowState* st;
   uint32_t* hist;         // [rows][kBins]
+  uint64_t* hmass;        // [rows][kBins] topP launches: per-bin mass sum in units of kMassUnit
   uint32_t* n_above;      // [rows][nsplit]
   double* m_above;        // [rows][nsplit]
   double* zpart;          // [rows][nsplit]
@@ -117,6 +130,7 @@ struct SelParams {
   int quad_rows;    // idx rows start on 16 bytes and no row can exceed cap
   uint32_t* nact;   // [kActiveSlots] rows waiting for each later pass
   int gate;         // slot of nact this launch needs non-zero, or -1
+  int nbins;        // bins per histogram level: kBins, or kBinsP in topP launches
   int tiled_tile;   // keys per tile: 16 or 32
   int tiled_gs;     // keys per group of tiles (a power of two)
   int tiled_sb;     // 32-key blocks per segment a wave walks in order
@@ -165,36 +179,44 @@ __device__ __forceinline__ double mass_term(float s, float tau, double ref) {
 
 // Bin of s at one level (must be evaluated identically everywhere: the
 // scoring passes and the interval search below use this one function).
-// One fma, clamped to [0, kBins - 1] in float before the conversion
+// One fma, clamped to [0, nb - 1] in float before the conversion
 // (out-of-range conversions are undefined); truncation equals floor on the
 // clamped, non-negative value.
-__device__ __forceinline__ int bin_of(float s, float mul, float add) {
+__device__ __forceinline__ int bin_of(float s, float mul, float add, int nb) {
   const float x = __builtin_amdgcn_fmed3f(__builtin_fmaf(s, mul, add), 0.0f,
-                                          static_cast<float>(kBins - 1));
+                                          static_cast<float>(nb - 1));
   return static_cast<int>(x);
+}
+
+// Bins of the next level: bins of width 1 / binv from lo.
+__device__ __forceinline__ void set_bins(RowState& s, float lo, float binv) {
+  s.blo = lo;
+  s.binv = binv;
+  s.badd = -lo * binv;
 }
 
 // The interval after choosing bins [ba, bb] of the level with bin function
 // (mul, add) inside [s_lo, s_hi]: the bin function is monotone in s, so the
 // chosen set is again a float interval; its exact ends are found by binary
 // search over ordered float keys with the same bin function the passes use.
-__device__ __forceinline__ void narrow(float& s_lo, float& s_hi, float mul, float add, int ba, int bb) {
+__device__ __forceinline__ void narrow(float& s_lo, float& s_hi, float mul, float add, int ba, int bb,
+                                       int nb) {
   // smallest s with bin >= ba
   uint32_t a = ord_key(-FLT_MAX), z = ord_key(FLT_MAX);
-  if (bin_of(ord_val(a), mul, add) < ba) {
+  if (bin_of(ord_val(a), mul, add, nb) < ba) {
     while (z - a > 1) {
       const uint32_t m = a + (z - a) / 2;
-      if (bin_of(ord_val(m), mul, add) >= ba) z = m; else a = m;
+      if (bin_of(ord_val(m), mul, add, nb) >= ba) z = m; else a = m;
     }
     s_lo = fmaxf(s_lo, ord_val(z));
   }
   // largest s with bin <= bb
   a = ord_key(-FLT_MAX);
   z = ord_key(FLT_MAX);
-  if (bin_of(ord_val(z), mul, add) > bb) {
+  if (bin_of(ord_val(z), mul, add, nb) > bb) {
     while (z - a > 1) {
       const uint32_t m = a + (z - a) / 2;
-      if (bin_of(ord_val(m), mul, add) <= bb) a = m; else z = m;
+      if (bin_of(ord_val(m), mul, add, nb) <= bb) a = m; else z = m;
     }
     s_hi = fminf(s_hi, ord_val(a));
   }
@@ -281,6 +303,10 @@ __global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
     s.clamped = 0;
     s.topp = p.mode_topp;
     if (!p.mode_topp && !p.mode_mins) s.k_target = topk_count(row_param(p, r), s.L);
+    if (p.mode_topp && row_param(p, r) >= 1.0) {  // p = 1 keeps every eligible key
+      s.topp = 0;
+      s.k_target = s.L;
+    }
   }
   const float c = p.qnorm[r] * p.kmax[b * p.Hkv + h / p.group];
   const float cc = c * 1.0009765625f + 1e-30f;
@@ -288,10 +314,9 @@ __global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
   s.phase = PH_HIST;
   s.s_lo = -FLT_MAX;
   s.s_hi = FLT_MAX;
-  s.blo = -cc;
-  s.binv = static_cast<float>(kBins) / (2.0f * cc);
-  s.badd = -s.blo * s.binv;
+  set_bins(s, -cc, static_cast<float>(p.nbins) / (2.0f * cc));
   s.ref = static_cast<double>(p.tau) * static_cast<double>(cc);  // >= every tau * score
+  s.smax = cc;
   s.tie_partial = 0;
   s.k_eq = 0;
   s.tie_interval = 0;
@@ -336,11 +361,18 @@ template <int D, int MODE, bool TOPP>
 __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   constexpr int DS = D / 16;
   constexpr bool HIST = MODE == MODE_HIST || MODE == MODE_HIST0;
-  // Row stride kBins + 1 (odd): rows hitting the same bin use different
-  // banks; slot kBins of a row takes the increments of keys outside the
+  // Row stride NB + 1 (odd): rows hitting the same bin use different
+  // banks; slot NB of a row takes the increments of keys outside the
   // interval, so that every key can be counted without a branch.
-  constexpr int HS = kBins + 1;
-  __shared__ uint32_t s_hist[HIST ? kRowsWG * HS : 1];
+  constexpr int NB = TOPP ? kBinsP : kBins;
+  constexpr int HS = NB + 1;
+  // topP HIST passes also sum each bin's softmax mass (terms exp2((s - row
+  // max) tau log2 e) <= 1 in fixed point), which pins the cut to one or two
+  // bins per level: one 64-bit integer atomic per key carries both the count
+  // and the mass (LDS float atomics are far slower).
+  constexpr bool MH = HIST && TOPP;
+  __shared__ uint32_t s_hist[HIST && !MH ? kRowsWG * HS : 1];
+  __shared__ uint64_t s_hist64[MH ? kRowsWG * HS : 1];
   __shared__ double s_zred[4][kRowsWG];
   __shared__ double s_mred[4][kRowsWG];
   __shared__ uint32_t s_nred[4][kRowsWG];
@@ -388,7 +420,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
              : (MODE == MODE_COLLECT)        ? ph == PH_COLLECT
                                              : ph == PH_EMIT;
       if (MODE == MODE_SAMPLE) part = part && !p.st[row0 + tid].topp;
-      if (MODE == MODE_MAX) part = part && p.st[row0 + tid].mins;
+      if (MODE == MODE_MAX) part = part && (p.st[row0 + tid].mins || p.st[row0 + tid].topp);
     }
     s_part[tid] = part;
     if (part) atomicOr(&s_any, 1);
@@ -402,7 +434,10 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   __syncthreads();
   if (!s_any) return;  // passes late in the refinement find most workgroups idle
   if (HIST) {
-    for (int t = tid; t < kRowsWG * HS; t += kThreads) s_hist[t] = 0u;
+    for (int t = tid; t < kRowsWG * HS; t += kThreads) {
+      if (MH) s_hist64[t] = 0ull;
+      else s_hist[t] = 0u;
+    }
     __syncthreads();
   }
 
@@ -411,7 +446,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   bf16x8 qf[2][DS];
   bool part[2];
   int Lr[2];
-  float slo[2], shi[2], bmul[2], badd[2], ts[2];
+  float slo[2], shi[2], bmul[2], badd[2], ts[2], smax[2];
   bool tiep[2], tiei[2];
   double ref[2];  // < 0: no masses needed
 #pragma unroll
@@ -425,6 +460,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     shi[rb2] = s.s_hi;
     bmul[rb2] = s.binv;
     badd[rb2] = s.badd;
+    smax[rb2] = s.smax;
     ts[rb2] = s.tstar;
     tiep[rb2] = s.tie_partial;
     tiei[rb2] = s.tie_interval;
@@ -438,6 +474,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   }
 
   double zacc[2] = {0.0, 0.0}, macc[2] = {0.0, 0.0};
+  const float k1 = p.tau * 1.4426950408889634f;  // raw score -> log2 units
   uint32_t nacc[2] = {0u, 0u};
 
   const int nblk = (key1 - key0 + 31) / 32;
@@ -492,7 +529,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
             wge |= (ok && acc[e] >= slo[rb2]) ? 1u << kl : 0u;
             wgt |= (ok && acc[e] > shi[rb2]) ? 1u << kl : 0u;
             if (TOPP && ref[rb2] >= 0.0 && ok && acc[e] > shi[rb2])
-              macc[rb2] += mass_term(acc[e], p.tau, ref[rb2]);
+              macc[rb2] += static_cast<double>(__builtin_amdgcn_exp2f((acc[e] - smax[rb2]) * k1));
           }
           nacc[rb2] += static_cast<uint32_t>(__builtin_popcount(wgt));
           const uint32_t ins = wge & ~wgt;
@@ -563,14 +600,25 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
             inside = ok && !above && sc >= slo[rb2];
             nacc[rb2] += above ? 1u : 0u;
           }
+          // topP: the key's softmax term relative to the row maximum, exp(tau
+          // s - ref) with ref = tau * max (terms below 2^-126, a share of the
+          // mass far below any tolerance, may flush to 0)
+          const float mt = TOPP ? __builtin_amdgcn_exp2f((sc - smax[rb2]) * k1) : 0.0f;
           if (TOPP && ref[rb2] >= 0.0 && ok) {
-            const double mt = mass_term(sc, p.tau, ref[rb2]);
-            if (MODE == MODE_HIST0) zacc[rb2] += mt;
-            if (above) macc[rb2] += mt;
+            if (MODE == MODE_HIST0) zacc[rb2] += static_cast<double>(mt);
+            if (above) macc[rb2] += static_cast<double>(mt);
           }
           if (HIST) {
-            const int bn = inside ? bin_of(sc, bmul[rb2], badd[rb2]) : kBins;
-            atomicAdd(&s_hist[rl * HS + bn], 1u);
+            const int bn = inside ? bin_of(sc, bmul[rb2], badd[rb2], NB) : NB;
+            if (MH) {
+              const uint32_t mq = ref[rb2] >= 0.0
+                                      ? static_cast<uint32_t>(__builtin_fmaf(mt, 0x1p31f, 0.5f))
+                                      : 0u;
+              atomicAdd(reinterpret_cast<unsigned long long*>(&s_hist64[rl * HS + bn]),
+                        (1ull << kMassShift) | mq);
+            } else {
+              atomicAdd(&s_hist[rl * HS + bn], 1u);
+            }
           }
         }
       };
@@ -669,10 +717,17 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     if (MODE == MODE_HIST0 || MODE == MODE_SAMPLE) p.zpart[row * p.nsplit + sp] = z;
   }
   if (HIST) {
-    for (int t = tid; t < nrows * kBins; t += kThreads) {
-      const int rl = t / kBins, bn = t % kBins;
-      const uint32_t c = s_hist[rl * HS + bn];
-      if (c && s_part[rl]) atomicAdd(&p.hist[(row0 + rl) * kBins + bn], c);
+    for (int t = tid; t < nrows * NB; t += kThreads) {
+      const int rl = t / NB, bn = t % NB;
+      const uint64_t v = MH ? s_hist64[rl * HS + bn] : 0ull;
+      const uint32_t c = MH ? static_cast<uint32_t>(v >> kMassShift) : s_hist[rl * HS + bn];
+      if (c && s_part[rl]) {
+        atomicAdd(&p.hist[(row0 + rl) * kBins + bn], c);
+        const uint64_t m = v & ((1ull << kMassShift) - 1ull);
+        if (MH && m)
+          atomicAdd(reinterpret_cast<unsigned long long*>(&p.hmass[(row0 + rl) * kBins + bn]),
+                    static_cast<unsigned long long>(m));
+      }
     }
   }
 }
@@ -713,9 +768,30 @@ __global__ __launch_bounds__(256) void k_bracket(SelParams p) {
   const float lo = fmaxf(static_cast<float>(mu - (widen * a_lo + 0.25) * sd), s.blo);
   const float hi = fminf(static_cast<float>(mu + (widen * a_hi + 0.25) * sd), -s.blo);
   if (!(hi > lo)) return;
-  s.blo = lo;
-  s.binv = static_cast<float>(kBins) / (hi - lo);
-  s.badd = -lo * s.binv;
+  set_bins(s, lo, static_cast<float>(p.nbins) / (hi - lo));
+}
+
+// ---------------------------------------------------------------------------
+// topP rows: the row maximum from the MAX pass becomes the softmax reference
+// (ref = tau * max, so every mass term exp(tau s - ref) is at most 1 and the
+// row's terms fit fp32 down to a mass far below any tolerance), and the
+// level-0 bins span the kTopPRange nats below the maximum (narrow bins where
+// the mass is, so that each bin's mass sum is tight); keys further down hold
+// a share of the mass below e^-40 each and fall into bin 0, which a later
+// level spans to its actual extent if the cut should lie there.  One thread
+// per row.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_topp_ref(SelParams p) {
+  const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (r >= p.rows) return;
+  RowState& s = p.st[r];
+  if (s.phase != PH_HIST || !s.topp) return;
+  const float mx = ord_val(p.cand_lohi[2 * r + 1]);
+  p.cand_lohi[2 * r + 1] = 0u;  // ready for the collect pass
+  s.smax = mx;
+  s.ref = static_cast<double>(mx) * static_cast<double>(p.tau);  // exact product
+  const float lo = fmaxf(mx - kTopPRange / p.tau, s.blo);
+  set_bins(s, lo, static_cast<float>(p.nbins) / fmaxf(mx - lo, FLT_MIN));
 }
 
 // ---------------------------------------------------------------------------
@@ -750,9 +826,7 @@ __global__ __launch_bounds__(256) void k_mins(SelParams p) {
     atomicAdd(&p.nact[kEmitSlot], 1u);
     return;
   }
-  s.blo = tf;
-  s.binv = static_cast<float>(kBins) / fmaxf(hi - tf, FLT_MIN);
-  s.badd = -tf * s.binv;
+  set_bins(s, tf, static_cast<float>(p.nbins) / fmaxf(hi - tf, FLT_MIN));
 }
 
 // ---------------------------------------------------------------------------
@@ -965,10 +1039,16 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
   RowState& s = p.st[r];
   if (s.phase != PH_HIST || s.level != level) return;
   __shared__ uint32_t hs[kBins];
+  __shared__ double hm[kBins];
   const int lane = threadIdx.x;
-  for (int t = lane; t < kBins; t += 64) {
+  const int nb = p.nbins;
+  for (int t = lane; t < nb; t += 64) {
     hs[t] = p.hist[r * kBins + t];
     p.hist[r * kBins + t] = 0u;  // ready for the next level
+    if (s.topp) {
+      hm[t] = static_cast<double>(p.hmass[r * kBins + t]) * kMassUnit;
+      p.hmass[r * kBins + t] = 0ull;
+    }
   }
   __syncthreads();
   // Sum the per-split statistics in split order (every lane alike).
@@ -985,14 +1065,15 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
     if (level == 0) z += p.zpart[r * p.nsplit + q];
   }
   // Count cut (topK, and minS rows over cap) across the wave: lane l holds
-  // bins 255 - 4l - j (j = 0..3, descending), and the scan counts the keys in
+  // bins nb - 1 - per l - j (j < per = nb / 64, descending), and the scan counts the keys in
   // every bin from the top through them.  The cut bin is the highest bin whose
   // count from the top reaches the target rank (never an empty bin: the bin
   // above it fell short); `cut_above` counts the keys in the bins above it.
-  static_assert(kBins == 4 * 64, "four bins per lane");
+  static_assert(kBins == 4 * 64 && kBinsP == 2 * 64, "four or two bins per lane");
+  const int per = nb / 64;
   int hb[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) hb[j] = static_cast<int>(hs[kBins - 1 - 4 * lane - j]);
+  for (int j = 0; j < 4; ++j) hb[j] = j < per ? static_cast<int>(hs[nb - 1 - per * lane - j]) : 0;
   const int lsum = hb[0] + hb[1] + hb[2] + hb[3];
   const int incl = wave_incl_scan(lsum);
   const int total_in = __builtin_amdgcn_readlane(incl, 63);
@@ -1010,7 +1091,7 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
         if (c + hb[j] >= want) { jb = j; break; }
         c += hb[j];
       }
-      cut_bin = __builtin_amdgcn_readlane(kBins - 1 - 4 * lane - jb, src);
+      cut_bin = __builtin_amdgcn_readlane(nb - 1 - per * lane - jb, src);
       cut_above = __builtin_amdgcn_readlane(c, src);
     } else {  // cannot happen unless the counts disagree: the lowest non-empty bin
       const uint64_t ne = __ballot(lsum > 0);
@@ -1019,7 +1100,7 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
         int jb = 0;
         for (int j = 3; j >= 0; --j)
           if (hb[j] != 0) { jb = j; break; }
-        cut_bin = __builtin_amdgcn_readlane(kBins - 1 - 4 * lane - jb, src);
+        cut_bin = __builtin_amdgcn_readlane(nb - 1 - per * lane - jb, src);
         const int h_low = jb == 0 ? hb[0] : jb == 1 ? hb[1] : jb == 2 ? hb[2] : hb[3];
         cut_above = total_in - __builtin_amdgcn_readlane(h_low, src);
       }
@@ -1055,31 +1136,44 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
     ba = bb = cut_bin;  // from the wave scan above (target: k_target, or cap for minS)
     above_bins = static_cast<uint32_t>(cut_above);
   } else {
-    // Mass bounds per bin from its score range; the cut bin range is every bin
-    // the true cut may lie in.
+    // Mass bounds per bin: from its score range (count times the mass at
+    // each edge), and from its mass sum -- the terms exp(tau s - ref) <= 1,
+    // each within a relative (2 + |x|) 2^-22 (exp2 and the rounding of its
+    // argument x = (s - max) tau log2 e, |x| bounded by the bin's lower
+    // edge), rounded to the 2^-31 grid (<= 2^-32 each) and summed exactly.
+    // The cut bin range runs from the first bin the cut for T may lie in
+    // down to the last one the cut for T - kTopPMassSlack * Z may lie in:
+    // usually one bin.
     const double T = s.pZ - mab;
+    const double Trel = T - kTopPMassSlack * s.Z;
+    const float k1 = p.tau * 1.4426950408889634f;
     const float w = 1.0f / inv;
     const float slop = fabsf(w) * 1e-3f + fabsf(lo) * 1e-6f;
     double before_lo = 0.0, before_hi = 0.0;
     int top_nonempty = -1;
-    for (int bn = kBins - 1; bn >= 0; --bn) {
+    for (int bn = nb - 1; bn >= 0; --bn) {
       if (hs[bn] == 0) continue;
       if (top_nonempty < 0) top_nonempty = bn;
       float e_lo = lo + static_cast<float>(bn) * w - slop;
       float e_hi = lo + static_cast<float>(bn + 1) * w + slop;
       if (level == 0 && bn == 0) e_lo = -FLT_MAX;
-      if (level == 0 && bn == kBins - 1) e_hi = top;
-      const double mlo = hs[bn] * mass_term(e_lo, p.tau, s.ref);
-      const double mhi = hs[bn] * mass_term(fminf(e_hi, top), p.tau, s.ref);
-      const bool may_before_lt = before_lo < T;          // true mass before bn may be < T
-      const bool may_through_ge = before_hi + mhi >= T;  // true mass through bn may be >= T
-      if (may_before_lt && may_through_ge) {
-        if (bb < 0) bb = bn;
-        ba = bn;
+      if (level == 0 && bn == nb - 1) e_hi = top;
+      const double grid = static_cast<double>(hs[bn]) * 0x1p-32;
+      const double xmax = (static_cast<double>(s.smax) - static_cast<double>(e_lo)) * k1;
+      const double eps = fmin(1.0, (2.0 + xmax) * 0x1p-22);
+      const double mlo = fmax(hs[bn] * mass_term(e_lo, p.tau, s.ref), hm[bn] * (1.0 - eps) - grid);
+      const double mhi = fmin(hs[bn] * mass_term(fminf(e_hi, top), p.tau, s.ref),
+                              hm[bn] * (1.0 + eps) + grid);
+      if (bb < 0) {
+        if (before_hi + mhi >= T) bb = ba = bn;  // the mass through bn may reach T
+      } else if (before_lo < Trel) {
+        ba = bn;  // the mass above bn may still fall short of T - slack
+      } else {
+        break;
       }
       before_lo += mlo;
       before_hi += mhi;
-      if (!may_before_lt) break;
+      if (bb >= 0 && before_lo >= Trel) break;
     }
     if (bb < 0) {  // T <= 0 or rounding: the cut is at the top of the interval
       bb = ba = top_nonempty >= 0 ? top_nonempty : 0;
@@ -1089,7 +1183,7 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
   for (int bn = ba; bn <= bb; ++bn) inside += hs[bn];
   (void)above_bins;
   // New interval: the chosen bins of this level, as exact float bounds.
-  narrow(s.s_lo, s.s_hi, inv, add, ba, bb);
+  narrow(s.s_lo, s.s_hi, inv, add, ba, bb, nb);
   const int nl = level + 1;
   s.level = nl;
   if (inside <= static_cast<uint32_t>(kCand) || nl >= kLevels) {
@@ -1100,10 +1194,8 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
     // rows bins a sampled bracket, not the whole range): the next level spans
     // the chosen bins' actual extent, within the Cauchy-Schwarz bound.
     const float nlo = ba == 0 ? fmaxf(s.s_lo, -top) : lo + static_cast<float>(ba) / inv;
-    const float nhi = bb == kBins - 1 ? fminf(s.s_hi, top) : lo + static_cast<float>(bb + 1) / inv;
-    s.blo = nlo;
-    s.binv = static_cast<float>(kBins) / fmaxf(nhi - nlo, FLT_MIN);
-    s.badd = -nlo * s.binv;
+    const float nhi = bb == nb - 1 ? fminf(s.s_hi, top) : lo + static_cast<float>(bb + 1) / inv;
+    set_bins(s, nlo, static_cast<float>(nb) / fmaxf(nhi - nlo, FLT_MIN));
   }
 }
 
@@ -1345,13 +1437,14 @@ __global__ __launch_bounds__(256) void k_zero_u32(uint32_t* p, int64_t n) {
 // Workspace layout.
 // ---------------------------------------------------------------------------
 struct Layout {
-  size_t qp, state, hist, nab, mab, zp, cand_n, cand_lohi, cand, bsel, btie, qnorm, kmax, qmax, kop,
-      nact, total;
+  size_t qp, state, hist, hmass, nab, mab, zp, cand_n, cand_lohi, cand, bsel, btie, qnorm, kmax,
+      qmax, kop, nact, total;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-Layout layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t D, int32_t P, int split) {
+Layout layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t D, int32_t P, int split,
+              bool topp) {
   const int64_t Np = (N + P - 1) / P;
   const int64_t rows = B * Hq * Np;
   const int64_t nsplit = (N + split - 1) / split;
@@ -1362,6 +1455,7 @@ Layout layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t D, int32_t 
   l.qp = take(rows * D * 2);
   l.state = take(rows * sizeof(RowState));
   l.hist = take(rows * kBins * 4);
+  l.hmass = take(topp ? rows * kBins * 8 : 0);
   l.nab = take(rows * nsplit * 4);
   l.mab = take(rows * nsplit * 8);
   l.zp = take(rows * nsplit * 8);
@@ -1395,7 +1489,7 @@ size_t select_workspace_bytes(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int
                               int32_t block, int32_t mode, int64_t cap) {
   (void)mode;
   (void)cap;
-  return layout(B, Hq, Hkv, N, D, block, choose_split(B, Hq, N, block)).total;
+  return layout(B, Hq, Hkv, N, D, block, choose_split(B, Hq, N, block), mode == 1).total;
 }
 
 template <int MODE>
@@ -1415,7 +1509,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   const int64_t Np = (N + P - 1) / P;
   const int64_t rows = B * Hq * Np;
   const int split = choose_split(B, Hq, N, P);
-  const Layout l = layout(B, Hq, Hkv, N, D, P, split);
+  const Layout l = layout(B, Hq, Hkv, N, D, P, split, a.mode == 1);
   if (a.workspace_bytes < l.total) return hipErrorInvalidValue;
   char* ws = static_cast<char*>(a.workspace);
   SelParams p{};
@@ -1423,6 +1517,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.k = static_cast<const uint16_t*>(a.k.ptr);
   p.st = reinterpret_cast<RowState*>(ws + l.state);
   p.hist = reinterpret_cast<uint32_t*>(ws + l.hist);
+  p.hmass = reinterpret_cast<uint64_t*>(ws + l.hmass);
   p.n_above = reinterpret_cast<uint32_t*>(ws + l.nab);
   p.m_above = reinterpret_cast<double*>(ws + l.mab);
   p.zpart = reinterpret_cast<double*>(ws + l.zp);
@@ -1454,6 +1549,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.W = static_cast<int>((N + 31) / 32);
   p.nrb = static_cast<int>((Np + kRowsWG - 1) / kRowsWG);
   p.mode_topp = a.mode == 1;
+  p.nbins = p.mode_topp ? kBinsP : kBins;
   p.mode_mins = a.mode == 2;
   p.mins_direct = p.mode_mins && a.cap >= N;
   p.mode_tiled = a.mode == 3;
@@ -1533,6 +1629,9 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   const int64_t nh = rows * kBins;
   hipLaunchKernelGGL(k_zero_u32, dim3(static_cast<unsigned>((nh + 255) / 256)), dim3(256), 0, stream,
                      p.hist, nh);
+  if (p.mode_topp)  // the bin masses (64-bit): 2 words each
+    hipLaunchKernelGGL(k_zero_u32, dim3(static_cast<unsigned>((2 * nh + 255) / 256)), dim3(256), 0,
+                       stream, reinterpret_cast<uint32_t*>(p.hmass), 2 * nh);
   p.items = B * Hq * static_cast<int64_t>(p.nsplit) * p.nrb;
   p.per_xcd = (p.items + 7) / 8;
   const dim3 pgrid(static_cast<unsigned>(p.per_xcd * 8));
@@ -1543,6 +1642,9 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
     if (p.mode_mins) {  // minS: the row maxima fix each row's threshold
       score_pass<MODE_MAX>(D, false, pgrid, p, stream);
       hipLaunchKernelGGL(k_mins, igrid, dim3(256), 0, stream, p);
+    } else if (round == 0 && p.mode_topp) {  // topP: the row maxima are the mass references
+      score_pass<MODE_MAX>(D, false, pgrid, p, stream);
+      hipLaunchKernelGGL(k_topp_ref, igrid, dim3(256), 0, stream, p);
     } else if (round == 0 && !p.mode_topp) {
       score_pass<MODE_SAMPLE>(D, false, pgrid, p, stream);
       hipLaunchKernelGGL(k_bracket, igrid, dim3(256), 0, stream, p);

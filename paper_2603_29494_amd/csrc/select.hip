@@ -383,12 +383,15 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   // overflows its LDS slots appends the rest directly.
   constexpr bool COL = MODE == MODE_COLLECT;
   constexpr int kStage = 96;  // LDS candidate slots per row
-  __shared__ uint64_t s_cand[COL ? kRowsWG * kStage : 1];
+  constexpr int kStageStride = kStage + 1;  // odd in 8-byte units: rows start in different banks
+  __shared__ uint64_t s_cand[COL ? kRowsWG * kStageStride : 1];
   __shared__ uint32_t s_ccnt[COL ? kRowsWG : 1];
   __shared__ uint32_t s_clo[COL ? kRowsWG : 1];
   __shared__ uint32_t s_chi[COL ? kRowsWG : 1];
   __shared__ uint32_t s_cbase[COL ? kRowsWG : 1];
-  __shared__ __align__(16) float s_acc[COL ? 4 * 64 * 16 : 1];  // per lane: its 16 scores
+  // per lane: its 16 scores, the 16-byte chunk q stored at q ^ ((lane / 4) % 4) so
+  // that the 16 lanes of a 16-byte store or load phase use distinct banks
+  __shared__ __align__(16) float s_acc[COL ? 4 * 64 * 16 : 1];
   __shared__ uint32_t s_max[MODE == MODE_MAX ? kRowsWG : 1];  // ordered keys of row maxima
 
   if (p.gate >= 0 && p.nact[p.gate] == 0u) return;  // no row needs this pass
@@ -539,9 +542,10 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
             // The lane's scores go through LDS so that a candidate's score can
             // be read by its (per-lane) position.
             float* sc = s_acc + (wave * 64 + lane) * 16;
+            const int csw = (lane >> 2) & 3;
 #pragma unroll
             for (int q4 = 0; q4 < 4; ++q4)
-              *reinterpret_cast<f32x4*>(sc + 4 * q4) =
+              *reinterpret_cast<f32x4*>(sc + 4 * (q4 ^ csw)) =
                   f32x4{acc[4 * q4], acc[4 * q4 + 1], acc[4 * q4 + 2], acc[4 * q4 + 3]};
             if (ins) {
               const int rl = rb2 * 32 + ln;
@@ -549,12 +553,12 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
               uint32_t lo_k = 0xFFFFFFFFu, hi_k = 0u;
               for (uint32_t m = ins; m; m &= m - 1u) {
                 const int kl = __builtin_ctz(m);
-                const uint32_t okey = ord_key(sc[4 * (kl >> 3) + (kl & 3)]);
+                const uint32_t okey = ord_key(sc[4 * ((kl >> 3) ^ csw) + (kl & 3)]);
                 const uint64_t entry = (static_cast<uint64_t>(okey) << 32) | (~static_cast<uint32_t>(kb + kl));
                 lo_k = min(lo_k, okey);
                 hi_k = max(hi_k, okey);
                 if (rank++ < kStage) {
-                  s_cand[rl * kStage + rank - 1] = entry;
+                  s_cand[rl * kStageStride + rank - 1] = entry;
                 } else {  // LDS slots of this row full: append directly
                   const int64_t row = row0 + rl;
                   const uint32_t pos = atomicAdd(&p.cand_n[row], 1u);
@@ -704,7 +708,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
       const int rl = t / kStage, j = t % kStage;
       if (!s_part[rl] || j >= static_cast<int>(min(s_ccnt[rl], static_cast<uint32_t>(kStage)))) continue;
       const uint32_t pos = s_cbase[rl] + j;
-      if (pos < kCand) p.cand[(row0 + rl) * kCand + pos] = s_cand[rl * kStage + j];
+      if (pos < kCand) p.cand[(row0 + rl) * kCand + pos] = s_cand[rl * kStageStride + j];
     }
   }
   if (tid < nrows && s_part[tid]) {

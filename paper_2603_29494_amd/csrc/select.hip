@@ -361,11 +361,14 @@ template <int D, int MODE, bool TOPP>
 __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   constexpr int DS = D / 16;
   constexpr bool HIST = MODE == MODE_HIST || MODE == MODE_HIST0;
-  // Row stride NB + 1 (odd): rows hitting the same bin use different
-  // banks; slot NB of a row takes the increments of keys outside the
+  // Bin-major layout, entry (bin, row) at bin * kRowsWG + row: the 32 rows of
+  // a wave's update sit in 32 distinct banks whatever their bins (the two
+  // lanes of one row share a bank: at most 2-way conflicts; a row-major
+  // layout gave ~4-way ones from bins colliding across rows).  Bin NB of a
+  // row takes the increments of keys outside the
   // interval, so that every key can be counted without a branch.
   constexpr int NB = TOPP ? kBinsP : kBins;
-  constexpr int HS = NB + 1;
+  constexpr int HS = NB + 1;  // bins per row including the spare one
   // topP HIST passes also sum each bin's softmax mass (terms exp2((s - row
   // max) tau log2 e) <= 1 in fixed point), which pins the cut to one or two
   // bins per level: one 64-bit integer atomic per key carries both the count
@@ -618,10 +621,10 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
               const uint32_t mq = ref[rb2] >= 0.0
                                       ? static_cast<uint32_t>(__builtin_fmaf(mt, 0x1p31f, 0.5f))
                                       : 0u;
-              atomicAdd(reinterpret_cast<unsigned long long*>(&s_hist64[rl * HS + bn]),
+              atomicAdd(reinterpret_cast<unsigned long long*>(&s_hist64[bn * kRowsWG + rl]),
                         (1ull << kMassShift) | mq);
             } else {
-              atomicAdd(&s_hist[rl * HS + bn], 1u);
+              atomicAdd(&s_hist[bn * kRowsWG + rl], 1u);
             }
           }
         }
@@ -723,8 +726,8 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   if (HIST) {
     for (int t = tid; t < nrows * NB; t += kThreads) {
       const int rl = t / NB, bn = t % NB;
-      const uint64_t v = MH ? s_hist64[rl * HS + bn] : 0ull;
-      const uint32_t c = MH ? static_cast<uint32_t>(v >> kMassShift) : s_hist[rl * HS + bn];
+      const uint64_t v = MH ? s_hist64[bn * kRowsWG + rl] : 0ull;
+      const uint32_t c = MH ? static_cast<uint32_t>(v >> kMassShift) : s_hist[bn * kRowsWG + rl];
       if (c && s_part[rl]) {
         atomicAdd(&p.hist[(row0 + rl) * kBins + bn], c);
         const uint64_t m = v & ((1ull << kMassShift) - 1ull);

@@ -7,14 +7,20 @@ topK keep ratio 15% (11340 keys per block).  Inputs are seeded synthetic
 tensors with planted vertical structure (paper_2603_29494_amd.synth, workload
 4); the paper's model activations are not available.
 
-A step = vecattn_select (pooling, scoring, topK) + vecattn_sparse_attn over all
-heads, inputs resident in HBM.  Prints one JSON line:
-  value  = dense-equivalent TFLOP/s = 4 * Hq * N^2 * D / (ms per layer)
-  ms_per_step = ms per layer
+A step = vecattn_select (pooling, scoring, topK; lists without the -1 padding
+past each count, which the attention never reads) + vecattn_sparse_attn over
+all heads, inputs resident in HBM.  Timing: HIP events on the launch stream around
+each call.  The W warm-up steps run back to back (their last ones give the
+warm-cache figures); each of the K timed steps starts cold: a 1 GiB scratch
+buffer is written just before it (outside its events), evicting the 256 MB
+last-level cache and the L2s.  Prints one JSON line:
+  value  = dense-equivalent TFLOP/s = 4 * Hq * N^2 * D / (median cold ms per layer)
+  ms_per_step = median cold ms per layer (min / max and the warm figures beside)
   roofline   = the sparse-attention kernel (the dominant one): algorithmic
-               MFMA FLOPs on the gathered tiles per launch / its average
-               duration (HIP events on its stream) against 2516.6 TFLOP/s
-  cpu_baseline = the CPU oracle on a bounded sample of the same layer
+               MFMA FLOPs on the gathered tiles per launch / its mean duration
+               over the timed steps, against 2516.6 TFLOP/s
+  cpu_baseline = the CPU oracle on a bounded sample of the same layer,
+               extrapolated to the layer
 """
 import argparse
 import json
@@ -54,8 +60,8 @@ def recorded_traffic(workload: str):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", type=int, default=4, help="synthetic workload id (1-5)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-blocks", type=int, default=0,
@@ -94,10 +100,13 @@ def cpu_baseline(layer, sample_blocks):
         dense += 4.0 * n_i * keys * D
         nrows += n_i
     secs = t2 - t0
+    total_rows = B * Hq * N
     return {"value": dense / secs / 1e12, "unit": "TFLOP/s (dense-equivalent)", "cores": nthreads,
-            "kind": "oracle",
-            "sample": f"{sample_blocks} random query blocks of the same layer ({nrows} query rows); "
-                      f"select {t1 - t0:.2f} s + attention {t2 - t1:.2f} s",
+            "kind": "oracle", "extrapolated": True,
+            "sample": f"{sample_blocks} random query blocks of the same layer ({nrows} of its "
+                      f"{total_rows} query rows), select {t1 - t0:.2f} s + attention {t2 - t1:.2f} s; "
+                      f"value = the sample's dense-equivalent FLOPs over its time, so the whole "
+                      f"layer would take ~{secs * total_rows / nrows:.0f} s on these cores",
             "seconds": secs}
 
 
@@ -136,29 +145,49 @@ def main():
     out = torch.empty_like(q)
     stream = torch.cuda.current_stream(dev)
 
-    def step(ev=None):
-        if ev is not None:
-            ev[0].record(stream)
-        va.select(q, k, P, mode, w.param, w.causal, cap=cap, idx=idx, counts=counts, workspace=ws)
-        if ev is not None:
-            ev[1].record(stream)
-        va.sparse_attn(q, k, v, idx, counts, P, w.causal, out=out)
-        if ev is not None:
-            ev[2].record(stream)
+    scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev)   # cache eviction
 
-    for _ in range(args.warmup):
-        step()
+    def step(ev):
+        ev[0].record(stream)
+        va.select(q, k, P, mode, w.param, w.causal, cap=cap, idx=idx, counts=counts, workspace=ws,
+                  unpadded=True)
+        ev[1].record(stream)
+        va.sparse_attn(q, k, v, idx, counts, P, w.causal, out=out)
+        ev[2].record(stream)
+
+    def new_events(n):
+        return [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n)]
+
+    warm_ev = new_events(args.warmup)
+    for s in range(args.warmup):          # back to back: warm caches
+        step(warm_ev[s])
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    events = new_events(args.steps)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for s in range(args.steps):
+    for s in range(args.steps):           # timed: each step after a 1 GiB write
+        scratch.fill_(s & 0xFF)
         step(events[s])
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
-    sel_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
-    attn_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
-    layer_ms = sel_ms + attn_ms
+
+    def stats(evs):
+        sel = np.array([e[0].elapsed_time(e[1]) for e in evs])
+        att = np.array([e[1].elapsed_time(e[2]) for e in evs])
+        lay = sel + att
+        return sel, att, lay
+
+    sel_all, attn_all, layer_all = stats(events)
+    sel_ms = float(np.median(sel_all))
+    attn_ms = float(np.median(attn_all))
+    layer_ms = float(np.median(layer_all))
+    attn_mean_ms = float(np.mean(attn_all))    # the roofline's launch average
+    warm = None
+    if args.warmup >= 3:                  # the warm-up steps after the first two
+        ws_, wa_, wl_ = stats(warm_ev[2:])
+        warm = {"ms_per_step_median": round(float(np.median(wl_)), 4),
+                "ms_select_median": round(float(np.median(ws_)), 4),
+                "ms_attention_median": round(float(np.median(wa_)), 4), "steps": len(wl_)}
 
     cnt = counts.cpu().numpy().astype(np.int64)
     rows_per_block = np.minimum(N, (np.arange(Np) + 1) * P) - np.arange(Np) * P
@@ -173,7 +202,7 @@ def main():
     keep = float(cnt.sum()) / float(B * Hq * L.sum())
     bytes_sel = 2.0 * B * N * D * (Hq + k.shape[1]) + 4.0 * cnt.sum() + 4.0 * B * Hq * Np
     dense_tflops = f_dense / (layer_ms * 1e-3) / 1e12
-    attn_tflops = f_alg / (attn_ms * 1e-3) / 1e12
+    attn_tflops = f_alg / (attn_mean_ms * 1e-3) / 1e12
 
     result = {
         "metric": "ms/layer + dense-equiv TFLOP/s (MFMA-peak %) at 75k-token DiT shape",
@@ -191,9 +220,15 @@ def main():
         "config": {"workload": w.name, "batch": B, "q_heads": Hq, "kv_heads": int(k.shape[1]),
                    "seq_len": N, "head_dim": D, "causal": bool(w.causal), "query_block": P,
                    "selection": f"{mode} {w.param}"},
+        "timing": "cold cache (1 GiB written before each timed step); median of the steps",
+        "ms_per_step_min": round(float(layer_all.min()), 4),
+        "ms_per_step_max": round(float(layer_all.max()), 4),
         "ms_select": round(sel_ms, 4),
+        "ms_select_min_max": [round(float(sel_all.min()), 4), round(float(sel_all.max()), 4)],
         "ms_attention": round(attn_ms, 4),
+        "ms_attention_min_max": [round(float(attn_all.min()), 4), round(float(attn_all.max()), 4)],
         "selection_pct": round(100.0 * sel_ms / layer_ms, 2),
+        "warm": warm,
         "wall_ms_per_step": round(wall_ms, 4),
         "attention_mfma_pct": round(100.0 * attn_tflops / PEAK_BF16_TFLOPS, 2),
         "selection_hbm_pct": round(100.0 * bytes_sel / (sel_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 2),

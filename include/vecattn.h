@@ -33,7 +33,8 @@
  *     [i*P, min(N, (i+1)*P)) (the last block may be ragged).
  *   - I (idx) is int32 [B, Hq, N_p, cap], contiguous.  Row (b, h, i) lists the
  *     selected keys of block i in strictly ascending order in its first C[b,h,i]
- *     entries; the remaining entries are -1.  C (counts) is int32 [B, Hq, N_p].
+ *     entries; the remaining entries are -1 (left unwritten with
+ *     VECATTN_UNPADDED).  C (counts) is int32 [B, Hq, N_p].
  *   - Argument errors are detected on the host before any launch and return a
  *     status without touching memory.  Launch failures return
  *     VECATTN_ERR_DEVICE.
@@ -72,12 +73,18 @@ typedef enum vecattn_sel_mode {
 } vecattn_sel_mode;
 
 /* Bits of the `causal` argument of the selection entry points.  0 (none) and
- * 1 (VECATTN_CAUSAL) keep their plain meaning; other bits are invalid. */
+ * 1 (VECATTN_CAUSAL) keep their plain meaning; bits other than these three are
+ * invalid. */
 #define VECATTN_CAUSAL 1    /* block i's eligible keys end at its last row */
 #define VECATTN_KEEP_DIAG 2 /* block i also keeps the keys of its own rows,
                                [i*P, min(N, (i+1)*P)); cap must then cover
                                vecattn_select_max_count for the same flags in
                                every mode (no block is clamped) */
+#define VECATTN_UNPADDED 4  /* the entries of I past a row's count are left as
+                               they were instead of being set to -1 (the
+                               attention and vecattn_check_lists read only the
+                               first C entries): with a large cap (threshold
+                               modes, cap = N) this saves writing the padding */
 
 typedef struct vecattn_tdesc {
   int64_t B, H, N, D; /* logical sizes */
@@ -236,8 +243,8 @@ vecattn_status vecattn_select_per_head(const void* q, const vecattn_tdesc* qd, c
  *   idx, counts : as produced by vecattn_select (any source is accepted if
  *   every listed key is in [0, N) and the lists are strictly ascending;
  *   other contents are undefined behaviour).
- *   causal : the VECATTN_CAUSAL bit (VECATTN_KEEP_DIAG is accepted and has no
- *   effect here; other bits are invalid).
+ *   causal : the VECATTN_CAUSAL bit (VECATTN_KEEP_DIAG and VECATTN_UNPADDED are
+ *   accepted and have no effect here; other bits are invalid).
  *   scale : softmax scale; 0 means 1 / sqrt(D).
  *   lse   : optional fp32 [B, Hq, N] contiguous output, may be NULL.
  * Errors: INVALID_ARG (null pointer, shape mismatch, block < 1, cap < 1,

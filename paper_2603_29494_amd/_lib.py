@@ -17,7 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libvecattn.so")
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_CAPACITY, ERR_DEVICE = range(5)
-CAUSAL, KEEP_DIAG = 1, 2  # bits of the selection entry points' `causal` argument
+CAUSAL, KEEP_DIAG, UNPADDED = 1, 2, 4  # bits of the selection entry points' `causal` argument
 SEL_TOPK, SEL_TOPP, SEL_MINS, SEL_MINS_TILED = 0, 1, 2, 3
 _MODES = {"topk": SEL_TOPK, "topp": SEL_TOPP, "mins": SEL_MINS, "mins_tiled": SEL_MINS_TILED}
 
@@ -128,8 +128,8 @@ def _per_head(param) -> bool:
     return np.ndim(param) > 0
 
 
-def _flags(causal: bool, keep_diag: bool) -> int:
-    return (CAUSAL if causal else 0) | (KEEP_DIAG if keep_diag else 0)
+def _flags(causal: bool, keep_diag: bool, unpadded: bool = False) -> int:
+    return (CAUSAL if causal else 0) | (KEEP_DIAG if keep_diag else 0) | (UNPADDED if unpadded else 0)
 
 
 def max_count(N: int, block: int, causal: bool, mode, param, keep_diag: bool = False) -> int:
@@ -172,20 +172,21 @@ def select(q: torch.Tensor, k: torch.Tensor, block: int, mode, param: float,
            workspace: Optional[torch.Tensor] = None,
            n_clamped: Optional[torch.Tensor] = None, tile: Optional[int] = None,
            group_tiles: Optional[int] = None,
-           keep_diag: bool = False) -> Tuple[torch.Tensor, torch.Tensor]:
+           keep_diag: bool = False, unpadded: bool = False) -> Tuple[torch.Tensor, torch.Tensor]:
     """Per-block key-index lists (I, C) of Algorithm 1 for topK / topP / minS (Eq. 3)
     selection, or minS with Algorithm 1's cross-tile running maximum ("mins_tiled":
     ``tile`` = B_K and ``group_tiles`` = G_K, both 16 when not given).  ``param``
     may be one value per query head (a sequence of Hq values, e.g. from
     plan_filter_ratios).  ``keep_diag``: every block also keeps the keys of its own
-    rows (cap must then cover max_count(..., keep_diag=True))."""
+    rows (cap must then cover max_count(..., keep_diag=True)).  ``unpadded``: list
+    entries past a block's count are left unwritten instead of -1."""
     _bf16_cuda(q, "q")
     _bf16_cuda(k, "k")
     B, Hq, N, Dd = q.shape
     Np = (N + block - 1) // block
     if cap is None:
         cap = max_count(N, block, causal, mode, param, keep_diag)
-    flags = _flags(causal, keep_diag)
+    flags = _flags(causal, keep_diag, unpadded)
     dev = q.device
     if idx is None:
         idx = torch.empty((B, Hq, Np, cap), dtype=torch.int32, device=dev)

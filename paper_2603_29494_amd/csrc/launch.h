@@ -37,6 +37,7 @@ struct SelectArgs {
   int32_t block;
   int32_t causal;
   int32_t keep_diag;  // every block also keeps the keys of its own rows
+  int32_t unpadded;   // entries past a row's count are left unwritten
   int32_t mode;
   double param;
   const double* head_params;  // NULL, or one parameter per query head (host memory, Hq <= 128)

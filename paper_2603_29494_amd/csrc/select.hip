@@ -127,6 +127,7 @@ struct SelParams {
   int mins_direct;  // minS with cap >= every block's eligible keys: no count needed
   int mode_tiled;   // cross-tile minS (Algorithm 1)
   int keep_diag;    // every block also keeps the keys of its own rows
+  int unpadded;     // entries past a row's count are left unwritten (no -1 padding)
   int quad_rows;    // idx rows start on 16 bytes and no row can exceed cap
   uint32_t* nact;   // [kActiveSlots] rows waiting for each later pass
   int gate;         // slot of nact this launch needs non-zero, or -1
@@ -1429,7 +1430,8 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
     if (lane < base - done) out[done + lane] = stage[lane];
   }
   const int n = min(base, static_cast<int>(p.cap));
-  for (int t = n + lane; t < p.cap; t += 64) out[t] = -1;
+  if (!p.unpadded)
+    for (int t = n + lane; t < p.cap; t += 64) out[t] = -1;
   if (lane == 0) p.counts[r] = n;
   // Cross-tile minS keeps a block's first cap keys (key order) and counts it.
   if (lane == 0 && p.mode_tiled && base > p.cap && p.n_clamped) atomicAdd(p.n_clamped, 1);
@@ -1550,6 +1552,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.D = static_cast<int>(D);
   p.causal = a.causal;
   p.keep_diag = a.keep_diag;
+  p.unpadded = a.unpadded;
   p.quad_rows = (a.cap % 4 == 0) && (reinterpret_cast<uintptr_t>(a.idx) % 16 == 0) && a.mode != 3;
   p.split = split;
   p.nsplit = static_cast<int>((N + split - 1) / split);

@@ -61,7 +61,10 @@ bool tiling_ok(int32_t tile, int32_t group_tiles) {
 }
 
 // Bits of the `causal` argument of the selection entry points.
-constexpr int32_t kCausal = VECATTN_CAUSAL, kKeepDiag = VECATTN_KEEP_DIAG;
+constexpr int32_t kCausal = VECATTN_CAUSAL, kKeepDiag = VECATTN_KEEP_DIAG,
+                  kUnpadded = VECATTN_UNPADDED;
+// Bits the selection entry points accept.
+constexpr int32_t kSelBits = kCausal | kKeepDiag | kUnpadded;
 
 // Largest count any block can produce.  Without the diagonal, k_i is
 // non-decreasing in L_i, so the largest L_i decides; with it (block i adds
@@ -112,7 +115,7 @@ vecattn_status check_attn(const void* q, const vecattn_tdesc* qd, const void* k,
     return VECATTN_ERR_INVALID_ARG;
   if (!idx || !counts || block < 1 || cap < 1 || cap > kMaxN) return VECATTN_ERR_INVALID_ARG;
   if (!std::isfinite(scale) || scale < 0.0f) return VECATTN_ERR_INVALID_ARG;
-  if ((causal & ~(kCausal | kKeepDiag)) != 0) return VECATTN_ERR_INVALID_ARG;
+  if ((causal & ~kSelBits) != 0) return VECATTN_ERR_INVALID_ARG;
   if (!gather_offsets_ok(kd) || !gather_offsets_ok(vd)) return VECATTN_ERR_UNSUPPORTED;
   return VECATTN_OK;
 }
@@ -131,7 +134,7 @@ vecattn_status select_check(const void* q, const vecattn_tdesc* qd, const void* 
   if (kd->B != qd->B || kd->N != qd->N || kd->D != qd->D || qd->H % kd->H != 0)
     return VECATTN_ERR_INVALID_ARG;
   if (!idx || !counts || block < 1 || cap < 1 || cap > kMaxN) return VECATTN_ERR_INVALID_ARG;
-  if (!mode_ok(mode) || (causal & ~(kCausal | kKeepDiag)) != 0) return VECATTN_ERR_INVALID_ARG;
+  if (!mode_ok(mode) || (causal & ~kSelBits) != 0) return VECATTN_ERR_INVALID_ARG;
   if (head_params) {
     if (qd->H > kMaxHeadParams) return VECATTN_ERR_UNSUPPORTED;
     for (int64_t h = 0; h < qd->H; ++h) {
@@ -170,7 +173,8 @@ vecattn_status select_impl(const void* q, const vecattn_tdesc* qd, const void* k
   if (workspace && !aligned16(workspace)) return VECATTN_ERR_INVALID_ARG;
   if (head_params) param = head_params[0];
   vecattn::SelectArgs a{to_tensor(q, qd), to_tensor(k, kd), block, (causal & kCausal) ? 1 : 0,
-                        (causal & kKeepDiag) ? 1 : 0, mode, param, head_params, tile, group_tiles,
+                        (causal & kKeepDiag) ? 1 : 0, (causal & kUnpadded) ? 1 : 0, mode, param,
+                        head_params, tile, group_tiles,
                         idx, cap, counts, n_clamped, workspace, workspace_bytes};
   hipError_t e = vecattn::launch_select(a, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
@@ -210,7 +214,7 @@ vecattn_status vecattn_pool(const void* q, const vecattn_tdesc* qd, int32_t bloc
 vecattn_status vecattn_select_max_count(int64_t N, int32_t block, int32_t causal, int32_t mode,
                                         double param, int64_t* out) {
   if (!out || N < 1 || N > kMaxN || block < 1 || !mode_ok(mode) || !param_ok(mode, param) ||
-      (causal & ~(kCausal | kKeepDiag)) != 0)
+      (causal & ~kSelBits) != 0)
     return VECATTN_ERR_INVALID_ARG;
   *out = max_count(N, block, causal, mode, param);
   return VECATTN_OK;
@@ -238,7 +242,7 @@ vecattn_status vecattn_head_sparsity(const int32_t* counts, int64_t B, int64_t H
                                      int32_t block, int32_t causal, double* sparsity,
                                      void* stream) {
   if (!counts || !sparsity || B < 1 || Hq < 1 || Hq > INT32_MAX || N < 1 || N > kMaxN ||
-      block < 1 || (causal & ~(kCausal | kKeepDiag)) != 0)
+      block < 1 || (causal & ~kSelBits) != 0)
     return VECATTN_ERR_INVALID_ARG;
   hipError_t e = vecattn::launch_head_sparsity(counts, B, Hq, N, block, (causal & kCausal) ? 1 : 0,
                                                sparsity, static_cast<hipStream_t>(stream));
@@ -257,7 +261,7 @@ vecattn_status vecattn_recall(const void* q, const vecattn_tdesc* qd, const void
   if (!idx || !counts || !kept || block < 1 || cap < 1 || cap > kMaxN)
     return VECATTN_ERR_INVALID_ARG;
   if (!std::isfinite(scale) || scale < 0.0f) return VECATTN_ERR_INVALID_ARG;
-  if ((causal & ~(kCausal | kKeepDiag)) != 0) return VECATTN_ERR_INVALID_ARG;
+  if ((causal & ~kSelBits) != 0) return VECATTN_ERR_INVALID_ARG;
   if (qd->N > vecattn::kRecallMaxN) return VECATTN_ERR_UNSUPPORTED;
   vecattn::RecallArgs a{to_tensor(q, qd), to_tensor(k, kd), idx, counts, cap, block,
                         (causal & kCausal) ? 1 : 0, scale, kept};
@@ -381,7 +385,7 @@ vecattn_status vecattn_select_varlen(const void* q, const vecattn_tdesc* qd, con
     return VECATTN_ERR_INVALID_ARG;
   if (!cu_ok(cu_seqlens, nseq, qd->N) || !idx || !counts || block < 1 || cap < 1 || cap > kMaxN)
     return VECATTN_ERR_INVALID_ARG;
-  if (!mode_ok(mode) || !param_ok(mode, param) || (causal & ~(kCausal | kKeepDiag)) != 0)
+  if (!mode_ok(mode) || !param_ok(mode, param) || (causal & ~kSelBits) != 0)
     return VECATTN_ERR_INVALID_ARG;
   // Every sequence's checks first, so that an error launches nothing.
   for (int32_t s = 0; s < nseq; ++s) {

@@ -178,11 +178,11 @@ def test_keep_diag_flag():
     assert va.max_count(1024, 64, True, "topk", 0.125, keep_diag=True) == 192
     assert va.max_count(100, 64, True, "topk", 0.5, keep_diag=True) == 86   # 50 + 36 rows
     assert va.max_count(1000, 64, True, "topp", 0.5, keep_diag=True) == 1000
-    assert select(mode=0, param=0.25, cap=64, causal=4) == INVALID        # unknown bit
+    assert select(mode=0, param=0.25, cap=64, causal=8) == INVALID        # unknown bit
     assert select(mode=0, param=0.25, cap=127, causal=2) == CAPACITY       # 64 + 64 needed
     assert select(mode=1, param=0.5, cap=255, causal=2) == CAPACITY        # no clamping
     assert select(mode=1, param=0.5, cap=256, causal=3, ws=None) == CAPACITY   # valid flags
-    assert attn(causal=4) == INVALID
+    assert attn(causal=8) == INVALID
 
 
 def test_varlen_rejects_bad_offsets():
@@ -323,7 +323,7 @@ def test_head_sparsity_and_recall_reject_bad_arguments():
         return lib.vecattn_head_sparsity(cnt, B, H, N, block, causal, out, None)
     assert hs(cnt=None) == INVALID and hs(out=None) == INVALID
     assert hs(B=0) == INVALID and hs(H=0) == INVALID and hs(N=0) == INVALID
-    assert hs(N=(1 << 30) + 1) == INVALID and hs(block=0) == INVALID and hs(causal=4) == INVALID
+    assert hs(N=(1 << 30) + 1) == INVALID and hs(block=0) == INVALID and hs(causal=8) == INVALID
 
     def rc(q=FAKE, qd=None, k=FAKE, kd=None, idx=FAKE, cap=16, cnt=FAKE, block=64, causal=0,
            scale=0.0, kept=FAKE):
@@ -333,7 +333,7 @@ def test_head_sparsity_and_recall_reject_bad_arguments():
                                   causal, scale, kept, None)
     assert rc(q=None) == INVALID and rc(k=None) == INVALID and rc(idx=None) == INVALID
     assert rc(cnt=None) == INVALID and rc(kept=None) == INVALID
-    assert rc(block=0) == INVALID and rc(cap=0) == INVALID and rc(causal=4) == INVALID
+    assert rc(block=0) == INVALID and rc(cap=0) == INVALID and rc(causal=8) == INVALID
     assert rc(scale=-1.0) == INVALID and rc(scale=float("nan")) == INVALID
     assert rc(kd=desc(1, 3, 256, 128)) == INVALID and rc(kd=desc(1, 2, 255, 128)) == INVALID
     assert rc(q=FAKE + 2) == INVALID
@@ -353,7 +353,7 @@ def test_select_noalloc_checks_before_any_device_call():
         return lib.vecattn_select_noalloc(FAKE, ctypes.byref(qd), FAKE, ctypes.byref(kd), block,
                                           causal, mode, param, idx, cap, cnt, None, None)
     assert sel(idx=None) == INVALID and sel(cnt=None) == INVALID and sel(block=0) == INVALID
-    assert sel(param=1.5) == INVALID and sel(mode=9) == INVALID and sel(causal=4) == INVALID
+    assert sel(param=1.5) == INVALID and sel(mode=9) == INVALID and sel(causal=8) == INVALID
     assert sel(kd=desc(1, 3, 256, 128)) == INVALID
     assert sel(cap=63) == CAPACITY
     big_q, big_k = desc(1, 40, 75600, 128), desc(1, 40, 75600, 128)

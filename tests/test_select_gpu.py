@@ -389,3 +389,24 @@ def test_topp_mass_beyond_fp32_exponent_range(gpu):
     for p in (0.5, 0.99, 0.999999):
         idx, cnt, cap, _ = run(q, k, block, oracle.TOPP, p, False)
         check_rows(q, k, block, oracle.TOPP, p, False, cap, idx, cnt, all_rows(q, block))
+
+
+@pytest.mark.parametrize("mode,param", [("topk", 0.2), ("topp", 0.9), ("mins", 0.5),
+                                        ("mins_tiled", 0.3)])
+def test_unpadded_lists(gpu, mode, param):
+    # VECATTN_UNPADDED: the first C entries of each list are those of the padded
+    # call, the entries past C keep what the caller left there.
+    q, k, _ = synth.planted_case(770 + len(mode), 1, 3, 3, 1500, 128)
+    tq, tk = dev(q), dev(k)
+    cap = va.max_count(1500, 64, True, mode, param)
+    a_idx, a_cnt = va.select(tq, tk, 64, mode, param, True, cap=cap)
+    Np = (1500 + 63) // 64
+    b_idx = torch.full((1, 3, Np, cap), 0x7FFF7FFF, dtype=torch.int32, device="cuda")
+    b_cnt = torch.empty((1, 3, Np), dtype=torch.int32, device="cuda")
+    va.select(tq, tk, 64, mode, param, True, cap=cap, idx=b_idx, counts=b_cnt, unpadded=True)
+    torch.cuda.synchronize()
+    assert torch.equal(a_cnt, b_cnt)
+    live = torch.arange(cap, device="cuda").view(1, 1, 1, -1) < a_cnt.unsqueeze(-1)
+    assert torch.equal(torch.where(live, a_idx, 0), torch.where(live, b_idx, 0))
+    assert bool((b_idx[~live] == 0x7FFF7FFF).all())
+    assert va.check_lists(b_idx, b_cnt, 1500) == 0

@@ -66,10 +66,9 @@ constexpr int kActiveSlots = 16;
 
 enum Phase : int { PH_IDLE = 0, PH_HIST = 1, PH_COLLECT = 2, PH_DONE = 3, PH_EMIT = 4 };
 // MODE_HIST0: first histogram level (the interval is everything).
-// MODE_SAMPLE: moments of the scores of every kSampleStride-th key block.
 // MODE_MAX: the largest score of each minS row.
 enum Mode : int {
-  MODE_HIST = 0, MODE_COLLECT = 1, MODE_EMIT = 2, MODE_HIST0 = 3, MODE_SAMPLE = 4, MODE_MAX = 5
+  MODE_HIST = 0, MODE_COLLECT = 1, MODE_EMIT = 2, MODE_HIST0 = 3, MODE_MAX = 5
 };
 constexpr int kSampleStride = 16;  // 32-key blocks between sampled blocks
 
@@ -423,10 +422,9 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     int part = 0;
     if (tid < nrows) {
       const int ph = p.st[row0 + tid].phase;
-      part = (HIST || MODE == MODE_SAMPLE || MODE == MODE_MAX) ? ph == PH_HIST
+      part = (HIST || MODE == MODE_MAX) ? ph == PH_HIST
              : (MODE == MODE_COLLECT)        ? ph == PH_COLLECT
                                              : ph == PH_EMIT;
-      if (MODE == MODE_SAMPLE) part = part && !p.st[row0 + tid].topp;
       if (MODE == MODE_MAX) part = part && (p.st[row0 + tid].mins || p.st[row0 + tid].topp);
     }
     s_part[tid] = part;
@@ -481,7 +479,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   }
 
   double zacc[2] = {0.0, 0.0}, macc[2] = {0.0, 0.0};
-  const float k1 = p.tau * 1.4426950408889634f;  // raw score -> log2 units
+  const float tl2 = p.tau * 1.4426950408889634f;  // raw score -> log2 units
   uint32_t nacc[2] = {0u, 0u};
 
   const int nblk = (key1 - key0 + 31) / 32;
@@ -536,7 +534,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
             wge |= (ok && acc[e] >= slo[rb2]) ? 1u << kl : 0u;
             wgt |= (ok && acc[e] > shi[rb2]) ? 1u << kl : 0u;
             if (TOPP && ref[rb2] >= 0.0 && ok && acc[e] > shi[rb2])
-              macc[rb2] += static_cast<double>(__builtin_amdgcn_exp2f((acc[e] - smax[rb2]) * k1));
+              macc[rb2] += static_cast<double>(__builtin_amdgcn_exp2f((acc[e] - smax[rb2]) * tl2));
           }
           nacc[rb2] += static_cast<uint32_t>(__builtin_popcount(wgt));
           const uint32_t ins = wge & ~wgt;
@@ -611,7 +609,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
           // topP: the key's softmax term relative to the row maximum, exp(tau
           // s - ref) with ref = tau * max (terms below 2^-126, a share of the
           // mass far below any tolerance, may flush to 0)
-          const float mt = TOPP ? __builtin_amdgcn_exp2f((sc - smax[rb2]) * k1) : 0.0f;
+          const float mt = TOPP ? __builtin_amdgcn_exp2f((sc - smax[rb2]) * tl2) : 0.0f;
           if (TOPP && ref[rb2] >= 0.0 && ok) {
             if (MODE == MODE_HIST0) zacc[rb2] += static_cast<double>(mt);
             if (above) macc[rb2] += static_cast<double>(mt);
@@ -634,38 +632,6 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
       else rowproc(false);
     }
   };
-  if (MODE == MODE_SAMPLE) {
-    // Sampled blocks: every kSampleStride-th 32-key block of the split (the
-    // split starts on a multiple of the stride), spread over the waves.
-    float s1[2] = {0.0f, 0.0f}, s2[2] = {0.0f, 0.0f};
-    for (int blk = wave * kSampleStride; blk < nblk; blk += 4 * kSampleStride) {
-      u32x4 ka[DS];
-      kload(ka, blk);
-      const int kb = key0 + blk * 32;
-#pragma unroll
-      for (int rb2 = 0; rb2 < 2; ++rb2) {
-        f32x16 acc = f32x16{};
-#pragma unroll
-        for (int q2 = 0; q2 < DS; ++q2)
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ka[q2]),
-                                                        qf[rb2][q2], acc, 0, 0, 0);
-        const int lim = Lr[rb2] - kb;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
-          const float sc = kl < lim ? acc[e] : 0.0f;
-          s1[rb2] += sc;
-          s2[rb2] = __builtin_fmaf(sc, sc, s2[rb2]);
-          nacc[rb2] += kl < lim ? 1u : 0u;
-        }
-      }
-    }
-#pragma unroll
-    for (int rb2 = 0; rb2 < 2; ++rb2) {
-      zacc[rb2] = s1[rb2];
-      macc[rb2] = s2[rb2];
-    }
-  } else {
   u32x4 k0[DS], k1[DS];
   kload(k0, wave);
   for (int blk = wave; blk < nblk; blk += 8) {
@@ -674,7 +640,6 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     if (blk + 4 >= nblk) break;
     kload(k0, blk + 8);
     kproc(k1, blk + 4);
-  }
   }
   if (MODE == MODE_EMIT) return;
   if (MODE == MODE_MAX) {
@@ -722,7 +687,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
     const uint32_t n = s_nred[0][tid] + s_nred[1][tid] + s_nred[2][tid] + s_nred[3][tid];
     p.n_above[row * p.nsplit + sp] = n;
     p.m_above[row * p.nsplit + sp] = m;
-    if (MODE == MODE_HIST0 || MODE == MODE_SAMPLE) p.zpart[row * p.nsplit + sp] = z;
+    if (MODE == MODE_HIST0) p.zpart[row * p.nsplit + sp] = z;
   }
   if (HIST) {
     for (int t = tid; t < nrows * NB; t += kThreads) {
@@ -741,42 +706,200 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// Level-0 bins of topK rows from a sample of their scores.  For any set of
-// values with mean mu and deviation sigma, at most a fraction 1 / (1 + a^2)
-// lies at or above mu + a sigma, and as much at or below mu - a sigma
-// (Cantelli's inequality); with a = sqrt((L - k) / k) above and
-// sqrt((k - 1) / (L - k + 1)) below, the k-th largest of L scores lies
-// between.  mu and sigma come from the sampled keys, so the bound is widened;
-// it only places the 256 bins (the tails fall into the end bins): a cut
-// outside it costs another level, never a wrong selection.
+// Level-0 bins of topK rows from a sample of their scores: every
+// kSampleStride-th 32-key block of the row's eligible keys.  One workgroup per
+// 64 pooled rows walks all of their sampled blocks twice (the second walk hits
+// L2), with the score pass's MFMA sequence:
+//   1. Moments: for any set of values with mean mu and deviation sigma, at
+//      most a fraction 1 / (1 + a^2) lies at or above mu + a sigma, and as much
+//      at or below mu - a sigma (Cantelli's inequality); with a = sqrt((L - k)
+//      / k) above and sqrt((k - 1) / (L - k + 1)) below, the k-th largest of L
+//      scores lies between (widened for sampling).
+//   2. A histogram of the sampled scores over that bracket: the k-th largest
+//      key's rank among the n sampled ones is about k n / L, with deviation
+//      sqrt(n p (1 - p)) for independent samples (p = k / L).  The level-0
+//      bins span the sampled values between the ranks k n / L -/+ (12 sd + 4):
+//      6 deviations at twice the independent spread, since sampled blocks of
+//      32 consecutive keys are correlated.
+// Both only place the bins: keys outside fall into the end bins, and a cut
+// that lands there costs a level (the next spans that bin's actual extent),
+// never a wrong set.  Rows with fewer than 64 (moments) or 256 (histogram)
+// sampled keys keep the wider bins.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_bracket(SelParams p) {
-  const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (r >= p.rows) return;
-  RowState& s = p.st[r];
-  if (s.phase != PH_HIST || s.level != 0 || s.topp) return;
-  const int i = static_cast<int>(r % p.Np);
-  const int rb = i / kRowsWG;
-  const int i_last = min(p.Np, (rb + 1) * kRowsWG) - 1;
-  const int ns = (eligible(i_last, p.P, p.N, p.causal) + p.split - 1) / p.split;
-  double n = 0.0, m1 = 0.0, m2 = 0.0;
-  for (int q = 0; q < ns; ++q) {
-    n += p.n_above[r * p.nsplit + q];
-    m1 += p.zpart[r * p.nsplit + q];
-    m2 += p.m_above[r * p.nsplit + q];
+template <int D>
+__global__ __launch_bounds__(kThreads) void k_sample_bracket(SelParams p) {
+  constexpr int DS = D / 16;
+  __shared__ uint32_t s_hist[(kBins + 1) * kRowsWG];  // bin-major, as in the score pass
+  __shared__ float s_m1[4][kRowsWG], s_m2[4][kRowsWG];
+  __shared__ uint32_t s_n[4][kRowsWG];
+  __shared__ float s_mul[kRowsWG], s_add[kRowsWG];
+  __shared__ int s_part[kRowsWG];
+  const int64_t item = xcd_work_item(p.per_xcd);
+  if (item >= p.items) return;
+  const int rb = static_cast<int>(item % p.nrb);
+  const int64_t bh = item / p.nrb;
+  const int b = static_cast<int>(bh / p.Hq), h = static_cast<int>(bh % p.Hq);
+  const int hk = h / p.group;
+  const int i0 = rb * kRowsWG;
+  const int nrows = min(kRowsWG, p.Np - i0);
+  const int Ltile = eligible(i0 + nrows - 1, p.P, p.N, p.causal);
+  const int64_t row0 = bh * p.Np + i0;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63, g = lane >> 5, ln = lane & 31;
+  if (tid < kRowsWG) {
+    int part = 0;
+    if (tid < nrows) {
+      const RowState& st = p.st[row0 + tid];
+      part = st.phase == PH_HIST && st.level == 0 && !st.topp;
+    }
+    s_part[tid] = part;
   }
-  const int L = s.L, k = s.k_target;
-  if (n < 64.0 || k >= L) return;
-  const double mu = m1 / n;
-  const double sd = sqrt(fmax(m2 / n - mu * mu, 0.0));
-  if (!(sd > 0.0)) return;
-  const double a_hi = sqrt(static_cast<double>(L - k) / k);
-  const double a_lo = sqrt(static_cast<double>(k - 1) / (L - k + 1));
-  const double widen = 1.2 + 4.0 / sqrt(n);
-  const float lo = fmaxf(static_cast<float>(mu - (widen * a_lo + 0.25) * sd), s.blo);
-  const float hi = fminf(static_cast<float>(mu + (widen * a_hi + 0.25) * sd), -s.blo);
-  if (!(hi > lo)) return;
-  set_bins(s, lo, static_cast<float>(p.nbins) / (hi - lo));
+  for (int t = tid; t < (kBins + 1) * kRowsWG; t += kThreads) s_hist[t] = 0u;
+  __syncthreads();
+
+  bf16x8 qf[2][DS];
+  bool part[2];
+  int Lr[2];
+#pragma unroll
+  for (int rb2 = 0; rb2 < 2; ++rb2) {
+    const int rl = rb2 * 32 + ln;
+    part[rb2] = rl < nrows && s_part[rl];
+    Lr[rb2] = rl < nrows ? p.st[row0 + rl].L : 0;
+    const u32x4* src = reinterpret_cast<const u32x4*>(p.qp + (row0 + (rl < nrows ? rl : 0)) * D);
+#pragma unroll
+    for (int s2 = 0; s2 < DS; ++s2) {
+      const u32x4 t = rl < nrows ? src[2 * s2 + g] : u32x4{0, 0, 0, 0};
+      qf[rb2][s2] = __builtin_bit_cast(bf16x8, t);
+    }
+  }
+  // Sampled block j is key block kSampleStride * j: keys [32 kSampleStride j, +32).
+  const int nsb = (Ltile + 32 * kSampleStride - 1) / (32 * kSampleStride);
+  auto scores = [&](int j, int rb2, const u32x4 (&ka)[DS]) __attribute__((always_inline)) {
+    f32x16 acc = f32x16{};
+#pragma unroll
+    for (int s2 = 0; s2 < DS; ++s2)
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ka[s2]),
+                                                    qf[rb2][s2], acc, 0, 0, 0);
+    return acc;
+  };
+  auto kload = [&](u32x4 (&dst)[DS], int j) __attribute__((always_inline)) {
+    const int kbi = min(kSampleStride * j, p.nkb - 1);
+    const u32x4* ksrc =
+        p.kop + ((static_cast<int64_t>(b) * p.Hkv + hk) * p.nkb + kbi) * (DS * 64) + lane;
+#pragma unroll
+    for (int s2 = 0; s2 < DS; ++s2) dst[s2] = ksrc[s2 * 64];
+  };
+
+  // 1. Moments of the sampled scores.
+  float m1[2] = {0.0f, 0.0f}, m2[2] = {0.0f, 0.0f};
+  uint32_t cnt[2] = {0u, 0u};
+  for (int j = wave; j < nsb; j += 4) {
+    u32x4 ka[DS];
+    kload(ka, j);
+    const int kb = 32 * kSampleStride * j;
+#pragma unroll
+    for (int rb2 = 0; rb2 < 2; ++rb2) {
+      const f32x16 acc = scores(j, rb2, ka);
+      const int lim = Lr[rb2] - kb;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+        const float sc = kl < lim ? acc[e] : 0.0f;
+        m1[rb2] += sc;
+        m2[rb2] = __builtin_fmaf(sc, sc, m2[rb2]);
+        cnt[rb2] += kl < lim ? 1u : 0u;
+      }
+    }
+  }
+#pragma unroll
+  for (int rb2 = 0; rb2 < 2; ++rb2) {
+    const float a = m1[rb2] + __shfl_xor(m1[rb2], 32);
+    const float c = m2[rb2] + __shfl_xor(m2[rb2], 32);
+    const uint32_t n = cnt[rb2] + __shfl_xor(cnt[rb2], 32);
+    if (g == 0) {
+      s_m1[wave][rb2 * 32 + ln] = a;
+      s_m2[wave][rb2 * 32 + ln] = c;
+      s_n[wave][rb2 * 32 + ln] = n;
+    }
+  }
+  __syncthreads();
+  if (tid < kRowsWG) {  // the Cantelli bracket of row tid
+    float mul = 0.0f, add = 0.0f;
+    if (s_part[tid]) {
+      RowState& st = p.st[row0 + tid];
+      const double n = static_cast<double>(s_n[0][tid] + s_n[1][tid] + s_n[2][tid] + s_n[3][tid]);
+      const double a1 = ((static_cast<double>(s_m1[0][tid]) + s_m1[1][tid]) + s_m1[2][tid]) + s_m1[3][tid];
+      const double a2 = ((static_cast<double>(s_m2[0][tid]) + s_m2[1][tid]) + s_m2[2][tid]) + s_m2[3][tid];
+      const int L = st.L, k = st.k_target;
+      if (n >= 64.0 && k < L) {
+        const double mu = a1 / n;
+        const double sd = sqrt(fmax(a2 / n - mu * mu, 0.0));
+        if (sd > 0.0) {
+          const double a_hi = sqrt(static_cast<double>(L - k) / k);
+          const double a_lo = sqrt(static_cast<double>(k - 1) / (L - k + 1));
+          const double widen = 1.2 + 4.0 / sqrt(n);
+          const float lo = fmaxf(static_cast<float>(mu - (widen * a_lo + 0.25) * sd), st.blo);
+          const float hi = fminf(static_cast<float>(mu + (widen * a_hi + 0.25) * sd), -st.blo);
+          if (hi > lo) set_bins(st, lo, static_cast<float>(p.nbins) / (hi - lo));
+        }
+      }
+      mul = st.binv;
+      add = st.badd;
+      if (!(n >= 256.0 && k < L)) s_part[tid] = 0;  // too few samples for the quantile step
+    }
+    s_mul[tid] = mul;
+    s_add[tid] = add;
+  }
+  __syncthreads();
+
+  // 2. Histogram of the sampled scores over those bins.
+  float bmul[2], badd[2];
+#pragma unroll
+  for (int rb2 = 0; rb2 < 2; ++rb2) {
+    const int rl = rb2 * 32 + ln;
+    part[rb2] = rl < nrows && s_part[rl];
+    bmul[rb2] = s_mul[rl];
+    badd[rb2] = s_add[rl];
+  }
+  for (int j = wave; j < nsb; j += 4) {
+    u32x4 ka[DS];
+    kload(ka, j);
+    const int kb = 32 * kSampleStride * j;
+#pragma unroll
+    for (int rb2 = 0; rb2 < 2; ++rb2) {
+      const f32x16 acc = scores(j, rb2, ka);
+      if (!part[rb2]) continue;
+      const int lim = Lr[rb2] - kb;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+        const int bn = kl < lim ? bin_of(acc[e], bmul[rb2], badd[rb2], kBins) : kBins;
+        atomicAdd(&s_hist[bn * kRowsWG + rb2 * 32 + ln], 1u);
+      }
+    }
+  }
+  __syncthreads();
+  if (tid < kRowsWG && s_part[tid]) {  // the quantile band of row tid
+    RowState& st = p.st[row0 + tid];
+    uint32_t n = 0;
+    for (int bn = 0; bn < kBins; ++bn) n += s_hist[bn * kRowsWG + tid];
+    const double pk = static_cast<double>(st.k_target) / st.L;
+    const double mid = pk * n;
+    const double margin = 12.0 * sqrt(n * pk * (1.0 - pk)) + 4.0;
+    const double r_top = mid - margin, r_bot = mid + margin;  // ranks from the top
+    int bt = kBins - 1, bb = 0;
+    bool have_top = r_top < 1.0;
+    double c = 0.0;
+    for (int bn = kBins - 1; bn >= 0; --bn) {
+      c += s_hist[bn * kRowsWG + tid];
+      if (!have_top && c >= r_top) { bt = bn; have_top = true; }
+      if (c >= r_bot) { bb = bn; break; }
+    }
+    const float w = 1.0f / st.binv;
+    const float lo = bb == 0 ? st.blo : st.blo + static_cast<float>(bb) * w;
+    const float hi = st.blo + static_cast<float>(bt + 1) * w;
+    if (hi > lo) set_bins(st, lo, static_cast<float>(p.nbins) / (hi - lo));
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1656,8 +1779,14 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
       score_pass<MODE_MAX>(D, false, pgrid, p, stream);
       hipLaunchKernelGGL(k_topp_ref, igrid, dim3(256), 0, stream, p);
     } else if (round == 0 && !p.mode_topp) {
-      score_pass<MODE_SAMPLE>(D, false, pgrid, p, stream);
-      hipLaunchKernelGGL(k_bracket, igrid, dim3(256), 0, stream, p);
+      SelParams ps = p;  // one work item per 64 pooled rows (no key splits)
+      ps.items = B * Hq * static_cast<int64_t>(p.nrb);
+      ps.per_xcd = (ps.items + 7) / 8;
+      const dim3 sgrid(static_cast<unsigned>(ps.per_xcd * 8));
+      if (D == 128)
+        hipLaunchKernelGGL(k_sample_bracket<128>, sgrid, dim3(kThreads), 0, stream, ps);
+      else
+        hipLaunchKernelGGL(k_sample_bracket<64>, sgrid, dim3(kThreads), 0, stream, ps);
     }
     if (p.mins_direct) break;  // every row goes straight to the emit pass
     for (int lv = 0; lv < kLevels; ++lv) {

@@ -1484,14 +1484,20 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
   // next one, and go out one by one after the last chunk.
   const bool quads = p.quad_rows;
   int done = 0;      // entries stored (quad path)
-  for (int c0 = 0; c0 < nw; c0 += 64 * kCompactBatch) {
-    uint32_t mb[kCompactBatch], tb[kCompactBatch];
+  // The next batch's words are loaded while this batch is listed.
+  uint32_t mb[kCompactBatch], tb[kCompactBatch], mn[kCompactBatch], tn[kCompactBatch];
+  auto load_batch = [&](uint32_t (&m)[kCompactBatch], uint32_t (&t)[kCompactBatch], int c0)
+      __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < kCompactBatch; ++j) {
       const int wd = c0 + 64 * j + lane;
-      mb[j] = wd < nw ? bsel[wd] : 0u;
-      tb[j] = (tiep && wd < nw) ? btie[wd] : 0u;
+      m[j] = wd < nw ? bsel[wd] : 0u;
+      t[j] = (tiep && wd < nw) ? btie[wd] : 0u;
     }
+  };
+  load_batch(mb, tb, 0);
+  for (int c0 = 0; c0 < nw; c0 += 64 * kCompactBatch) {
+    load_batch(mn, tn, c0 + 64 * kCompactBatch);
 #pragma unroll
     for (int j = 0; j < kCompactBatch; ++j) {
       const int wd = c0 + 64 * j + lane;
@@ -1546,6 +1552,11 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
         __syncthreads();
       }
       base += total;
+    }
+#pragma unroll
+    for (int j = 0; j < kCompactBatch; ++j) {
+      mb[j] = mn[j];
+      tb[j] = tn[j];
     }
   }
   if (quads) {  // the last entries, fewer than 4

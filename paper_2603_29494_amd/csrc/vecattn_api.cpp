@@ -68,7 +68,9 @@ constexpr int32_t kSelBits = kCausal | kKeepDiag | kUnpadded;
 
 // Largest count any block can produce.  Without the diagonal, k_i is
 // non-decreasing in L_i, so the largest L_i decides; with it (block i adds
-// its own n_i rows' keys), min(L_i, k_i + n_i) is taken over the blocks.
+// its own n_i rows' keys), the largest min(L_i, k_i + n_i).  Every block but
+// the last has n_i = P and L_i, k_i non-decreasing in i, so that value is
+// non-decreasing over them: the last two blocks decide.
 int64_t max_count(int64_t N, int32_t P, int32_t flags, int32_t mode, double param) {
   const bool causal = (flags & kCausal) != 0;
   const int64_t Np = num_blocks(N, P);
@@ -76,7 +78,7 @@ int64_t max_count(int64_t N, int32_t P, int32_t flags, int32_t mode, double para
   if (mode != VECATTN_SEL_TOPK) return Lmax;
   if (!(flags & kKeepDiag)) return topk_count(param, Lmax);
   int64_t best = 0;
-  for (int64_t i = 0; i < Np; ++i) {
+  for (int64_t i = std::max<int64_t>(0, Np - 2); i < Np; ++i) {
     const int64_t n_i = std::min<int64_t>(N, (i + 1) * P) - i * P;
     const int64_t L = causal ? std::min<int64_t>(N, (i + 1) * P) : N;
     best = std::max(best, std::min(L, topk_count(param, L) + n_i));

@@ -42,9 +42,10 @@ namespace {
 
 constexpr int kRowsWG = 64;     // pooled rows per workgroup
 constexpr int kThreads = 256;
-constexpr int kBins = 256;     // bins per histogram level (topK, minS)
-constexpr int kBinsP = 128;    // bins per level in topP launches: each bin also sums its mass, and
-                               // 128 64-bit bins fit the LDS of two workgroups per CU
+constexpr int kBins = 128;     // bins per histogram level: 64 rows x 129 bins of 32 bits fit the LDS
+                               // of three workgroups per CU (topK, minS), of 64 bits (topP: each
+                               // bin also sums its mass) that of two
+constexpr int kSampleBins = 256;  // bins of the sampled-score histogram that places level 0 (topK)
 // topP bin entries: count << 48 | mass in units of 2^-31 (terms exp(tau s -
 // ref) <= 1 rounded to that grid); a workgroup adds at most 4096 terms to a
 // bin, so neither field can carry into the other.
@@ -130,7 +131,6 @@ struct SelParams {
   int quad_rows;    // idx rows start on 16 bytes and no row can exceed cap
   uint32_t* nact;   // [kActiveSlots] rows waiting for each later pass
   int gate;         // slot of nact this launch needs non-zero, or -1
-  int nbins;        // bins per histogram level: kBins, or kBinsP in topP launches
   int tiled_tile;   // keys per tile: 16 or 32
   int tiled_gs;     // keys per group of tiles (a power of two)
   int tiled_sb;     // 32-key blocks per segment a wave walks in order
@@ -314,7 +314,7 @@ __global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
   s.phase = PH_HIST;
   s.s_lo = -FLT_MAX;
   s.s_hi = FLT_MAX;
-  set_bins(s, -cc, static_cast<float>(p.nbins) / (2.0f * cc));
+  set_bins(s, -cc, static_cast<float>(kBins) / (2.0f * cc));
   s.ref = static_cast<double>(p.tau) * static_cast<double>(cc);  // >= every tau * score
   s.smax = cc;
   s.tie_partial = 0;
@@ -357,8 +357,13 @@ __global__ __launch_bounds__(256) void k_kmax_init(float* kmax, int n) {
 // ---------------------------------------------------------------------------
 // TOPP: the launch selects by mass (rows restarted as topK(cap) may be mixed
 // in); otherwise no mass is computed.
+// topK / minS histogram passes are held to 168 VGPRs so that three waves share
+// each SIMD (their 33 KB of LDS allows it): the latency of the K loads and of the
+// MFMA chains is then hidden better (~5% of the selection at the 75k DiT layer).
 template <int D, int MODE, bool TOPP>
-__global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
+__global__ __launch_bounds__(kThreads)
+__attribute__((amdgpu_waves_per_eu(((MODE == MODE_HIST || MODE == MODE_HIST0) && !TOPP) ? 3 : 1)))
+void k_score_pass(SelParams p) {
   constexpr int DS = D / 16;
   constexpr bool HIST = MODE == MODE_HIST || MODE == MODE_HIST0;
   // Bin-major layout, entry (bin, row) at bin * kRowsWG + row: the 32 rows of
@@ -367,7 +372,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
   // layout gave ~4-way ones from bins colliding across rows).  Bin NB of a
   // row takes the increments of keys outside the
   // interval, so that every key can be counted without a branch.
-  constexpr int NB = TOPP ? kBinsP : kBins;
+  constexpr int NB = kBins;
   constexpr int HS = NB + 1;  // bins per row including the spare one
   // topP HIST passes also sum each bin's softmax mass (terms exp2((s - row
   // max) tau log2 e) <= 1 in fixed point), which pins the cut to one or two
@@ -729,7 +734,7 @@ __global__ __launch_bounds__(kThreads) void k_score_pass(SelParams p) {
 template <int D>
 __global__ __launch_bounds__(kThreads) void k_sample_bracket(SelParams p) {
   constexpr int DS = D / 16;
-  __shared__ uint32_t s_hist[(kBins + 1) * kRowsWG];  // bin-major, as in the score pass
+  __shared__ uint32_t s_hist[(kSampleBins + 1) * kRowsWG];  // bin-major, as in the score pass
   __shared__ float s_m1[4][kRowsWG], s_m2[4][kRowsWG];
   __shared__ uint32_t s_n[4][kRowsWG];
   __shared__ float s_mul[kRowsWG], s_add[kRowsWG];
@@ -754,7 +759,7 @@ __global__ __launch_bounds__(kThreads) void k_sample_bracket(SelParams p) {
     }
     s_part[tid] = part;
   }
-  for (int t = tid; t < (kBins + 1) * kRowsWG; t += kThreads) s_hist[t] = 0u;
+  for (int t = tid; t < (kSampleBins + 1) * kRowsWG; t += kThreads) s_hist[t] = 0u;
   __syncthreads();
 
   bf16x8 qf[2][DS];
@@ -840,11 +845,14 @@ __global__ __launch_bounds__(kThreads) void k_sample_bracket(SelParams p) {
           const double widen = 1.2 + 4.0 / sqrt(n);
           const float lo = fmaxf(static_cast<float>(mu - (widen * a_lo + 0.25) * sd), st.blo);
           const float hi = fminf(static_cast<float>(mu + (widen * a_hi + 0.25) * sd), -st.blo);
-          if (hi > lo) set_bins(st, lo, static_cast<float>(p.nbins) / (hi - lo));
+          if (hi > lo) set_bins(st, lo, static_cast<float>(kBins) / (hi - lo));
         }
       }
-      mul = st.binv;
-      add = st.badd;
+      // sampled scores go into bins of half the level-0 width over the same range
+      // (both factors exact powers of two)
+      static_assert(kSampleBins == 2 * kBins, "sample bins halve the level-0 bins");
+      mul = 2.0f * st.binv;
+      add = 2.0f * st.badd;
       if (!(n >= 256.0 && k < L)) s_part[tid] = 0;  // too few samples for the quantile step
     }
     s_mul[tid] = mul;
@@ -873,7 +881,7 @@ __global__ __launch_bounds__(kThreads) void k_sample_bracket(SelParams p) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
-        const int bn = kl < lim ? bin_of(acc[e], bmul[rb2], badd[rb2], kBins) : kBins;
+        const int bn = kl < lim ? bin_of(acc[e], bmul[rb2], badd[rb2], kSampleBins) : kSampleBins;
         atomicAdd(&s_hist[bn * kRowsWG + rb2 * 32 + ln], 1u);
       }
     }
@@ -882,23 +890,23 @@ __global__ __launch_bounds__(kThreads) void k_sample_bracket(SelParams p) {
   if (tid < kRowsWG && s_part[tid]) {  // the quantile band of row tid
     RowState& st = p.st[row0 + tid];
     uint32_t n = 0;
-    for (int bn = 0; bn < kBins; ++bn) n += s_hist[bn * kRowsWG + tid];
+    for (int bn = 0; bn < kSampleBins; ++bn) n += s_hist[bn * kRowsWG + tid];
     const double pk = static_cast<double>(st.k_target) / st.L;
     const double mid = pk * n;
     const double margin = 12.0 * sqrt(n * pk * (1.0 - pk)) + 4.0;
     const double r_top = mid - margin, r_bot = mid + margin;  // ranks from the top
-    int bt = kBins - 1, bb = 0;
+    int bt = kSampleBins - 1, bb = 0;
     bool have_top = r_top < 1.0;
     double c = 0.0;
-    for (int bn = kBins - 1; bn >= 0; --bn) {
+    for (int bn = kSampleBins - 1; bn >= 0; --bn) {
       c += s_hist[bn * kRowsWG + tid];
       if (!have_top && c >= r_top) { bt = bn; have_top = true; }
       if (c >= r_bot) { bb = bn; break; }
     }
-    const float w = 1.0f / st.binv;
+    const float w = 0.5f / st.binv;  // width of a sample bin
     const float lo = bb == 0 ? st.blo : st.blo + static_cast<float>(bb) * w;
     const float hi = st.blo + static_cast<float>(bt + 1) * w;
-    if (hi > lo) set_bins(st, lo, static_cast<float>(p.nbins) / (hi - lo));
+    if (hi > lo) set_bins(st, lo, static_cast<float>(kBins) / (hi - lo));
   }
 }
 
@@ -922,7 +930,7 @@ __global__ __launch_bounds__(256) void k_topp_ref(SelParams p) {
   s.smax = mx;
   s.ref = static_cast<double>(mx) * static_cast<double>(p.tau);  // exact product
   const float lo = fmaxf(mx - kTopPRange / p.tau, s.blo);
-  set_bins(s, lo, static_cast<float>(p.nbins) / fmaxf(mx - lo, FLT_MIN));
+  set_bins(s, lo, static_cast<float>(kBins) / fmaxf(mx - lo, FLT_MIN));
 }
 
 // ---------------------------------------------------------------------------
@@ -957,7 +965,7 @@ __global__ __launch_bounds__(256) void k_mins(SelParams p) {
     atomicAdd(&p.nact[kEmitSlot], 1u);
     return;
   }
-  set_bins(s, tf, static_cast<float>(p.nbins) / fmaxf(hi - tf, FLT_MIN));
+  set_bins(s, tf, static_cast<float>(kBins) / fmaxf(hi - tf, FLT_MIN));
 }
 
 // ---------------------------------------------------------------------------
@@ -1172,7 +1180,7 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
   __shared__ uint32_t hs[kBins];
   __shared__ double hm[kBins];
   const int lane = threadIdx.x;
-  const int nb = p.nbins;
+  const int nb = kBins;
   for (int t = lane; t < nb; t += 64) {
     hs[t] = p.hist[r * kBins + t];
     p.hist[r * kBins + t] = 0u;  // ready for the next level
@@ -1196,16 +1204,16 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
     if (level == 0) z += p.zpart[r * p.nsplit + q];
   }
   // Count cut (topK, and minS rows over cap) across the wave: lane l holds
-  // bins nb - 1 - per l - j (j < per = nb / 64, descending), and the scan counts the keys in
+  // bins nb - 1 - 2 l - j (j < 2, descending), and the scan counts the keys in
   // every bin from the top through them.  The cut bin is the highest bin whose
   // count from the top reaches the target rank (never an empty bin: the bin
   // above it fell short); `cut_above` counts the keys in the bins above it.
-  static_assert(kBins == 4 * 64 && kBinsP == 2 * 64, "four or two bins per lane");
-  const int per = nb / 64;
-  int hb[4];
+  static_assert(kBins == 2 * 64, "two bins per lane");
+  constexpr int per = 2;
+  int hb[2];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) hb[j] = j < per ? static_cast<int>(hs[nb - 1 - per * lane - j]) : 0;
-  const int lsum = hb[0] + hb[1] + hb[2] + hb[3];
+  for (int j = 0; j < 2; ++j) hb[j] = static_cast<int>(hs[nb - 1 - per * lane - j]);
+  const int lsum = hb[0] + hb[1];
   const int incl = wave_incl_scan(lsum);
   const int total_in = __builtin_amdgcn_readlane(incl, 63);
   int cut_bin = -1, cut_above = 0;
@@ -1217,22 +1225,18 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
     const uint64_t hit = __ballot(incl >= want);
     if (hit != 0ull) {
       const int src = __builtin_ctzll(hit);  // lowest lane: the highest bins
-      int c = incl - lsum, jb = 3;  // in lane src: the first j whose count reaches `want`
-      for (int j = 0; j < 4; ++j) {
-        if (c + hb[j] >= want) { jb = j; break; }
-        c += hb[j];
-      }
+      int c = incl - lsum, jb = 1;  // in lane src: the first j whose count reaches `want`
+      if (c + hb[0] >= want) jb = 0;
+      else c += hb[0];
       cut_bin = __builtin_amdgcn_readlane(nb - 1 - per * lane - jb, src);
       cut_above = __builtin_amdgcn_readlane(c, src);
     } else {  // cannot happen unless the counts disagree: the lowest non-empty bin
       const uint64_t ne = __ballot(lsum > 0);
       if (ne != 0ull) {
         const int src = 63 - __builtin_clzll(ne);  // highest lane: the lowest bins
-        int jb = 0;
-        for (int j = 3; j >= 0; --j)
-          if (hb[j] != 0) { jb = j; break; }
+        const int jb = hb[1] != 0 ? 1 : 0;
         cut_bin = __builtin_amdgcn_readlane(nb - 1 - per * lane - jb, src);
-        const int h_low = jb == 0 ? hb[0] : jb == 1 ? hb[1] : jb == 2 ? hb[2] : hb[3];
+        const int h_low = jb == 0 ? hb[0] : hb[1];
         cut_above = total_in - __builtin_amdgcn_readlane(h_low, src);
       }
     }
@@ -1693,7 +1697,6 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.W = static_cast<int>((N + 31) / 32);
   p.nrb = static_cast<int>((Np + kRowsWG - 1) / kRowsWG);
   p.mode_topp = a.mode == 1;
-  p.nbins = p.mode_topp ? kBinsP : kBins;
   p.mode_mins = a.mode == 2;
   p.mins_direct = p.mode_mins && a.cap >= N;
   p.mode_tiled = a.mode == 3;

@@ -177,6 +177,30 @@ __device__ __forceinline__ double mass_term(float s, float tau, double ref) {
   return ldexp(static_cast<double>(__builtin_amdgcn_exp2f(static_cast<float>(y - n))), static_cast<int>(n));
 }
 
+// Key of a 32-key block that the operand-order copy of K places in A-operand
+// row r: rows 8 a + 4 g + b hold keys 16 g + 4 a + b.  The product's
+// accumulator entry e of lane group g (row 8 (e / 4) + 4 g + e % 4) is then
+// key 16 g + e: a lane's 16 scores are 16 consecutive keys.
+__host__ __device__ constexpr int block_key_of_row(int r) {
+  return 16 * ((r >> 2) & 1) + 4 * (r >> 3) + (r & 3);
+}
+
+// Comparisons as lane masks (bit l: lane l; one compare into a scalar register
+// pair), for shift_in.
+__device__ __forceinline__ uint64_t lanes_ge(float a, float b) { return __ballot(a >= b); }
+__device__ __forceinline__ uint64_t lanes_gt(float a, float b) { return __ballot(a > b); }
+__device__ __forceinline__ uint64_t lanes_lt(int a, int b) { return __ballot(a < b); }
+
+// 2 w + (this lane's bit of m): one add with the lane mask as carry-in, so a
+// lane's word of flags is built with one instruction per key and no per-lane
+// bit constants.
+__device__ __forceinline__ uint32_t shift_in(uint32_t w, uint64_t m) {
+  uint32_t r;
+  uint64_t carry;
+  asm("v_addc_co_u32_e64 %0, %1, %2, %2, %3" : "=v"(r), "=s"(carry) : "v"(w), "s"(m));
+  return r;
+}
+
 // Bin of s at one level (must be evaluated identically everywhere: the
 // scoring passes and the interval search below use this one function).
 // One fma, clamped to [0, nb - 1] in float before the conversion
@@ -228,7 +252,7 @@ __device__ __forceinline__ void narrow(float& s_lo, float& s_hi, float mul, floa
 // ---------------------------------------------------------------------------
 // K of every key/value head in MFMA operand order, once per call: for each
 // 32-key block and head-dim step s2, the 64 lanes' A-operand pieces (lane l:
-// key l % 32 of the block, head-dim values 16 s2 + 8 (l / 32) .. +7) lie
+// key block_key_of_row(l % 32) of the block, head-dim values 16 s2 + 8 (l / 32) .. +7) lie
 // contiguously, so a score pass fetches each step with one fully coalesced
 // 1 KB load instead of 32 rows x 32 bytes.  Keys past N repeat key N - 1
 // (they are never eligible).  One wave per 32-key block.  The same read of K
@@ -252,7 +276,7 @@ __global__ __launch_bounds__(256) void k_k_operand_order(const uint16_t* __restr
     const int blk = static_cast<int>(t % nkb);
     bh = t / nkb;
     const int64_t b = bh / Hkv, hk = bh % Hkv;
-    const int key = min(blk * 32 + ln, N - 1);
+    const int key = min(blk * 32 + block_key_of_row(ln), N - 1);
     const u32x4* src = reinterpret_cast<const u32x4*>(k + b * sB + hk * sH + key * sN);
     u32x4* dst = kop + t * (DS * 64) + lane;
 #pragma unroll
@@ -503,7 +527,7 @@ void k_score_pass(SelParams p) {
     const int kb = key0 + blk * 32;
 #pragma unroll
     for (int rb2 = 0; rb2 < 2; ++rb2) {
-      // Raw scores s = <q_p, k> of keys kl = 8 (e / 4) + 4 g + e % 4 of the block.
+      // Raw scores s = <q_p, k> of keys kl = 16 g + e of the block.
       f32x16 acc = f32x16{};
 #pragma unroll
       for (int s2 = 0; s2 < DS; ++s2)
@@ -520,7 +544,7 @@ void k_score_pass(SelParams p) {
           float m = kNegInf;
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
-            const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+            const int kl = 16 * g + e;
             if (elig(kl)) m = fmaxf(m, acc[e]);
           }
           m = fmaxf(m, __shfl_xor(m, 32));
@@ -528,22 +552,27 @@ void k_score_pass(SelParams p) {
           return;
         }
         if (MODE == MODE_COLLECT) {
-          // Two bitmasks of this lane's keys (bit kl): at or above the interval
-          // (the kept set; the resolve step clears the candidates it rejects) and
-          // above it.  Their difference is the lane's candidates.
+          // Two words of this lane's 16 keys (bit e: key 16 g + e): at or above
+          // the interval (the kept set; the resolve step clears the candidates
+          // it rejects) and above it.  Their difference is the lane's candidates.
           uint32_t wge = 0u, wgt = 0u;
 #pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
-            const bool ok = elig(kl);
-            wge |= (ok && acc[e] >= slo[rb2]) ? 1u << kl : 0u;
-            wgt |= (ok && acc[e] > shi[rb2]) ? 1u << kl : 0u;
-            if (TOPP && ref[rb2] >= 0.0 && ok && acc[e] > shi[rb2])
+          for (int e = 15; e >= 0; --e) {
+            uint64_t ge = lanes_ge(acc[e], slo[rb2]), gt = lanes_gt(acc[e], shi[rb2]);
+            if (!all_elig) {
+              const uint64_t ok = lanes_lt(16 * g + e, lim);
+              ge &= ok;
+              gt &= ok;
+            }
+            wge = shift_in(wge, ge);
+            wgt = shift_in(wgt, gt);
+            if (TOPP && ref[rb2] >= 0.0 && elig(16 * g + e) && acc[e] > shi[rb2])
               macc[rb2] += static_cast<double>(__builtin_amdgcn_exp2f((acc[e] - smax[rb2]) * tl2));
           }
           nacc[rb2] += static_cast<uint32_t>(__builtin_popcount(wgt));
           const uint32_t ins = wge & ~wgt;
-          const uint32_t w = wge | __shfl_xor(wge, 32);
+          const uint32_t wl = wge << (16 * g);
+          const uint32_t w = wl | __shfl_xor(wl, 32);
           if (g == 0) p.bsel[(row0 + rb2 * 32 + ln) * p.W + kb / 32] = w;
           if (__any(ins != 0u)) {
             // The lane's scores go through LDS so that a candidate's score can
@@ -559,9 +588,10 @@ void k_score_pass(SelParams p) {
               uint32_t rank = atomicAdd(&s_ccnt[rl], static_cast<uint32_t>(__builtin_popcount(ins)));
               uint32_t lo_k = 0xFFFFFFFFu, hi_k = 0u;
               for (uint32_t m = ins; m; m &= m - 1u) {
-                const int kl = __builtin_ctz(m);
-                const uint32_t okey = ord_key(sc[4 * ((kl >> 3) ^ csw) + (kl & 3)]);
-                const uint64_t entry = (static_cast<uint64_t>(okey) << 32) | (~static_cast<uint32_t>(kb + kl));
+                const int e = __builtin_ctz(m);
+                const uint32_t okey = ord_key(sc[4 * ((e >> 2) ^ csw) + (e & 3)]);
+                const uint64_t entry =
+                    (static_cast<uint64_t>(okey) << 32) | (~static_cast<uint32_t>(kb + 16 * g + e));
                 lo_k = min(lo_k, okey);
                 hi_k = max(hi_k, okey);
                 if (rank++ < kStage) {
@@ -582,7 +612,7 @@ void k_score_pass(SelParams p) {
           uint32_t wsel = 0u, wtie = 0u;
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
-            const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+            const int kl = 16 * g + e;
             const bool ok = elig(kl);
             wsel |= (ok && acc[e] > ts[rb2]) ? 1u << kl : 0u;
             const bool tie = tiei[rb2] ? (acc[e] >= slo[rb2] && acc[e] <= shi[rb2])
@@ -602,7 +632,7 @@ void k_score_pass(SelParams p) {
         const int rl = rb2 * 32 + ln;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+          const int kl = 16 * g + e;
           const float sc = acc[e];
           const bool ok = elig(kl);
           bool above = false, inside = ok;
@@ -808,7 +838,7 @@ __global__ __launch_bounds__(kThreads) void k_sample_bracket(SelParams p) {
       const int lim = Lr[rb2] - kb;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+        const int kl = 16 * g + e;
         const float sc = kl < lim ? acc[e] : 0.0f;
         m1[rb2] += sc;
         m2[rb2] = __builtin_fmaf(sc, sc, m2[rb2]);
@@ -880,7 +910,7 @@ __global__ __launch_bounds__(kThreads) void k_sample_bracket(SelParams p) {
       const int lim = Lr[rb2] - kb;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+        const int kl = 16 * g + e;
         const int bn = kl < lim ? bin_of(acc[e], bmul[rb2], badd[rb2], kSampleBins) : kSampleBins;
         atomicAdd(&s_hist[bn * kRowsWG + rb2 * 32 + ln], 1u);
       }
@@ -1056,8 +1086,8 @@ __global__ __launch_bounds__(kThreads) void k_mins_tiled(SelParams p) {
     const int kb = key0 + blk * 32;
 #pragma unroll
     for (int rb2 = 0; rb2 < 2; ++rb2) {
-      // Raw scores of keys kl = 8 (e / 4) + 4 g + e % 4 of the block (keys
-      // 0-15, the first 16-key tile, are e < 8).
+      // Raw scores of keys kl = 16 g + e of the block (with 16-key tiles,
+      // lane group g holds tile g).
       f32x16 acc = f32x16{};
 #pragma unroll
       for (int s2 = 0; s2 < DS; ++s2)
@@ -1069,36 +1099,42 @@ __global__ __launch_bounds__(kThreads) void k_mins_tiled(SelParams p) {
         float tm = kNegInf;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
+          const int kl = 16 * g + e;
           if (kl < lim) tm = fmaxf(tm, acc[e]);
         }
         m[rb2] = fmaxf(m[rb2], tm);
         continue;
       }
-      uint32_t w = 0u;
-      auto do_tile = [&](const int e0, const int ne, const int toff) __attribute__((always_inline)) {
-        float tm = kNegInf;
+      float tm = kNegInf;  // this lane's 16 keys
 #pragma unroll
-        for (int e = e0; e < e0 + ne; ++e) {
-          const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
-          if (kl < lim) tm = fmaxf(tm, acc[e]);
-        }
-        tm = fmaxf(tm, __shfl_xor(tm, 32));
+      for (int e = 0; e < 16; ++e) {
+        const int kl = 16 * g + e;
+        if (kl < lim) tm = fmaxf(tm, acc[e]);
+      }
+      const float tm_x = __shfl_xor(tm, 32);  // the other lane group's
+      // The running maximum through the tile starting at key toff of the block
+      // (both lanes of a row compute the same values).
+      auto advance = [&](const float tmax, const int toff) __attribute__((always_inline)) {
         const bool fresh = (static_cast<uint32_t>(kb + toff) & gmask) == 0u;  // a group starts
-        const float mn = fmaxf(fresh ? kNegInf : m[rb2], tm);
+        const float mn = fmaxf(fresh ? kNegInf : m[rb2], tmax);
         if (__any(mn != m[rb2])) thr[rb2] = tiled_threshold(mn, a_raw);
         m[rb2] = mn;
-#pragma unroll
-        for (int e = e0; e < e0 + ne; ++e) {
-          const int kl = 8 * (e >> 2) + 4 * g + (e & 3);
-          w |= (kl < lim && acc[e] >= thr[rb2]) ? 1u << kl : 0u;
-        }
       };
+      float my_thr;
       if (two_tiles) {
-        do_tile(0, 8, 0);
-        do_tile(8, 8, 16);
+        advance(g ? tm_x : tm, 0);  // tile 0: keys 0-15, lane group 0
+        const float thr0 = thr[rb2];
+        advance(g ? tm : tm_x, 16);  // tile 1: keys 16-31, lane group 1
+        my_thr = g ? thr[rb2] : thr0;
       } else {
-        do_tile(0, 16, 0);
+        advance(fmaxf(tm, tm_x), 0);
+        my_thr = thr[rb2];
+      }
+      uint32_t w = 0u;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int kl = 16 * g + e;
+        w |= (kl < lim && acc[e] >= my_thr) ? 1u << kl : 0u;
       }
       w |= __shfl_xor(w, 32);
       if (g == 0) p.bsel[(row0 + rb2 * 32 + ln) * p.W + kb / 32] = w;

@@ -1,7 +1,8 @@
 // Vector-sparse attention (paper Eq. 4, Sec. 3.2; appendix Algorithm 2) for gfx950.
 //
-// One workgroup (4 waves) owns up to 64 query rows of one query block of one
-// head and walks the block's index list I[b,h,i,0:C) in tiles of 64 keys
+// One workgroup owns up to 64 query rows (4 waves) or, for blocks of a
+// multiple of 128 rows, up to 128 (8 waves) of one query block of one head and
+// walks the block's index list I[b,h,i,0:C) in tiles of 64 keys
 // (starting at the tile where the workgroups running on its XCD are, and
 // wrapping around; see below).  Blocks are dealt to groups of XCDs sized so
 // that the heads swept at once fit the last-level cache (xcd_group).
@@ -12,8 +13,8 @@
 // free of bank conflicts.  The waves compute S^T = K_tile Q^T and
 // O^T += V_tile^T P^T with v_mfma_f32_32x32x16_bf16 and keep the
 // online-softmax state in registers.  Wave w = (rw, kw): rw picks 32 of the
-// 64 query rows, kw picks 32 of the 64 keys of each tile; the two key halves
-// are merged at the end.
+// workgroup's query rows, kw picks 32 of the 64 keys of each tile; the two
+// key halves are merged at the end.
 //
 // MFMA 32x32x16 lane layout (lane l, g = l / 32):
 //   A (M x K): lane holds row l % 32, K-slots 8g .. 8g + 7
@@ -32,10 +33,7 @@
 namespace vecattn {
 namespace {
 
-constexpr int kRows = 64;     // query rows per workgroup
 constexpr int kTile = 64;     // keys per gathered tile
-constexpr int kThreads = 256;
-constexpr int kStages = 2;
 // Tiles processed by this kernel on each XCD since the library was loaded
 // (wraps at 2^32).  It paces the tile order below: a locality hint only, so
 // concurrent calls sharing it affect speed, never results.
@@ -92,9 +90,11 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 // SAME_STRIDE: K and V rows have the same stride, so a gathered row's K and V
-// offsets coincide.
-template <int D, bool SAME_STRIDE>
-__global__ __launch_bounds__(kThreads) void k_sparse_attn(
+// offsets coincide.  ROWS: query rows per workgroup (64: 4 waves, or 128: 8
+// waves, for blocks of a multiple of 128 rows, so that one gather of a tile
+// serves all 128 rows of the block).
+template <int D, bool SAME_STRIDE, int ROWS>
+__global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
     const uint16_t* __restrict__ q, int64_t q_sB, int64_t q_sH, int64_t q_sN,
     const uint16_t* __restrict__ k, int64_t k_sB, int64_t k_sH, int64_t k_sN,
     const uint16_t* __restrict__ v, int64_t v_sB, int64_t v_sH, int64_t v_sN,
@@ -103,6 +103,8 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
     int32_t group, int32_t N, int32_t P, int32_t Np, int32_t chunks, int32_t causal,
     float scale_log2, int64_t total, int64_t per_xcd, int32_t xgroup, int32_t herd_slots) {
   constexpr int CH = D / 8;                 // 16-byte chunks per row
+  constexpr int kThreads = 4 * ROWS;  // 2 key halves x ROWS / 32 row groups, 64 lanes each
+  constexpr int RG = ROWS / 32;             // row groups (waves per key half)
   constexpr int U = kTile * CH / kThreads;  // direct-load instructions per wave per matrix
   constexpr int DS = D / 16;                // MFMA K-steps over the head dimension
   constexpr int DB = D / 32;                // 32-wide blocks of the head dimension
@@ -116,6 +118,7 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
   __shared__ __align__(16) uint16_t v_s1[kTile * D];
   __shared__ __align__(16) int32_t id_s0[kTile];
   __shared__ __align__(16) int32_t id_s1[kTile];
+  __shared__ float s_ml[RG][128];  // (m, l) of the kw = 1 waves for the merge
   // Stage selectors; always called with a constant stage, so they fold to a
   // direct reference to one LDS object.
   auto kbuf = [&](int st) __attribute__((always_inline)) { return st ? k_s1 : k_s0; };
@@ -146,8 +149,8 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
   const int h = static_cast<int>(bh % Hq);
   const int hk = h / group;
 
-  const int row0 = i * P + chunk * kRows;
-  const int row_end = min(N, min(i * P + P, row0 + kRows));
+  const int row0 = i * P + chunk * ROWS;
+  const int row_end = min(N, min(i * P + P, row0 + ROWS));
   const int count = __builtin_amdgcn_readfirstlane(
       static_cast<int>(min<int64_t>(max(counts[bh * Np + i], 0), cap)));
   const int32_t* list = idx + (bh * Np + i) * cap;
@@ -204,8 +207,8 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
   const int lane = tid & 63;
   const int g = lane >> 5;
   const int ln = lane & 31;
-  const int rw = wave & 1;
-  const int kw = wave >> 1;
+  const int rw = wave % RG;
+  const int kw = wave / RG;
 
   // Q^T operand: this lane's query row, head-dim slots 16s + 8g .. +7.
   const int my_row = row0 + 32 * rw + ln;
@@ -417,9 +420,9 @@ __global__ __launch_bounds__(kThreads) void k_sparse_attn(
   l_run += __shfl_xor(l_run, 32);
   wait_vmcnt<0>();  // no gather may still be landing in the buffers reused below
   __syncthreads();
-  // Reuse the tile buffers: O of row half rw in k_s0 / v_s0, (m, l) in k_s1.
-  float* red_o = reinterpret_cast<float*>(rw ? v_s0 : k_s0);
-  float* red_ml = reinterpret_cast<float*>(k_s1) + rw * 128;
+  // Reuse the tile buffers (each holds one row group's 32 x D fp32 O).
+  float* red_o = reinterpret_cast<float*>(rw == 0 ? k_s0 : rw == 1 ? v_s0 : rw == 2 ? k_s1 : v_s1);
+  float* red_ml = s_ml[rw];
   if (kw == 1) {
 #pragma unroll
     for (int db = 0; db < DB; ++db)
@@ -486,7 +489,10 @@ hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream) {
   const int64_t B = a.q.B, Hq = a.q.H, N = a.q.N, D = a.q.D;
   const int32_t P = a.block;
   const int32_t Np = static_cast<int32_t>((N + P - 1) / P);
-  const int32_t chunks = (P + kRows - 1) / kRows;
+  // 128 rows per workgroup when blocks come in multiples of 128 rows (one
+  // gather of a tile then serves the whole block), else 64.
+  const int32_t rows = P % 128 == 0 ? 128 : 64;
+  const int32_t chunks = (P + rows - 1) / rows;
   const int64_t blocks = B * Hq * static_cast<int64_t>(Np);
   const int64_t total = blocks * chunks;
   if (total == 0) return hipSuccess;
@@ -506,18 +512,23 @@ hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream) {
     int dev = 0, cus = 0, per_cu = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0);
+    const int threads = 4 * rows;
+    if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0);
     if (e != hipSuccess) return e;
     const int32_t slots = max(1, per_cu * cus / 8);
-    hipLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, stream, q, a.q.sB, a.q.sH, a.q.sN, k,
+    hipLaunchKernelGGL(kernel, grid, dim3(threads), 0, stream, q, a.q.sB, a.q.sH, a.q.sN, k,
                        a.k.sB, a.k.sH, a.k.sN, v, a.v.sB, a.v.sH, a.v.sN, o, a.o_sB, a.o_sH,
                        a.o_sN, a.lse, a.idx, a.counts, a.cap, static_cast<int32_t>(Hq), group,
                        static_cast<int32_t>(N), P, Np, chunks, a.causal, scale_log2, total,
                        per_xcd, xgroup, slots);
     return hipGetLastError();
   };
-  if (D == 128) return same ? launch(k_sparse_attn<128, true>) : launch(k_sparse_attn<128, false>);
-  return same ? launch(k_sparse_attn<64, true>) : launch(k_sparse_attn<64, false>);
+  if (rows == 128) {
+    if (D == 128) return same ? launch(k_sparse_attn<128, true, 128>) : launch(k_sparse_attn<128, false, 128>);
+    return same ? launch(k_sparse_attn<64, true, 128>) : launch(k_sparse_attn<64, false, 128>);
+  }
+  if (D == 128) return same ? launch(k_sparse_attn<128, true, 64>) : launch(k_sparse_attn<128, false, 64>);
+  return same ? launch(k_sparse_attn<64, true, 64>) : launch(k_sparse_attn<64, false, 64>);
 }
 
 }  // namespace vecattn

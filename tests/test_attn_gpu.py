@@ -83,6 +83,9 @@ CASES = [
     (1, 3, 3, 400, 64, 16, True, 150, 150),
     (1, 2, 1, 500, 128, 128, False, 300, 320),
     (1, 2, 2, 190, 128, 48, True, 190, 190),
+    # 128-row workgroups (8 waves): causal with D = 64, and two per 256-row block
+    (1, 2, 2, 300, 64, 128, True, 300, 300),
+    (1, 2, 1, 600, 128, 256, True, 600, 600),
 ]
 
 

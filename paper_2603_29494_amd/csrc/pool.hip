@@ -29,14 +29,25 @@ __global__ __launch_bounds__(256) void k_pool(const uint16_t* __restrict__ q, in
   double acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] = 0.0;
-  for (int r = r0; r < r1; ++r) {
-    const u32x4 w = *reinterpret_cast<const u32x4*>(base + static_cast<int64_t>(r) * q_sN);
+  auto add_row = [&](const u32x4 w) __attribute__((always_inline)) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       acc[2 * e] += static_cast<double>(bf16_bits_to_f32(w[e] & 0xFFFFu));
       acc[2 * e + 1] += static_cast<double>(bf16_bits_to_f32(w[e] >> 16));
     }
+  };
+  // Eight rows are loaded before any is summed, so that a thread keeps eight
+  // loads in flight; the sums still run in row order.
+  int r = r0;
+  for (; r + 8 <= r1; r += 8) {
+    u32x4 w[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      w[j] = *reinterpret_cast<const u32x4*>(base + static_cast<int64_t>(r + j) * q_sN);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) add_row(w[j]);
   }
+  for (; r < r1; ++r) add_row(*reinterpret_cast<const u32x4*>(base + static_cast<int64_t>(r) * q_sN));
   const double n = static_cast<double>(r1 - r0);
   u32x4 out;
 #pragma unroll

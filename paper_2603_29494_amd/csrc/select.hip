@@ -96,6 +96,10 @@ struct RowState {
   double ref;       // softmax reference (an upper bound of the row's scores)
   double Z;         // total mass (topP)
   double pZ;        // p * Z
+  // topP: bounds of the mass of the keys above the current interval, from the
+  // per-bin sums of level 0 and the edge bounds of later levels (exact only in
+  // the collect pass, which sums it again).
+  double mab_lo, mab_hi;
 };
 
 struct SelParams {
@@ -345,6 +349,8 @@ __global__ __launch_bounds__(256) void k_sel_init(SelParams p, int round) {
   s.k_eq = 0;
   s.tie_interval = 0;
   s.mins = p.mode_mins && round == 0;
+  s.mab_lo = 0.0;
+  s.mab_hi = 0.0;
   p.cand_n[r] = 0;
   p.cand_lohi[2 * r] = 0xFFFFFFFFu;
   p.cand_lohi[2 * r + 1] = 0u;
@@ -381,12 +387,13 @@ __global__ __launch_bounds__(256) void k_kmax_init(float* kmax, int n) {
 // ---------------------------------------------------------------------------
 // TOPP: the launch selects by mass (rows restarted as topK(cap) may be mixed
 // in); otherwise no mass is computed.
-// topK / minS histogram passes are held to 168 VGPRs so that three waves share
+// Histogram passes without per-bin masses (every level of topK / minS rows,
+// levels >= 1 of topP rows) are held to 168 VGPRs so that three waves share
 // each SIMD (their 33 KB of LDS allows it): the latency of the K loads and of the
 // MFMA chains is then hidden better (~5% of the selection at the 75k DiT layer).
 template <int D, int MODE, bool TOPP>
 __global__ __launch_bounds__(kThreads)
-__attribute__((amdgpu_waves_per_eu(((MODE == MODE_HIST || MODE == MODE_HIST0) && !TOPP) ? 3 : 1)))
+__attribute__((amdgpu_waves_per_eu((MODE == MODE_HIST || (MODE == MODE_HIST0 && !TOPP)) ? 3 : 1)))
 void k_score_pass(SelParams p) {
   constexpr int DS = D / 16;
   constexpr bool HIST = MODE == MODE_HIST || MODE == MODE_HIST0;
@@ -398,11 +405,16 @@ void k_score_pass(SelParams p) {
   // interval, so that every key can be counted without a branch.
   constexpr int NB = kBins;
   constexpr int HS = NB + 1;  // bins per row including the spare one
-  // topP HIST passes also sum each bin's softmax mass (terms exp2((s - row
-  // max) tau log2 e) <= 1 in fixed point), which pins the cut to one or two
-  // bins per level: one 64-bit integer atomic per key carries both the count
-  // and the mass (LDS float atomics are far slower).
-  constexpr bool MH = HIST && TOPP;
+  // The level-0 topP pass also sums each bin's softmax mass (terms exp2((s -
+  // row max) tau log2 e) <= 1 in fixed point), which pins the cut to one or
+  // two bins: one 64-bit integer atomic per key carries both the count and the
+  // mass (LDS float atomics are far slower).  Later levels split one such bin
+  // into bins so narrow that the mass bounds from their score edges suffice;
+  // they count keys only, and the mass above their interval is carried from
+  // the levels before (bounds in the row state), so no key's mass is computed
+  // there.
+  constexpr bool MH = MODE == MODE_HIST0 && TOPP;
+  constexpr bool MASS = MODE != MODE_HIST && TOPP;  // this pass computes key masses
   __shared__ uint32_t s_hist[HIST && !MH ? kRowsWG * HS : 1];
   __shared__ uint64_t s_hist64[MH ? kRowsWG * HS : 1];
   __shared__ double s_zred[4][kRowsWG];
@@ -644,8 +656,8 @@ void k_score_pass(SelParams p) {
           // topP: the key's softmax term relative to the row maximum, exp(tau
           // s - ref) with ref = tau * max (terms below 2^-126, a share of the
           // mass far below any tolerance, may flush to 0)
-          const float mt = TOPP ? __builtin_amdgcn_exp2f((sc - smax[rb2]) * tl2) : 0.0f;
-          if (TOPP && ref[rb2] >= 0.0 && ok) {
+          const float mt = MASS ? __builtin_amdgcn_exp2f((sc - smax[rb2]) * tl2) : 0.0f;
+          if (MASS && ref[rb2] >= 0.0 && ok) {
             if (MODE == MODE_HIST0) zacc[rb2] += static_cast<double>(mt);
             if (above) macc[rb2] += static_cast<double>(mt);
           }
@@ -1232,11 +1244,11 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
   const int i_last = min(p.Np, (rb + 1) * kRowsWG) - 1;
   const int Ltile = eligible(i_last, p.P, p.N, p.causal);
   const int ns = (Ltile + p.split - 1) / p.split;
+  // (The mass above the interval of topP rows is carried in the row state.)
   uint32_t nab = 0;
-  double mab = 0.0, z = 0.0;
+  double z = 0.0;
   for (int q = 0; q < ns; ++q) {
     nab += p.n_above[r * p.nsplit + q];
-    mab += p.m_above[r * p.nsplit + q];
     if (level == 0) z += p.zpart[r * p.nsplit + q];
   }
   // Count cut (topK, and minS rows over cap) across the wave: lane l holds
@@ -1308,19 +1320,21 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
     above_bins = static_cast<uint32_t>(cut_above);
   } else {
     // Mass bounds per bin: from its score range (count times the mass at
-    // each edge), and from its mass sum -- the terms exp(tau s - ref) <= 1,
-    // each within a relative (2 + |x|) 2^-22 (exp2 and the rounding of its
-    // argument x = (s - max) tau log2 e, |x| bounded by the bin's lower
+    // each edge) and, at level 0, from its mass sum -- the terms exp(tau s -
+    // ref) <= 1, each within a relative (2 + |x|) 2^-22 (exp2 and the rounding
+    // of its argument x = (s - max) tau log2 e, |x| bounded by the bin's lower
     // edge), rounded to the 2^-31 grid (<= 2^-32 each) and summed exactly.
-    // The cut bin range runs from the first bin the cut for T may lie in
-    // down to the last one the cut for T - kTopPMassSlack * Z may lie in:
-    // usually one bin.
-    const double T = s.pZ - mab;
-    const double Trel = T - kTopPMassSlack * s.Z;
+    // Later levels split one level-0 bin 128 ways, so that the edge bounds
+    // of a bin differ by a factor of ~1.003 at most.  The mass above the
+    // interval lies in [mab_lo, mab_hi].  The cut bin range runs from the
+    // first bin the cut for T may lie in down to the last one the cut for
+    // T - kTopPMassSlack * Z may lie in: usually one bin.
+    const double T_lo = s.pZ - s.mab_hi;
+    const double Trel = s.pZ - s.mab_lo - kTopPMassSlack * s.Z;
     const float k1 = p.tau * 1.4426950408889634f;
     const float w = 1.0f / inv;
     const float slop = fabsf(w) * 1e-3f + fabsf(lo) * 1e-6f;
-    double before_lo = 0.0, before_hi = 0.0;
+    double before_lo = 0.0, before_hi = 0.0, cut_lo = 0.0, cut_hi = 0.0;
     int top_nonempty = -1;
     for (int bn = nb - 1; bn >= 0; --bn) {
       if (hs[bn] == 0) continue;
@@ -1329,14 +1343,21 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
       float e_hi = lo + static_cast<float>(bn + 1) * w + slop;
       if (level == 0 && bn == 0) e_lo = -FLT_MAX;
       if (level == 0 && bn == nb - 1) e_hi = top;
-      const double grid = static_cast<double>(hs[bn]) * 0x1p-32;
-      const double xmax = (static_cast<double>(s.smax) - static_cast<double>(e_lo)) * k1;
-      const double eps = fmin(1.0, (2.0 + xmax) * 0x1p-22);
-      const double mlo = fmax(hs[bn] * mass_term(e_lo, p.tau, s.ref), hm[bn] * (1.0 - eps) - grid);
-      const double mhi = fmin(hs[bn] * mass_term(fminf(e_hi, top), p.tau, s.ref),
-                              hm[bn] * (1.0 + eps) + grid);
+      double mlo = hs[bn] * mass_term(e_lo, p.tau, s.ref);
+      double mhi = hs[bn] * mass_term(fminf(e_hi, top), p.tau, s.ref);
+      if (level == 0) {
+        const double grid = static_cast<double>(hs[bn]) * 0x1p-32;
+        const double xmax = (static_cast<double>(s.smax) - static_cast<double>(e_lo)) * k1;
+        const double eps = fmin(1.0, (2.0 + xmax) * 0x1p-22);
+        mlo = fmax(mlo, hm[bn] * (1.0 - eps) - grid);
+        mhi = fmin(mhi, hm[bn] * (1.0 + eps) + grid);
+      }
       if (bb < 0) {
-        if (before_hi + mhi >= T) bb = ba = bn;  // the mass through bn may reach T
+        if (before_hi + mhi >= T_lo) {  // the mass through bn may reach T
+          bb = ba = bn;
+          cut_lo = before_lo;
+          cut_hi = before_hi;
+        }
       } else if (before_lo < Trel) {
         ba = bn;  // the mass above bn may still fall short of T - slack
       } else {
@@ -1349,6 +1370,8 @@ __global__ __launch_bounds__(64) void k_resolve_hist(SelParams p, int level) {
     if (bb < 0) {  // T <= 0 or rounding: the cut is at the top of the interval
       bb = ba = top_nonempty >= 0 ? top_nonempty : 0;
     }
+    s.mab_lo += cut_lo;  // the bins above bb join the mass above the interval
+    s.mab_hi += cut_hi;
   }
   uint32_t inside = 0;
   for (int bn = ba; bn <= bb; ++bn) inside += hs[bn];

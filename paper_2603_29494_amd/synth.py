@@ -57,9 +57,10 @@ def _seed(cid: int) -> int:
 # (u a unit vector) add gamma*beta/sqrt(D) to the score.  mu (the planted
 # columns' logit boost) of the two topP workloads was set by bisection on mu,
 # measuring the mean share of eligible keys the CPU oracle's topP selection
-# keeps on seeded random blocks: for the Hunyuan-shaped DiT, 8 blocks of each
-# of its 24 heads, mu = 4.67 -> mean keep 0.378 (per-head means 0.10 to 0.75,
-# from the heads' planted densities of 1% to 8%); for the long VLM prefill, 48
+# keeps on seeded random blocks: for the Hunyuan-shaped DiT, 64 blocks of each
+# of its 24 heads, mu = 4.745 -> mean keep 0.379 (per-head means 0.14 to 0.75,
+# from the heads' planted densities of 1% to 8%; 8 blocks per head had put the
+# mean 0.02 low); for the long VLM prefill, 48
 # blocks of 3 heads, mu = 8 -> median keep ~2%, mean ~18% (blocks whose local
 # window holds most of the mass keep far more).
 WORKLOADS: Dict[int, Workload] = {
@@ -74,7 +75,7 @@ WORKLOADS: Dict[int, Workload] = {
     4: Workload(4, "dit_wan_75k", 1, 40, 40, 75600, 128, False, 64, "topk", 0.15, _seed(4),
                 dict(planted_frac=0.04, key_shift_sqrtd=2.0, frame=3600, frame_sigma=0.5)),
     5: Workload(5, "dit_hunyuan_119k", 1, 24, 24, 118800, 128, False, 128, "topp", 0.9, _seed(5),
-                dict(dens_lo=0.01, dens_hi=0.08, mu=4.67, query_shift=1.0)),
+                dict(dens_lo=0.01, dens_hi=0.08, mu=4.745, query_shift=1.0)),
 }
 
 

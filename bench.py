@@ -234,7 +234,8 @@ def main():
         "selection_hbm_pct": round(100.0 * bytes_sel / (sel_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 2),
         "achieved_keep": round(keep, 6),
         "roofline": {"bound": "mfma",
-                     "kernel": f"k_sparse_attn<{D}, {'true' if k.stride() == v.stride() else 'false'}>",
+                     "kernel": f"k_sparse_attn<{D}, {'true' if k.stride() == v.stride() else 'false'}, "
+                               f"{128 if w.block % 128 == 0 else 64}>",
                      "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": recorded_traffic(w.name)},

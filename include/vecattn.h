@@ -18,9 +18,10 @@
  *     frees or synchronises; every call is asynchronous on `stream` (a
  *     hipStream_t; NULL means the default stream), and calls on different
  *     streams may run concurrently.  The only state kept between calls is a
- *     per-process, per-device locality counter of vecattn_sparse_attn (tiles
- *     processed per XCD, which paces the order in which a workgroup walks its
- *     list): concurrent calls share it, which changes their speed and the
+ *     per-process, per-device locality counter of vecattn_sparse_attn (the
+ *     progress of the workgroups on each XCD through their lists, which paces
+ *     the order in which a workgroup walks its list): concurrent calls share
+ *     it, which changes their speed and the
  *     order of the softmax sums (the last bits of O), never which keys are
  *     attended.
  *   - Q, K, V, O are bf16 with logical shape [B, H, N, D] described by a

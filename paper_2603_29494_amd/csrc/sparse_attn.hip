@@ -34,13 +34,15 @@ namespace vecattn {
 namespace {
 
 constexpr int kTile = 64;     // keys per gathered tile
-// Tiles processed by this kernel on each XCD since the library was loaded
-// (wraps at 2^32).  It paces the tile order below: a locality hint only, so
-// concurrent calls sharing it affect speed, never results.
-__device__ unsigned int g_herd_tiles[8];
-// Tiles counted per update of that counter: updates to one address serialise
-// in L2, so they must be rare next to the gathers.
-constexpr unsigned int kHerdBatch = 16;
+// Progress of this kernel's workgroups on each XCD since the library was
+// loaded, in units of 1/kHerdUnit of a list (wraps at 2^32).  It paces the
+// tile order below: a locality hint only, so concurrent calls sharing it
+// affect speed, never results.
+__device__ unsigned int g_herd[8];
+constexpr int kHerdUnit = 4096;
+// Tiles per update of that counter: updates to one address serialise in L2,
+// so they must be rare next to the gathers.
+constexpr int kHerdBatch = 16;
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
@@ -158,24 +160,31 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
   // Tile order.  A block's keys are random rows of the head's K/V, far more
   // than an XCD's L2 holds; the workgroups running together on an XCD share
   // L2 hits only if they gather from the same key range at the same time.
-  // Lists are ascending, so a workgroup's position in its list is a position
-  // in key space.  Every workgroup counts its tiles into its XCD's counter;
-  // that count over the XCD's workgroup slots is the mean position of the
-  // workgroups running there, and a new workgroup starts at that tile (then
-  // wraps around), so the workgroups on an XCD sweep the keys together at
-  // their actual pace.  The order of the tiles changes only the order of the
-  // softmax sums (results can differ between runs within fp32 rounding).
+  // Lists are ascending, so the fraction of its list a workgroup has walked
+  // is a position in key space (the same for lists of different lengths).
+  // Every workgroup adds its progress, in 1/kHerdUnit of its list, to its
+  // XCD's counter; that sum over the XCD's workgroup slots is the mean
+  // position of the workgroups running there, and a new workgroup starts at
+  // the tile at that fraction of its own list (then wraps around), so the
+  // workgroups on an XCD sweep the keys together at their actual pace.  The
+  // order of the tiles changes only the order of the softmax sums (results
+  // can differ between runs within fp32 rounding).
   const int xcd = blockIdx.x & 7;  // the hardware deals workgroup x to XCD x % 8
   __shared__ int s_rot;
   if (threadIdx.x == 0) {
     const unsigned int herd =
-        __hip_atomic_load(&g_herd_tiles[xcd], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    s_rot = ntiles > 1 ? static_cast<int>((herd / static_cast<unsigned int>(herd_slots)) %
-                                          static_cast<unsigned int>(ntiles))
-                       : 0;
+        __hip_atomic_load(&g_herd[xcd], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned int pos = (herd / static_cast<unsigned int>(herd_slots)) % kHerdUnit;
+    // ntiles < 2^18 (N < 2^24), so the product fits 32 bits.
+    s_rot = static_cast<int>((pos * static_cast<unsigned int>(ntiles)) / kHerdUnit);
   }
   __syncthreads();
   const int t_rot = __builtin_amdgcn_readfirstlane(s_rot);
+  // Progress after t tiles, in 1/kHerdUnit of the list (a whole list adds up
+  // to kHerdUnit exactly).
+  auto herd_units = [&](int t) __attribute__((always_inline)) {
+    return static_cast<unsigned int>((kHerdUnit * t) / ntiles);
+  };
   auto tile_of = [&](int t) __attribute__((always_inline)) {  // t-th tile processed
     if (t >= ntiles) return t;  // past the list (reads 0)
     const int x = t + t_rot;
@@ -285,8 +294,8 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
     wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
     if (wave == 0 && lane == 0 && (t % kHerdBatch) == kHerdBatch - 1)
-      __hip_atomic_fetch_add(&g_herd_tiles[xcd], kHerdBatch, __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_fetch_add(&g_herd[xcd], herd_units(t + 1) - herd_units(t + 1 - kHerdBatch),
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (t + 1 < ntiles) issue_tile(t + 1, st ^ 1);
     load_ids(t + 2);  // past the list these read 0
 
@@ -413,7 +422,7 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
   }
 
   if (wave == 0 && lane == 0 && ntiles % kHerdBatch != 0)
-    __hip_atomic_fetch_add(&g_herd_tiles[xcd], static_cast<unsigned int>(ntiles) % kHerdBatch,
+    __hip_atomic_fetch_add(&g_herd[xcd], kHerdUnit - herd_units(ntiles - ntiles % kHerdBatch),
                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
   // Merge the two key halves (kw = 1 hands its state to kw = 0 through LDS).

@@ -8,8 +8,9 @@ tensors with planted vertical structure (paper_2603_29494_amd.synth, workload
 4); the paper's model activations are not available.
 
 A step = vecattn_select (pooling, scoring, topK; lists without the -1 padding
-past each count, which the attention never reads) + vecattn_sparse_attn over
-all heads, inputs resident in HBM.  Timing: HIP events on the launch stream around
+past each count, which the attention never reads) + vecattn_attn_order (the
+order in which the attention takes each head's blocks) +
+vecattn_sparse_attn_ordered over all heads, inputs resident in HBM.  Timing: HIP events on the launch stream around
 each call.  The W warm-up steps run back to back (their last ones give the
 warm-cache figures); each of the K timed steps starts cold: a 1 GiB scratch
 buffer is written just before it (outside its events), evicting the 256 MB
@@ -143,6 +144,7 @@ def main():
     counts = torch.empty((B, Hq, Np), dtype=torch.int32, device=dev)
     ws = torch.empty(va.workspace_bytes(q, k, P, w.causal, mode, cap), dtype=torch.uint8, device=dev)
     out = torch.empty_like(q)
+    order = torch.empty((B, Hq, Np), dtype=torch.int32, device=dev)
     stream = torch.cuda.current_stream(dev)
 
     scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev)   # cache eviction
@@ -152,11 +154,13 @@ def main():
         va.select(q, k, P, mode, w.param, w.causal, cap=cap, idx=idx, counts=counts, workspace=ws,
                   unpadded=True)
         ev[1].record(stream)
-        va.sparse_attn(q, k, v, idx, counts, P, w.causal, out=out)
+        va.attn_order(idx, counts, N, P, out=order)
         ev[2].record(stream)
+        va.sparse_attn(q, k, v, idx, counts, P, w.causal, out=out, order=order)
+        ev[3].record(stream)
 
     def new_events(n):
-        return [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n)]
+        return [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n)]
 
     warm_ev = new_events(args.warmup)
     for s in range(args.warmup):          # back to back: warm caches
@@ -173,18 +177,19 @@ def main():
 
     def stats(evs):
         sel = np.array([e[0].elapsed_time(e[1]) for e in evs])
-        att = np.array([e[1].elapsed_time(e[2]) for e in evs])
-        lay = sel + att
-        return sel, att, lay
+        odr = np.array([e[1].elapsed_time(e[2]) for e in evs])
+        att = np.array([e[2].elapsed_time(e[3]) for e in evs])
+        lay = np.array([e[0].elapsed_time(e[3]) for e in evs])
+        return sel, odr, att, lay
 
-    sel_all, attn_all, layer_all = stats(events)
+    sel_all, order_all, attn_all, layer_all = stats(events)
     sel_ms = float(np.median(sel_all))
     attn_ms = float(np.median(attn_all))
     layer_ms = float(np.median(layer_all))
     attn_mean_ms = float(np.mean(attn_all))    # the roofline's launch average
     warm = None
     if args.warmup >= 3:                  # the warm-up steps after the first two
-        ws_, wa_, wl_ = stats(warm_ev[2:])
+        ws_, _, wa_, wl_ = stats(warm_ev[2:])
         warm = {"ms_per_step_median": round(float(np.median(wl_)), 4),
                 "ms_select_median": round(float(np.median(ws_)), 4),
                 "ms_attention_median": round(float(np.median(wa_)), 4), "steps": len(wl_)}
@@ -225,6 +230,7 @@ def main():
         "ms_per_step_max": round(float(layer_all.max()), 4),
         "ms_select": round(sel_ms, 4),
         "ms_select_min_max": [round(float(sel_all.min()), 4), round(float(sel_all.max()), 4)],
+        "ms_order": round(float(np.median(order_all)), 4),
         "ms_attention": round(attn_ms, 4),
         "ms_attention_min_max": [round(float(attn_all.min()), 4), round(float(attn_all.max()), 4)],
         "selection_pct": round(100.0 * sel_ms / layer_ms, 2),

@@ -262,6 +262,51 @@ vecattn_status vecattn_sparse_attn(const void* q, const vecattn_tdesc* qd, const
                                    const vecattn_tdesc* od, float* lse, void* stream);
 
 /*
+ * Block schedule for vecattn_sparse_attn_ordered.  Eq. 4 and Algorithm 2 treat
+ * the query blocks independently, so the order in which the attention takes
+ * them changes only its speed.  This call orders the N_p blocks of each
+ * (b, h) by:
+ *   1. count C[b,h,i], largest first (the longest lists start first, so the
+ *      workgroups of a head finish together, and lists of like length, which
+ *      walk the keys at a like pace, run side by side and share cache hits);
+ *   2. then a signature: the mean of the entries at positions
+ *      floor((2j + 1) * C / 16), j = 0..7, of the list (each clamped to
+ *      [0, N - 1]), as floor(sum * 64 / N) capped at 511, smallest first;
+ *   3. then the block index, smallest first.
+ * Rows with N_p > 16384 get the ascending order 0, 1, ..., N_p - 1.
+ *   idx, cap, counts : as for vecattn_sparse_attn (counts are clamped to
+ *            [0, cap]; only the 8 sampled entries of each list are read)
+ *   B, Hq, N, block  : the selection's shapes; N_p = ceil(N / block)
+ *   order  : int32 [B, Hq, N_p] device output; row (b, h) is a permutation of
+ *            [0, N_p)
+ * Asynchronous on `stream`; one read of counts and of the sampled entries.
+ * Errors: INVALID_ARG (a NULL pointer, B, Hq, N or block < 1, N or cap
+ * outside [1, 2^30], B * Hq > 2^31 - 1).
+ */
+vecattn_status vecattn_attn_order(const int32_t* idx, int64_t cap, const int32_t* counts,
+                                  int64_t B, int32_t Hq, int64_t N, int32_t block, int32_t* order,
+                                  void* stream);
+
+/*
+ * vecattn_sparse_attn taking the blocks of each (b, h) in a given order:
+ *   order : int32 [B, Hq, N_p] device memory, row (b, h) a permutation of
+ *           [0, N_p) (e.g. from vecattn_attn_order), or NULL for the
+ *           ascending order (then this is vecattn_sparse_attn).  Entries are
+ *           clamped to [0, N_p); a row that is not a permutation leaves the
+ *           blocks missing from it unwritten.
+ * Every other argument, the results and the errors are those of
+ * vecattn_sparse_attn (the order of the softmax sums, and so the last bits
+ * of O, can differ between calls, as there).
+ */
+vecattn_status vecattn_sparse_attn_ordered(const void* q, const vecattn_tdesc* qd, const void* k,
+                                           const vecattn_tdesc* kd, const void* v,
+                                           const vecattn_tdesc* vd, const int32_t* idx,
+                                           int64_t cap, const int32_t* counts,
+                                           const int32_t* order, int32_t block, int32_t causal,
+                                           float scale, void* o, const vecattn_tdesc* od,
+                                           float* lse, void* stream);
+
+/*
  * Checker for the index input of vecattn_sparse_attn, for lists that did not
  * come from vecattn_select.  Sets *n_bad (device int32, cleared by the call)
  * to the number of rows whose list breaks the attention's contract: a count

@@ -8,12 +8,14 @@ attention restricted to the gathered K/V rows of those columns (Eq. 4,
 Algorithm 2).  Both stages are HIP kernels in libvecattn.so behind the C ABI
 of include/vecattn.h; this package only marshals torch tensors to it.
 """
-from ._lib import (SEL_MINS, SEL_MINS_TILED, SEL_TOPK, SEL_TOPP, VecattnError, check_lists,
+from ._lib import (SEL_MINS, SEL_MINS_TILED, SEL_TOPK, SEL_TOPP, VecattnError, attn_order,
+                   check_lists,
                    head_sparsity, head_sparsity_of, load, max_count, plan_filter_ratios, pool,
                    recall, select, select_varlen, sparse_attn, sparse_attn_varlen, varlen_blocks,
                    workspace_bytes)
 
-__all__ = ["SEL_TOPK", "SEL_TOPP", "SEL_MINS", "SEL_MINS_TILED", "VecattnError", "check_lists",
+__all__ = ["SEL_TOPK", "SEL_TOPP", "SEL_MINS", "SEL_MINS_TILED", "VecattnError", "attn_order",
+           "check_lists",
            "head_sparsity", "head_sparsity_of", "recall",
            "load", "max_count", "plan_filter_ratios", "pool", "select", "select_varlen",
            "sparse_attn", "sparse_attn_varlen", "varlen_blocks", "workspace_bytes"]

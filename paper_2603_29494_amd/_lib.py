@@ -61,6 +61,9 @@ def load() -> ctypes.CDLL:
     lib.vecattn_select_mins_tiled.argtypes = [P, D, P, D, i32, i32, f64, i32, i32, P, i64, P, P,
                                               P, ctypes.c_size_t, P]
     lib.vecattn_sparse_attn.argtypes = [P, D, P, D, P, D, P, i64, P, i32, i32, f32, P, D, P, P]
+    lib.vecattn_sparse_attn_ordered.argtypes = [P, D, P, D, P, D, P, i64, P, P, i32, i32, f32, P, D,
+                                                P, P]
+    lib.vecattn_attn_order.argtypes = [P, i64, P, i64, i32, i64, i32, P, P]
     lib.vecattn_check_lists.argtypes = [P, i64, i64, P, i64, P, P]
     lib.vecattn_plan_filter_ratios.argtypes = [i32, i32, P, P, f64, i32, P, ctypes.POINTER(f64)]
     lib.vecattn_select_per_head.argtypes = [P, D, P, D, i32, i32, i32, P, i32, i32, P, i64, P, P,
@@ -78,7 +81,8 @@ def load() -> ctypes.CDLL:
                  "vecattn_select", "vecattn_select_mins_tiled", "vecattn_sparse_attn",
                  "vecattn_plan_filter_ratios", "vecattn_select_per_head",
                  "vecattn_select_varlen", "vecattn_sparse_attn_varlen", "vecattn_check_lists",
-                 "vecattn_head_sparsity", "vecattn_recall", "vecattn_select_noalloc"):
+                 "vecattn_head_sparsity", "vecattn_recall", "vecattn_select_noalloc",
+                 "vecattn_sparse_attn_ordered", "vecattn_attn_order"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -257,8 +261,11 @@ def select_noalloc(q: torch.Tensor, k: torch.Tensor, block: int, mode, param: fl
 
 def sparse_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: torch.Tensor,
                 counts: torch.Tensor, block: int, causal: bool = False, scale: float = 0.0,
-                out: Optional[torch.Tensor] = None, return_lse: bool = False):
-    """Vector-sparse attention, Eq. 4: O (bf16, like q) and optionally LSE (fp32 [B,Hq,N])."""
+                out: Optional[torch.Tensor] = None, return_lse: bool = False,
+                order: Optional[torch.Tensor] = None):
+    """Vector-sparse attention, Eq. 4: O (bf16, like q) and optionally LSE (fp32 [B,Hq,N]).
+    ``order`` (int32 [B, Hq, N_p], e.g. from attn_order) sets the order in which
+    the blocks of each head are taken (speed only)."""
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
         _bf16_cuda(t, n)
     if idx.dtype != torch.int32 or counts.dtype != torch.int32 or not idx.is_contiguous() \
@@ -268,16 +275,47 @@ def sparse_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: torch.Te
     Np = (N + block - 1) // block
     if idx.dim() != 4 or tuple(idx.shape[:3]) != (B, Hq, Np) or tuple(counts.shape) != (B, Hq, Np):
         raise ValueError("idx must be [B, Hq, N_p, cap] and counts [B, Hq, N_p]")
+    if order is not None and (order.dtype != torch.int32 or not order.is_contiguous()
+                              or tuple(order.shape) != (B, Hq, Np)):
+        raise ValueError("order must be a contiguous int32 [B, Hq, N_p] tensor")
     if out is None:
         out = torch.empty_like(q, memory_format=torch.contiguous_format)
     lse = torch.empty((B, Hq, N), dtype=torch.float32, device=q.device) if return_lse else None
     qd, kd, vd, od = desc(q), desc(k), desc(v), desc(out)
-    _check(load().vecattn_sparse_attn(_ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd), _ptr(v),
-                                      ctypes.byref(vd), _ptr(idx), int(idx.shape[-1]),
-                                      _ptr(counts), int(block), int(bool(causal)), float(scale),
-                                      _ptr(out), ctypes.byref(od), _ptr(lse), _stream(q)),
-           "sparse_attn")
+    if order is None:
+        rc = load().vecattn_sparse_attn(_ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd),
+                                        _ptr(v), ctypes.byref(vd), _ptr(idx), int(idx.shape[-1]),
+                                        _ptr(counts), int(block), int(bool(causal)), float(scale),
+                                        _ptr(out), ctypes.byref(od), _ptr(lse), _stream(q))
+    else:
+        rc = load().vecattn_sparse_attn_ordered(
+            _ptr(q), ctypes.byref(qd), _ptr(k), ctypes.byref(kd), _ptr(v), ctypes.byref(vd),
+            _ptr(idx), int(idx.shape[-1]), _ptr(counts), _ptr(order), int(block),
+            int(bool(causal)), float(scale), _ptr(out), ctypes.byref(od), _ptr(lse), _stream(q))
+    _check(rc, "sparse_attn")
     return (out, lse) if return_lse else out
+
+
+def attn_order(idx: torch.Tensor, counts: torch.Tensor, n_keys: int, block: int,
+               out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Block order for sparse_attn (int32 [B, Hq, N_p]): per head, count
+    descending, then a sampled mean key, then block index."""
+    if idx.dtype != torch.int32 or counts.dtype != torch.int32 or not idx.is_cuda \
+            or not counts.is_cuda or not idx.is_contiguous() or not counts.is_contiguous():
+        raise ValueError("idx and counts must be contiguous int32 CUDA tensors")
+    if idx.dim() != 4 or counts.dim() != 3 or tuple(idx.shape[:3]) != tuple(counts.shape):
+        raise ValueError("idx must be [B, Hq, N_p, cap] and counts [B, Hq, N_p]")
+    B, Hq, Np = counts.shape
+    if Np != (int(n_keys) + int(block) - 1) // int(block):
+        raise ValueError("counts hold N_p = ceil(n_keys / block) blocks per head")
+    if out is None:
+        out = torch.empty((B, Hq, Np), dtype=torch.int32, device=idx.device)
+    elif out.dtype != torch.int32 or not out.is_contiguous() or tuple(out.shape) != (B, Hq, Np):
+        raise ValueError("out must be a contiguous int32 [B, Hq, N_p] tensor")
+    _check(load().vecattn_attn_order(_ptr(idx), int(idx.shape[-1]), _ptr(counts), int(B), int(Hq),
+                                     int(n_keys), int(block), _ptr(out), _stream(idx)),
+           "attn_order")
+    return out
 
 
 def check_lists(idx: torch.Tensor, counts: torch.Tensor, n_keys: int) -> int:

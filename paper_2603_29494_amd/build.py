@@ -14,7 +14,7 @@ LIB = os.path.join(HERE, "libvecattn.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
 SOURCES = ["vecattn_api.cpp", "plan.cpp", "pool.hip", "sparse_attn.hip", "select.hip", "check.hip",
-           "stats.hip", "noalloc.hip"]
+           "stats.hip", "noalloc.hip", "attn_order.hip"]
 
 # Packed fp32 VALU instructions are disabled for all device code.
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

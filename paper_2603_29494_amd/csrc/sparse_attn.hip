@@ -101,7 +101,8 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
     const uint16_t* __restrict__ k, int64_t k_sB, int64_t k_sH, int64_t k_sN,
     const uint16_t* __restrict__ v, int64_t v_sB, int64_t v_sH, int64_t v_sN,
     uint16_t* __restrict__ o, int64_t o_sB, int64_t o_sH, int64_t o_sN, float* __restrict__ lse,
-    const int32_t* __restrict__ idx, const int32_t* __restrict__ counts, int64_t cap, int32_t Hq,
+    const int32_t* __restrict__ idx, const int32_t* __restrict__ counts,
+    const int32_t* __restrict__ order, int64_t cap, int32_t Hq,
     int32_t group, int32_t N, int32_t P, int32_t Np, int32_t chunks, int32_t causal,
     float scale_log2, int64_t total, int64_t per_xcd, int32_t xgroup, int32_t herd_slots) {
   constexpr int CH = D / 8;                 // 16-byte chunks per row
@@ -127,8 +128,9 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
   auto vbuf = [&](int st) __attribute__((always_inline)) { return st ? v_s1 : v_s0; };
   auto ibuf = [&](int st) __attribute__((always_inline)) { return st ? id_s1 : id_s0; };
 
-  // Work item.  Items are (b, h, block, chunk) in that order; the chunks of a
-  // block stay on one XCD (they gather the same list).  XCDs form groups of
+  // Work item.  Items are (b, h, position, chunk) in that order, position p
+  // of head (b, h) being block order[b, h, p] (or p); the chunks of a block
+  // stay on one XCD (they gather the same list).  XCDs form groups of
   // `xgroup`; a group takes a contiguous range of blocks, dealt to its XCDs
   // one block at a time, so fewer heads are swept at once (their K/V rows then
   // compete less for the chip-wide last-level cache), and each XCD still walks
@@ -145,8 +147,9 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
   if (w >= total) return;
   const int chunk = static_cast<int>(w % chunks);
   const int64_t rest = w / chunks;
-  const int i = static_cast<int>(rest % Np);
   const int64_t bh = rest / Np;
+  const int pos = static_cast<int>(rest % Np);
+  const int i = order ? min(max(order[bh * Np + pos], 0), Np - 1) : pos;
   const int b = static_cast<int>(bh / Hq);
   const int h = static_cast<int>(bh % Hq);
   const int hk = h / group;
@@ -527,7 +530,7 @@ hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream) {
     const int32_t slots = max(1, per_cu * cus / 8);
     hipLaunchKernelGGL(kernel, grid, dim3(threads), 0, stream, q, a.q.sB, a.q.sH, a.q.sN, k,
                        a.k.sB, a.k.sH, a.k.sN, v, a.v.sB, a.v.sH, a.v.sN, o, a.o_sB, a.o_sH,
-                       a.o_sN, a.lse, a.idx, a.counts, a.cap, static_cast<int32_t>(Hq), group,
+                       a.o_sN, a.lse, a.idx, a.counts, a.order, a.cap, static_cast<int32_t>(Hq), group,
                        static_cast<int32_t>(N), P, Np, chunks, a.causal, scale_log2, total,
                        per_xcd, xgroup, slots);
     return hipGetLastError();

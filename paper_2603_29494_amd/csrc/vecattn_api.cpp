@@ -319,18 +319,41 @@ vecattn_status vecattn_select_mins_tiled(const void* q, const vecattn_tdesc* qd,
                      group_tiles, idx, cap, counts, n_clamped, workspace, workspace_bytes, stream);
 }
 
-vecattn_status vecattn_sparse_attn(const void* q, const vecattn_tdesc* qd, const void* k,
-                                   const vecattn_tdesc* kd, const void* v, const vecattn_tdesc* vd,
-                                   const int32_t* idx, int64_t cap, const int32_t* counts,
-                                   int32_t block, int32_t causal, float scale, void* o,
-                                   const vecattn_tdesc* od, float* lse, void* stream) {
+vecattn_status vecattn_sparse_attn_ordered(const void* q, const vecattn_tdesc* qd, const void* k,
+                                           const vecattn_tdesc* kd, const void* v,
+                                           const vecattn_tdesc* vd, const int32_t* idx,
+                                           int64_t cap, const int32_t* counts,
+                                           const int32_t* order, int32_t block, int32_t causal,
+                                           float scale, void* o, const vecattn_tdesc* od,
+                                           float* lse, void* stream) {
   const vecattn_status st =
       check_attn(q, qd, k, kd, v, vd, idx, cap, counts, block, causal, scale, o, od);
   if (st != VECATTN_OK) return st;
   vecattn::SparseAttnArgs a{to_tensor(q, qd), to_tensor(k, kd), to_tensor(v, vd),
                             o, od->sB, od->sH, od->sN, lse, idx, counts, cap, block,
-                            (causal & kCausal) ? 1 : 0, scale};
+                            (causal & kCausal) ? 1 : 0, scale, order};
   hipError_t e = vecattn::launch_sparse_attn(a, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
+}
+
+vecattn_status vecattn_sparse_attn(const void* q, const vecattn_tdesc* qd, const void* k,
+                                   const vecattn_tdesc* kd, const void* v, const vecattn_tdesc* vd,
+                                   const int32_t* idx, int64_t cap, const int32_t* counts,
+                                   int32_t block, int32_t causal, float scale, void* o,
+                                   const vecattn_tdesc* od, float* lse, void* stream) {
+  return vecattn_sparse_attn_ordered(q, qd, k, kd, v, vd, idx, cap, counts, nullptr, block, causal,
+                                     scale, o, od, lse, stream);
+}
+
+vecattn_status vecattn_attn_order(const int32_t* idx, int64_t cap, const int32_t* counts,
+                                  int64_t B, int32_t Hq, int64_t N, int32_t block, int32_t* order,
+                                  void* stream) {
+  if (!idx || !counts || !order || B < 1 || Hq < 1 || N < 1 || N > kMaxN || block < 1 ||
+      cap < 1 || cap > kMaxN || B * Hq > INT32_MAX)
+    return VECATTN_ERR_INVALID_ARG;
+  const int64_t Np = (N + block - 1) / block;
+  hipError_t e = vecattn::launch_attn_order(idx, cap, counts, B * Hq, static_cast<int32_t>(Np), N,
+                                            order, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? VECATTN_OK : VECATTN_ERR_DEVICE;
 }
 

@@ -90,6 +90,13 @@ int main() {
                         nullptr) == VECATTN_ERR_INVALID_ARG, "recall cap");
   vecattn_tdesc qp = desc(1, 4, 4, 128);
   expect(vecattn_pool(fake, &q, 0, fake, &qp, nullptr) == VECATTN_ERR_INVALID_ARG, "pool block");
+  expect(vecattn_attn_order(ifake, 16, ifake, 1, 4, 256, 0, ifake, nullptr) ==
+             VECATTN_ERR_INVALID_ARG, "order block");
+  expect(vecattn_attn_order(ifake, 16, ifake, int64_t(1) << 20, 1 << 12, 256, 64, ifake, nullptr) ==
+             VECATTN_ERR_INVALID_ARG, "order rows");
+  expect(vecattn_sparse_attn_ordered(fake, &q, fake, &k, fake, &bad, ifake, 16, ifake, ifake, 64, 0,
+                                     0.0f, fake, &q, nullptr, nullptr) == VECATTN_ERR_INVALID_ARG,
+         "ordered attn v");
 
   // Valid arguments reach the launch code: without a device it reports DEVICE.
   std::vector<uint8_t> dummy(64);
@@ -98,6 +105,8 @@ int main() {
                              nullptr, nullptr) == VECATTN_ERR_DEVICE, "attn launch");
   expect(vecattn_select_noalloc(fake, &q, fake, &k, 64, 0, 0, 0.25, ifake, 64, ifake, nullptr,
                                 nullptr) == VECATTN_ERR_DEVICE, "noalloc launch");
+  expect(vecattn_attn_order(ifake, 16, ifake, 1, 4, 256, 64, ifake, nullptr) == VECATTN_ERR_DEVICE,
+         "order launch");
 
   // Eq. 5's programme on random tables.
   std::mt19937_64 rng(11);

@@ -360,3 +360,29 @@ def test_select_noalloc_checks_before_any_device_call():
     assert lib.vecattn_select_workspace_bytes(ctypes.byref(big_q), ctypes.byref(big_k), 64, 0,
                                               11340) > _lib.STATIC_WORKSPACE_BYTES
     assert sel(qd=big_q, kd=big_k, cap=11340, param=0.15) == CAPACITY
+
+
+def test_attn_order_and_ordered_attention_reject_bad_arguments():
+    lib = _lib.load()
+
+    def order(idx=FAKE, cap=16, cnt=FAKE, B=1, H=4, N=256, block=64, out=FAKE):
+        return lib.vecattn_attn_order(idx, cap, cnt, B, H, N, block, out, None)
+    assert order(idx=None) == INVALID and order(cnt=None) == INVALID and order(out=None) == INVALID
+    assert order(B=0) == INVALID and order(H=0) == INVALID and order(N=0) == INVALID
+    assert order(block=0) == INVALID and order(cap=0) == INVALID
+    assert order(cap=(1 << 30) + 1) == INVALID and order(N=(1 << 30) + 1) == INVALID
+    assert order(B=1 << 20, H=1 << 12) == INVALID                      # B * Hq > 2^31 - 1
+
+    def oattn(q=FAKE, idx=FAKE, cnt=FAKE, order=FAKE, block=64, cap=16, scale=0.0, kd=None):
+        qd, od = desc(1, 4, 128, 128), desc(1, 4, 128, 128)
+        kd = kd or desc(1, 2, 128, 128)
+        vd = desc(1, 2, 128, 128)
+        return lib.vecattn_sparse_attn_ordered(q, ctypes.byref(qd), FAKE, ctypes.byref(kd), FAKE,
+                                               ctypes.byref(vd), idx, cap, cnt, order, block, 0,
+                                               scale, FAKE, ctypes.byref(od), None, None)
+    # the checks of vecattn_sparse_attn apply unchanged (a NULL order is allowed)
+    assert oattn(q=None) == INVALID and oattn(idx=None) == INVALID and oattn(cnt=None) == INVALID
+    assert oattn(block=0) == INVALID and oattn(cap=0) == INVALID and oattn(scale=-1.0) == INVALID
+    assert oattn(order=None, q=None) == INVALID
+    assert oattn(kd=desc(1, 2, 127, 128)) == INVALID
+    assert oattn(kd=desc(1, 2, 1 << 24, 128)) == INVALID                # N mismatch before size

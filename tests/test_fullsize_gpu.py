@@ -1,6 +1,6 @@
 """The five synthetic workloads at full size, in the launch configuration the
 benchmark times (selection with the library's default cap and workspace,
-then sparse attention on its lists), checked against the CPU oracle on a
+the block order, then sparse attention on its lists in that order), checked against the CPU oracle on a
 random sample of query blocks: the selection rule of selection_parity and
 the attention bar of test_attn_gpu (max-abs 2e-2, mean-abs 2e-3 against the
 fp64 oracle on the GPU's own lists).  Plus properties that hold for every
@@ -49,9 +49,15 @@ def test_workload_full_size(gpu, cid):
     Np = (N + P - 1) // P
     print(f"workload {cid} {w.name}: select + attention", flush=True)
     idx, cnt = va.select(q, k, P, w.mode, w.param, w.causal)
-    out = va.sparse_attn(q, k, v, idx, cnt, P, w.causal)
+    order = va.attn_order(idx, cnt, N, P)
+    out = va.sparse_attn(q, k, v, idx, cnt, P, w.causal, order=order)
     torch.cuda.synchronize()
     cap = idx.shape[-1]
+    # The block order: a permutation of each head's blocks, counts non-increasing.
+    ar = torch.arange(Np, device="cuda", dtype=torch.int32)
+    assert bool((torch.sort(order, dim=-1).values == ar).all())
+    oc = torch.gather(cnt, 2, order.long())
+    assert bool((oc[..., 1:] <= oc[..., :-1]).all())
 
     # Every block: counts, order, range (on the GPU, without copying the lists).
     L = torch.tensor([min(N, (i + 1) * P) if w.causal else N for i in range(Np)], device="cuda")

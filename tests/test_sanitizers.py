@@ -18,6 +18,8 @@ from concurrent.futures import ThreadPoolExecutor
 
 import pytest
 
+from paper_2603_29494_amd.build import SOURCES
+
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2603_29494_amd", "csrc")
 INC = os.path.join(ROOT, "include")
@@ -56,8 +58,8 @@ def test_host_api_under_sanitizers(tmp_path):
         jobs.append([CLANG, "-std=c++17", "-O1", "-g", "-D__HIP_PLATFORM_AMD__",
                      "-I" + os.path.join(ROCM, "include")] + inc + SAN +
                     ["-c", os.path.join(CSRC, src), "-o", src + ".o"])
-    for src in ("select.hip", "pool.hip", "sparse_attn.hip", "check.hip", "stats.hip",
-                "noalloc.hip"):
+    hip_srcs = [s for s in SOURCES if s.endswith(".hip")]
+    for src in hip_srcs:
         jobs.append([HIPCC, "-x", "hip", "--offload-arch=gfx950", "-std=c++17", "-O1", "-g",
                      "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"] + inc +
                     HOST_SAN + ["-c", os.path.join(CSRC, src), "-o", src + ".o"])
@@ -65,8 +67,7 @@ def test_host_api_under_sanitizers(tmp_path):
                 ["-c", os.path.join(ROOT, "tests", "sanitize", "api_main.cpp"), "-o", "api_main.o"])
     with ThreadPoolExecutor(max_workers=8) as ex:
         list(ex.map(lambda c: run(c, d), jobs))
-    objs = ["api_main.o", "vecattn_api.cpp.o", "plan.cpp.o", "select.hip.o", "pool.hip.o",
-            "sparse_attn.hip.o", "check.hip.o", "stats.hip.o", "noalloc.hip.o"]
+    objs = ["api_main.o", "vecattn_api.cpp.o", "plan.cpp.o"] + [s + ".o" for s in hip_srcs]
     run([HIPCC, "--offload-arch=gfx950"] + HOST_SAN[:4] + objs + ["-o", "api_san"], d)
     out = run([os.path.join(d, "api_san")], d)
     assert out.strip().endswith("ok"), out

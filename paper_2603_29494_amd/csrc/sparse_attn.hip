@@ -104,7 +104,7 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
     const int32_t* __restrict__ idx, const int32_t* __restrict__ counts,
     const int32_t* __restrict__ order, int64_t cap, int32_t Hq,
     int32_t group, int32_t N, int32_t P, int32_t Np, int32_t chunks, int32_t causal,
-    float scale_log2, int64_t total, int64_t per_xcd, int32_t xgroup, int32_t herd_slots) {
+    float scale_log2, int64_t total, int32_t xgroup, int32_t herd_slots) {
   constexpr int CH = D / 8;                 // 16-byte chunks per row
   constexpr int kThreads = 4 * ROWS;  // 2 key halves x ROWS / 32 row groups, 64 lanes each
   constexpr int RG = ROWS / 32;             // row groups (waves per key half)
@@ -128,27 +128,38 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
   auto vbuf = [&](int st) __attribute__((always_inline)) { return st ? v_s1 : v_s0; };
   auto ibuf = [&](int st) __attribute__((always_inline)) { return st ? id_s1 : id_s0; };
 
-  // Work item.  Items are (b, h, position, chunk) in that order, position p
-  // of head (b, h) being block order[b, h, p] (or p); the chunks of a block
-  // stay on one XCD (they gather the same list).  XCDs form groups of
-  // `xgroup`; a group takes a contiguous range of blocks, dealt to its XCDs
-  // one block at a time, so fewer heads are swept at once (their K/V rows then
-  // compete less for the chip-wide last-level cache), and each XCD still walks
-  // its blocks in order.  Every item in [0, 8 * per_xcd) is taken once.
-  const int64_t w = [&]() {
-    const int64_t x = blockIdx.x;
-    const int xc = static_cast<int>(x & 7);
-    const int64_t j = x >> 3;
-    const int64_t per_xcd_blocks = per_xcd / chunks;
-    const int64_t blk = (xc / xgroup) * (xgroup * per_xcd_blocks) + xgroup * (j / chunks) +
-                        (xc % xgroup);
-    return blk * chunks + j % chunks;
-  }();
-  if (w >= total) return;
-  const int chunk = static_cast<int>(w % chunks);
-  const int64_t rest = w / chunks;
-  const int64_t bh = rest / Np;
-  const int pos = static_cast<int>(rest % Np);
+  // Work item: head bh = b * Hq + h, position pos in the head (block
+  // order[bh, pos], or pos) and 64- or 128-row chunk of the block; the chunks
+  // of a block stay on one XCD (they gather the same list).  XCDs form
+  // 8 / xgroup groups.  Each group owns W = nheads / groups whole heads, in
+  // order, so that few heads are swept at once (their K/V rows then compete
+  // less for the chip-wide last-level cache); the nheads % groups heads left
+  // over are shared by all groups, group g taking the positions p = g (mod
+  // groups) of each, so that every group gets the same work whatever the
+  // blocks' list lengths (a head split at a group boundary would leave one
+  // side with its longest lists).  A group's sequence is dealt to its XCDs
+  // one block at a time, and each XCD walks its share in order.  The grid
+  // covers the longest sequence (group 0's); every item is taken once.
+  const int ngroups = 8 / xgroup;
+  const int64_t nheads = total / (static_cast<int64_t>(Np) * chunks);
+  const int64_t whole = nheads / ngroups;
+  const int grp = (blockIdx.x & 7) / xgroup;
+  const int64_t slot = blockIdx.x >> 3;
+  const int chunk = static_cast<int>(slot % chunks);
+  const int64_t e = (slot / chunks) * xgroup + (blockIdx.x & 7) % xgroup;
+  int64_t bh;
+  int pos;
+  if (e < whole * Np) {
+    bh = grp * whole + e / Np;
+    pos = static_cast<int>(e % Np);
+  } else {
+    const int64_t e2 = e - whole * Np;
+    const int64_t ng = (Np - grp + ngroups - 1) / ngroups;  // positions = grp (mod groups)
+    if (ng <= 0) return;
+    bh = whole * ngroups + e2 / ng;
+    if (bh >= nheads) return;
+    pos = static_cast<int>((e2 % ng) * ngroups + grp);
+  }
   const int i = order ? min(max(order[bh * Np + pos], 0), Np - 1) : pos;
   const int b = static_cast<int>(bh / Hq);
   const int h = static_cast<int>(bh % Hq);
@@ -505,12 +516,16 @@ hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream) {
   // gather of a tile then serves the whole block), else 64.
   const int32_t rows = P % 128 == 0 ? 128 : 64;
   const int32_t chunks = (P + rows - 1) / rows;
-  const int64_t blocks = B * Hq * static_cast<int64_t>(Np);
-  const int64_t total = blocks * chunks;
+  const int64_t nheads = B * Hq;
+  const int64_t total = nheads * Np * chunks;
   if (total == 0) return hipSuccess;
-  const int64_t per_xcd = (blocks + 7) / 8 * chunks;  // whole blocks per XCD
-  const dim3 grid(static_cast<unsigned>(per_xcd * 8));
   const int32_t xgroup = xcd_group(a.k.N, a.k.D, a.k.H, B, a.causal);
+  // Group 0's sequence (the longest): its whole heads and its share of the
+  // heads left over; each of its XCDs takes every xgroup-th block of it.
+  const int64_t ngroups = 8 / xgroup, whole = nheads / ngroups;
+  const int64_t seq0 = whole * Np + (nheads - whole * ngroups) * ((Np + ngroups - 1) / ngroups);
+  const int64_t per_xcd = (seq0 + xgroup - 1) / xgroup * chunks;
+  const dim3 grid(static_cast<unsigned>(per_xcd * 8));
   const float scale = a.scale != 0.0f ? a.scale : 1.0f / sqrtf(static_cast<float>(D));
   const float scale_log2 = scale * 1.4426950408889634f;
   const int32_t group = static_cast<int32_t>(Hq / a.k.H);
@@ -532,7 +547,7 @@ hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream) {
                        a.k.sB, a.k.sH, a.k.sN, v, a.v.sB, a.v.sH, a.v.sN, o, a.o_sB, a.o_sH,
                        a.o_sN, a.lse, a.idx, a.counts, a.order, a.cap, static_cast<int32_t>(Hq), group,
                        static_cast<int32_t>(N), P, Np, chunks, a.causal, scale_log2, total,
-                       per_xcd, xgroup, slots);
+                       xgroup, slots);
     return hipGetLastError();
   };
   if (rows == 128) {

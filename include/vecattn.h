@@ -20,10 +20,9 @@
  *     streams may run concurrently.  The only state kept between calls is a
  *     per-process, per-device locality counter of vecattn_sparse_attn (the
  *     progress of the workgroups on each XCD through their lists, which paces
- *     the order in which a workgroup walks its list): concurrent calls share
- *     it, which changes their speed and the
- *     order of the softmax sums (the last bits of O), never which keys are
- *     attended.
+ *     the order in which a workgroup walks its list; non-causal calls only):
+ *     concurrent calls share it, which changes their speed and the order of
+ *     the softmax sums (the last bits of O), never which keys are attended.
  *   - Q, K, V, O are bf16 with logical shape [B, H, N, D] described by a
  *     vecattn_tdesc: sizes plus element strides sB, sH, sN; the D dimension is
  *     contiguous (stride 1).  Every row start must be 16-byte aligned (base

@@ -182,13 +182,19 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
   // the tile at that fraction of its own list (then wraps around), so the
   // workgroups on an XCD sweep the keys together at their actual pace.  The
   // order of the tiles changes only the order of the softmax sums (results
-  // can differ between runs within fp32 rounding).
+  // can differ between runs within fp32 rounding).  Causal lists are walked
+  // from their first tile instead: block i's list lies in [0, (i + 1) P), so a
+  // fraction of it is a different key position for every block, while the
+  // walks from key 0 of lists of like length (taken together by the block
+  // order) stay together.
   const int xcd = blockIdx.x & 7;  // the hardware deals workgroup x to XCD x % 8
+  const bool herd = !causal;
   __shared__ int s_rot;
-  if (threadIdx.x == 0) {
-    const unsigned int herd =
+  if (threadIdx.x == 0 && !herd) s_rot = 0;
+  if (threadIdx.x == 0 && herd) {
+    const unsigned int progress =
         __hip_atomic_load(&g_herd[xcd], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const unsigned int pos = (herd / static_cast<unsigned int>(herd_slots)) % kHerdUnit;
+    const unsigned int pos = (progress / static_cast<unsigned int>(herd_slots)) % kHerdUnit;
     // ntiles < 2^18 (N < 2^24), so the product fits 32 bits.
     s_rot = static_cast<int>((pos * static_cast<unsigned int>(ntiles)) / kHerdUnit);
   }
@@ -307,7 +313,7 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
     // also guarantees every wave is done reading the other stage.
     wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
-    if (wave == 0 && lane == 0 && (t % kHerdBatch) == kHerdBatch - 1)
+    if (herd && wave == 0 && lane == 0 && (t % kHerdBatch) == kHerdBatch - 1)
       __hip_atomic_fetch_add(&g_herd[xcd], herd_units(t + 1) - herd_units(t + 1 - kHerdBatch),
                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (t + 1 < ntiles) issue_tile(t + 1, st ^ 1);
@@ -435,7 +441,7 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
     if (t + 1 < ntiles) step(t + 1, 1);
   }
 
-  if (wave == 0 && lane == 0 && ntiles % kHerdBatch != 0)
+  if (herd && wave == 0 && lane == 0 && ntiles % kHerdBatch != 0)
     __hip_atomic_fetch_add(&g_herd[xcd], kHerdUnit - herd_units(ntiles - ntiles % kHerdBatch),
                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 

@@ -274,3 +274,19 @@ def test_extreme_logits_move_the_softmax_reference(gpu, causal):
     torch.cuda.synchronize()
     check_attn(o, lse, o_ref, lse_ref, f"extreme logits causal={causal}")
     assert np.abs(lse_ref[fin]).max() > 100.0
+
+
+def test_causal_attention_is_deterministic(gpu):
+    """Causal lists are walked from their first tile, so the summation order and
+    O are the same on every call (with and without a block order)."""
+    B, Hq, Hkv, N, D, P = 1, 4, 2, 700, 128, 64
+    q, k, v = (dev(synth.random_bits(900 + j, (B, h, N, D))) for j, h in enumerate((Hq, Hkv, Hkv)))
+    Np = (N + P - 1) // P
+    idx, cnt = random_lists(77, B, Hq, Np, N, P, True, N, N)
+    ti, tc = torch.from_numpy(idx).cuda(), torch.from_numpy(cnt).cuda()
+    order = va.attn_order(ti, tc, N, P)
+    first, lse1 = va.sparse_attn(q, k, v, ti, tc, P, True, return_lse=True)
+    for o in (None, order, None):
+        again, lse2 = va.sparse_attn(q, k, v, ti, tc, P, True, return_lse=True, order=o)
+        assert torch.equal(again.view(torch.int16), first.view(torch.int16))
+        assert torch.equal(lse1, lse2)

@@ -1547,6 +1547,9 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
   // next one, and go out one by one after the last chunk.
   const bool quads = p.quad_rows;
   int done = 0;      // entries stored (quad path)
+  // keep_diag: this block's own rows, [i P, min(N, (i + 1) P))
+  const int diag_lo = p.keep_diag ? static_cast<int>(r % p.Np) * p.P : 0;
+  const int diag_hi = p.keep_diag ? min(p.N, diag_lo + p.P) : 0;
   // The next batch's words are loaded while this batch is listed.
   uint32_t mb[kCompactBatch], tb[kCompactBatch], mn[kCompactBatch], tn[kCompactBatch];
   auto load_batch = [&](uint32_t (&m)[kCompactBatch], uint32_t (&t)[kCompactBatch], int c0)
@@ -1580,9 +1583,8 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
         }
         ties_seen += __builtin_amdgcn_readlane(incl, 63);
       }
-      if (p.keep_diag) {  // the keys of the block's own rows, [i P, min(N, (i + 1) P))
-        const int i = static_cast<int>(r % p.Np);
-        const int lo = max(i * p.P - 32 * wd, 0), hi = min(min(p.N, (i + 1) * p.P) - 32 * wd, 32);
+      if (p.keep_diag) {  // the keys of the block's own rows
+        const int lo = max(diag_lo - 32 * wd, 0), hi = min(diag_hi - 32 * wd, 32);
         if (lo < hi) m |= (hi == 32 ? 0xFFFFFFFFu : (1u << hi) - 1u) & ~((1u << lo) - 1u);
       }
       if (wd < nw && L - 32 * wd < 32) m &= (1u << (L - 32 * wd)) - 1u;

@@ -272,7 +272,9 @@ vecattn_status vecattn_sparse_attn(const void* q, const vecattn_tdesc* qd, const
  *      floor((2j + 1) * C / 16), j = 0..7, of the list (each clamped to
  *      [0, N - 1]), as floor(sum * 64 / N) capped at 511, smallest first;
  *   3. then the block index, smallest first.
- * Rows with N_p > 16384 get the ascending order 0, 1, ..., N_p - 1.
+ * A head of more than 16384 blocks is ordered in consecutive segments of
+ * 16384 blocks, each segment by the rules above (positions [16384 s,
+ * 16384 (s + 1)) hold a permutation of the same blocks).
  *   idx, cap, counts : as for vecattn_sparse_attn (counts are clamped to
  *            [0, cap]; only the 8 sampled entries of each list are read)
  *   B, Hq, N, block  : the selection's shapes; N_p = ceil(N / block)

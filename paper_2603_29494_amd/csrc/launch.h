@@ -34,8 +34,8 @@ struct SparseAttnArgs {
 hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream);
 
 // Block order per (b, h) for the attention: blocks sorted by count (largest
-// first), then by a sampled mean key, then by index.  rows = B * Hq (fits the
-// grid); rows with N_p > kOrderMaxBlocks get the ascending order.
+// first), then by a sampled mean key, then by index, within consecutive
+// segments of kOrderMaxBlocks blocks.  rows = B * Hq (fits the grid).
 constexpr int32_t kOrderMaxBlocks = 16384;
 hipError_t launch_attn_order(const int32_t* idx, int64_t cap, const int32_t* counts, int64_t rows,
                              int32_t Np, int64_t N, int32_t* order, hipStream_t stream);

@@ -42,20 +42,19 @@ def order_ref(idx, cnt, N, cap):
     out = np.empty((B, H, Np), dtype=np.int32)
     for b in range(B):
         for h in range(H):
-            if Np > 16384:
-                out[b, h] = np.arange(Np)
-                continue
-            keys = []
-            for i in range(Np):
-                c = min(max(int(cnt[b, h, i]), 0), cap)
-                s = 0
-                if c > 0:
-                    for j in range(8):
-                        e = int(idx[b, h, i, ((2 * j + 1) * c) // 16])
-                        s += min(max(e, 0), N - 1)
-                sig = min((s * 64) // N, 511)
-                keys.append(((2 ** 30 - c) << 33) | (sig << 24) | i)
-            out[b, h] = np.argsort(np.array(keys, dtype=np.uint64), kind="stable")
+            for s0 in range(0, Np, 16384):  # heads of more blocks: segment by segment
+                keys = []
+                for i in range(s0, min(Np, s0 + 16384)):
+                    c = min(max(int(cnt[b, h, i]), 0), cap)
+                    s = 0
+                    if c > 0:
+                        for j in range(8):
+                            e = int(idx[b, h, i, ((2 * j + 1) * c) // 16])
+                            s += min(max(e, 0), N - 1)
+                    sig = min((s * 64) // N, 511)
+                    keys.append(((2 ** 30 - c) << 33) | (sig << 24) | (i - s0))
+                seg = np.argsort(np.array(keys, dtype=np.uint64), kind="stable")
+                out[b, h, s0:s0 + len(seg)] = s0 + seg
     return out
 
 
@@ -79,17 +78,20 @@ def test_order_matches_definition(gpu, N, P, cap, kind):
     assert np.array_equal(got, order_ref(idx, cnt, N, cap))
 
 
-@pytest.mark.parametrize("Np", [16384, 16385])
-def test_order_size_limit(gpu, Np):
-    """16384 blocks per head are sorted; more get the ascending order."""
+@pytest.mark.parametrize("Np", [16384, 16385, 40000])
+def test_order_segments(gpu, Np):
+    """Up to 16384 blocks per head are sorted at once; longer heads segment by
+    segment (a one-block tail, and two whole segments and a partial one)."""
     r = np.random.Generator(np.random.PCG64(Np))
-    N, P, cap = Np, 1, 1
-    cnt = r.integers(0, 2, size=(1, 1, Np)).astype(np.int32)
-    idx = np.where(cnt[..., None] > 0, r.integers(0, N, size=(1, 1, Np, 1)), -1).astype(np.int32)
+    N, P, cap = Np, 1, 2
+    cnt = r.integers(0, 3, size=(1, 1, Np)).astype(np.int32)
+    idx = np.sort(r.integers(0, N, size=(1, 1, Np, cap)), axis=-1).astype(np.int32)
+    idx = np.where(np.arange(cap)[None, None, None, :] < cnt[..., None], idx, -1).astype(np.int32)
     got = va.attn_order(cuda_i32(idx), cuda_i32(cnt), N, P).cpu().numpy()
     assert np.array_equal(got, order_ref(idx, cnt, N, cap))
-    if Np > 16384:
-        assert np.array_equal(got[0, 0], np.arange(Np))
+    for s0 in range(0, Np, 16384):  # each segment a permutation of its own blocks
+        seg = got[0, 0, s0:s0 + 16384]
+        assert np.array_equal(np.sort(seg), np.arange(s0, s0 + len(seg)))
 
 
 def check_attn(o_gpu, lse_gpu, o_ref, lse_ref, label):

@@ -131,8 +131,8 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
   // Work item: head bh = b * Hq + h, position pos in the head (block
   // order[bh, pos], or pos) and 64- or 128-row chunk of the block; the chunks
   // of a block stay on one XCD (they gather the same list).  XCDs form
-  // 8 / xgroup groups.  Each group owns W = nheads / groups whole heads, in
-  // order, so that few heads are swept at once (their K/V rows then compete
+  // 8 / xgroup groups.  Each group owns `whole` = nheads / groups whole heads,
+  // in order, so that few heads are swept at once (their K/V rows then compete
   // less for the chip-wide last-level cache); the nheads % groups heads left
   // over are shared by all groups, group g taking the positions p = g (mod
   // groups) of each, so that every group gets the same work whatever the
@@ -194,9 +194,9 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
   if (threadIdx.x == 0 && herd) {
     const unsigned int progress =
         __hip_atomic_load(&g_herd[xcd], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const unsigned int pos = (progress / static_cast<unsigned int>(herd_slots)) % kHerdUnit;
+    const unsigned int at = (progress / static_cast<unsigned int>(herd_slots)) % kHerdUnit;
     // ntiles < 2^18 (N < 2^24), so the product fits 32 bits.
-    s_rot = static_cast<int>((pos * static_cast<unsigned int>(ntiles)) / kHerdUnit);
+    s_rot = static_cast<int>((at * static_cast<unsigned int>(ntiles)) / kHerdUnit);
   }
   __syncthreads();
   const int t_rot = __builtin_amdgcn_readfirstlane(s_rot);

@@ -836,13 +836,24 @@ __global__ __launch_bounds__(kThreads) void k_sample_bracket(SelParams p) {
 #pragma unroll
     for (int s2 = 0; s2 < DS; ++s2) dst[s2] = ksrc[s2 * 64];
   };
+  // This wave's sampled blocks j = wave, wave + 4, ..., each block's K loaded
+  // one block ahead (kload clamps the index, so loads past the end are safe).
+  auto walk = [&](auto&& body) __attribute__((always_inline)) {
+    u32x4 k0[DS], k1[DS];
+    kload(k0, wave);
+    for (int j = wave; j < nsb; j += 8) {
+      kload(k1, j + 4);
+      body(j, k0);
+      if (j + 4 >= nsb) break;
+      kload(k0, j + 8);
+      body(j + 4, k1);
+    }
+  };
 
   // 1. Moments of the sampled scores.
   float m1[2] = {0.0f, 0.0f}, m2[2] = {0.0f, 0.0f};
   uint32_t cnt[2] = {0u, 0u};
-  for (int j = wave; j < nsb; j += 4) {
-    u32x4 ka[DS];
-    kload(ka, j);
+  walk([&](int j, const u32x4 (&ka)[DS]) __attribute__((always_inline)) {
     const int kb = 32 * kSampleStride * j;
 #pragma unroll
     for (int rb2 = 0; rb2 < 2; ++rb2) {
@@ -857,7 +868,7 @@ __global__ __launch_bounds__(kThreads) void k_sample_bracket(SelParams p) {
         cnt[rb2] += kl < lim ? 1u : 0u;
       }
     }
-  }
+  });
 #pragma unroll
   for (int rb2 = 0; rb2 < 2; ++rb2) {
     const float a = m1[rb2] + __shfl_xor(m1[rb2], 32);
@@ -911,9 +922,7 @@ __global__ __launch_bounds__(kThreads) void k_sample_bracket(SelParams p) {
     bmul[rb2] = s_mul[rl];
     badd[rb2] = s_add[rl];
   }
-  for (int j = wave; j < nsb; j += 4) {
-    u32x4 ka[DS];
-    kload(ka, j);
+  walk([&](int j, const u32x4 (&ka)[DS]) __attribute__((always_inline)) {
     const int kb = 32 * kSampleStride * j;
 #pragma unroll
     for (int rb2 = 0; rb2 < 2; ++rb2) {
@@ -927,7 +936,7 @@ __global__ __launch_bounds__(kThreads) void k_sample_bracket(SelParams p) {
         atomicAdd(&s_hist[bn * kRowsWG + rb2 * 32 + ln], 1u);
       }
     }
-  }
+  });
   __syncthreads();
   if (tid < kRowsWG && s_part[tid]) {  // the quantile band of row tid
     RowState& st = p.st[row0 + tid];

@@ -86,6 +86,9 @@ CASES = [
     # 128-row workgroups (8 waves): causal with D = 64, and two per 256-row block
     (1, 2, 2, 300, 64, 128, True, 300, 300),
     (1, 2, 1, 600, 128, 256, True, 600, 600),
+    # 12 heads over the XCD groups: whole heads per group and heads shared by all
+    (3, 4, 2, 200, 64, 64, False, 150, 150),
+    (3, 4, 1, 264, 128, 64, True, 264, 264),
 ]
 
 

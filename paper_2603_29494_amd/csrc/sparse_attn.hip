@@ -167,8 +167,10 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
 
   const int row0 = i * P + chunk * ROWS;
   const int row_end = min(N, min(i * P + P, row0 + ROWS));
-  const int count = __builtin_amdgcn_readfirstlane(
-      static_cast<int>(min<int64_t>(max(counts[bh * Np + i], 0), cap)));
+  // A valid list holds distinct keys of [0, N), so at most N of them; the
+  // clamp keeps the tile arithmetic below in range for any counts.
+  const int count = __builtin_amdgcn_readfirstlane(static_cast<int>(
+      min<int64_t>(min<int64_t>(max(counts[bh * Np + i], 0), cap), N)));
   const int32_t* list = idx + (bh * Np + i) * cap;
   const int ntiles = (count + kTile - 1) / kTile;
   // Tile order.  A block's keys are random rows of the head's K/V, far more
@@ -195,7 +197,7 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
     const unsigned int progress =
         __hip_atomic_load(&g_herd[xcd], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const unsigned int at = (progress / static_cast<unsigned int>(herd_slots)) % kHerdUnit;
-    // ntiles < 2^18 (N < 2^24), so the product fits 32 bits.
+    // ntiles <= 2^18 (count <= N < 2^24), so the product fits 32 bits.
     s_rot = static_cast<int>((at * static_cast<unsigned int>(ntiles)) / kHerdUnit);
   }
   __syncthreads();

@@ -34,6 +34,8 @@
 // read from a copy in MFMA operand order that each call writes once.
 #include <float.h>
 
+#include <type_traits>
+
 #include "device_common.h"
 #include "launch.h"
 
@@ -1537,6 +1539,16 @@ __global__ __launch_bounds__(256) void k_resolve_cand(SelParams p) {
 // loads do not wait for one another.
 constexpr int kCompactBatch = 8;
 
+// Orders this wave's LDS accesses on either side (a one-wave workgroup needs
+// no barrier).  Unlike __syncthreads() it does not wait for the wave's
+// global loads and stores: the prefetched bitmask words stay in flight and
+// the stores of the lists are not waited for.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 __global__ __launch_bounds__(64) void k_compact(SelParams p) {
   const int64_t r = blockIdx.x;
   const RowState& s = p.st[r];
@@ -1559,15 +1571,22 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
   // keep_diag: this block's own rows, [i P, min(N, (i + 1) P))
   const int diag_lo = p.keep_diag ? static_cast<int>(r % p.Np) * p.P : 0;
   const int diag_hi = p.keep_diag ? min(p.N, diag_lo + p.P) : 0;
-  // The next batch's words are loaded while this batch is listed.
+  // The next batch's words are loaded while this batch is listed.  Every
+  // load is issued (indices past the row's words are clamped to its last one
+  // and their words dropped when used), so that the compiler can count the
+  // loads in flight and wait for one batch only; rows with partial ties take
+  // a copy of the loop that also loads the tie words.
+  const int wlast = max(nw - 1, 0);
+  auto run = [&](auto tie_tag) __attribute__((always_inline)) {
+  constexpr bool TIEP = decltype(tie_tag)::value;
   uint32_t mb[kCompactBatch], tb[kCompactBatch], mn[kCompactBatch], tn[kCompactBatch];
   auto load_batch = [&](uint32_t (&m)[kCompactBatch], uint32_t (&t)[kCompactBatch], int c0)
       __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < kCompactBatch; ++j) {
-      const int wd = c0 + 64 * j + lane;
-      m[j] = wd < nw ? bsel[wd] : 0u;
-      t[j] = (tiep && wd < nw) ? btie[wd] : 0u;
+      const int wd = min(c0 + 64 * j + lane, wlast);
+      m[j] = bsel[wd];
+      t[j] = TIEP ? btie[wd] : 0u;
     }
   };
   load_batch(mb, tb, 0);
@@ -1577,9 +1596,9 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
     for (int j = 0; j < kCompactBatch; ++j) {
       const int wd = c0 + 64 * j + lane;
       if (c0 + 64 * j >= nw) break;  // uniform
-      uint32_t m = mb[j];
-      if (tiep) {  // uniform per row: keep only the first k_eq tied keys
-        const uint32_t tw = tb[j];
+      uint32_t m = wd < nw ? mb[j] : 0u;
+      if (TIEP) {  // keep only the first k_eq tied keys
+        const uint32_t tw = wd < nw ? tb[j] : 0u;
         const int nt = __builtin_popcount(tw);
         const int incl = wave_incl_scan(nt);
         int room = k_eq - (ties_seen + incl - nt);  // ties this lane may still keep
@@ -1608,7 +1627,7 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
         mm &= mm - 1;
         stage[pos++] = 32 * wd + bit;
       }
-      __syncthreads();
+      wave_sync();
       if (quads) {
         const int avail = pend + total;
         const int nq = avail / 4;
@@ -1617,13 +1636,13 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
         for (int t = lane; t < nq; t += 64) out4[t] = st4[t];
         const int rem = avail - 4 * nq;
         const int carry = lane < rem ? stage[4 * nq + lane] : 0;
-        __syncthreads();
+        wave_sync();
         if (lane < rem) stage[lane] = carry;
         done += 4 * nq;
       } else {
         for (int t = lane; t < total; t += 64)
           if (base + t < p.cap) out[base + t] = stage[t];
-        __syncthreads();
+        wave_sync();
       }
       base += total;
     }
@@ -1633,8 +1652,11 @@ __global__ __launch_bounds__(64) void k_compact(SelParams p) {
       tb[j] = tn[j];
     }
   }
+  };
+  if (tiep) run(std::true_type{});
+  else run(std::false_type{});
   if (quads) {  // the last entries, fewer than 4
-    __syncthreads();
+    wave_sync();
     if (lane < base - done) out[done + lane] = stage[lane];
   }
   const int n = min(base, static_cast<int>(p.cap));

@@ -128,3 +128,32 @@ def test_ordered_attention_parity(gpu, B, Hq, Hkv, N, D, P, causal):
                      .expand(B, Hq, Np).contiguous())):
         out, lse = va.sparse_attn(tq, tk, tv, ti, tc, P, causal, return_lse=True, order=o)
         check_attn(out, lse, o_ref, lse_ref, name)
+
+
+def test_order_not_a_permutation(gpu):
+    """Entries are clamped to [0, N_p); blocks an order row misses are left
+    unwritten, blocks it repeats are computed again (same result)."""
+    B, Hq, Hkv, N, D, P, causal = 1, 2, 1, 300, 64, 64, False
+    q = synth.random_bits(31, (B, Hq, N, D))
+    k = synth.random_bits(32, (B, Hkv, N, D))
+    v = synth.random_bits(33, (B, Hkv, N, D))
+    Np = (N + P - 1) // P  # 5, the last block 44 rows
+    cap = N
+    idx, cnt = lists(34, B, Hq, Np, N, P, causal, lambda r, L: r.integers(1, L + 1), cap)
+    o_ref, _ = oracle.sparse_attn(q, k, v, idx, cnt, P, causal)
+    tq, tk, tv = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).cuda() for x in (q, k, v))
+    rows = np.array([[0, 0, 7, -1, 2],   # clamped: 0, 0, 4, 0, 2 -> blocks 1 and 3 missed
+                     [3, 1, 3, 1, 3]])   # blocks 0, 2 and 4 missed
+    order = cuda_i32(rows.reshape(B, Hq, Np).astype(np.int32))
+    sentinel = 123.0
+    out = torch.full((B, Hq, N, D), sentinel, dtype=torch.bfloat16, device="cuda")
+    va.sparse_attn(tq, tk, tv, cuda_i32(idx), cuda_i32(cnt), P, causal, out=out, order=order)
+    o = out.float().cpu().numpy().astype(np.float64)
+    for h, taken in ((0, {0, 2, 4}), (1, {1, 3})):
+        for i in range(Np):
+            r0, r1 = i * P, min(N, (i + 1) * P)
+            blk = o[0, h, r0:r1]
+            if i in taken:
+                assert np.abs(blk - o_ref[0, h, r0:r1]).max() <= ATOL_MAX, (h, i)
+            else:
+                assert (blk == sentinel).all(), (h, i)

@@ -375,9 +375,10 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
     }
     // Lazy rescaling: x = s * scale - m_run (log2 units) is what exp2 needs
     // anyway, and the weights 2^x are computed first.  Their tile sum (of the
-    // bf16 weights that enter P V, two per dot2) bounds every weight, so a sum
-    // <= 256 on all lanes shows that no weight exceeds 256 (harmless in bf16 /
-    // fp32) and the reference m_run stays.  Otherwise (a new maximum, or
+    // fp32 weights, before the bf16 rounding of the ones that enter P V, so
+    // that the normaliser and the LSE carry no bf16 error) bounds every
+    // weight, so a sum <= 256 on all lanes shows that no weight exceeds 256
+    // (harmless in bf16 / fp32) and the reference m_run stays.  Otherwise (a new maximum, or
     // m_run = -inf: nothing seen yet) the rows whose maximum grew by more than
     // 8 move their reference, O and l are rescaled, and the weights are
     // recomputed.
@@ -391,22 +392,11 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
       for (int e = 0; e < 16; ++e) pf[e >> 3][e & 7] = __builtin_amdgcn_exp2f(x[e]);
       pb0 = __builtin_convertvector(pf[0], bf16x8);
       pb1 = __builtin_convertvector(pf[1], bf16x8);
-      // Pairs are taken with shufflevector: reading them through a bit_cast of
-      // the 8-vector has been miscompiled.
-      const bf16x2 one2 = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
-      float sum = 0.0f;
-      auto dot_pair = [&](const bf16x2 pr) __attribute__((always_inline)) {
-        sum = __builtin_amdgcn_fdot2_f32_bf16(pr, one2, sum, false);
-      };
-      dot_pair(__builtin_shufflevector(pb0, pb0, 0, 1));
-      dot_pair(__builtin_shufflevector(pb0, pb0, 2, 3));
-      dot_pair(__builtin_shufflevector(pb0, pb0, 4, 5));
-      dot_pair(__builtin_shufflevector(pb0, pb0, 6, 7));
-      dot_pair(__builtin_shufflevector(pb1, pb1, 0, 1));
-      dot_pair(__builtin_shufflevector(pb1, pb1, 2, 3));
-      dot_pair(__builtin_shufflevector(pb1, pb1, 4, 5));
-      dot_pair(__builtin_shufflevector(pb1, pb1, 6, 7));
-      return sum;
+      // a tree of fp32 adds (short dependency chains)
+      float s4[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s4[i] = (pf[0][i] + pf[0][i + 4]) + (pf[1][i] + pf[1][i + 4]);
+      return (s4[0] + s4[1]) + (s4[2] + s4[3]);
     };
     float tsum = weights();
     if (__any(!(tsum <= 256.0f))) {

@@ -3,11 +3,12 @@ Algorithm 2) against the CPU oracle, called through the C ABI.
 
 Tolerances: pooling is bit-exact (both sides round the exact block mean to
 bf16 once); attention output within max-abs 2e-2 and mean-abs 2e-3 of the fp64
-oracle on identical indices, LSE within 4e-3 absolute, empty rows exactly 0.
-The LSE bound follows from the arithmetic: the kernel's normaliser is the sum of
-the bf16-rounded softmax weights that also feed the P V product (each within a
-relative 2^-8 of its exact value, all positive), so log of the sum is within
-log(1 + 2^-8) = 3.9e-3 of the exact one, plus fp32 rounding.
+oracle on identical indices, LSE within 1e-4 absolute, empty rows exactly 0.
+The LSE bound follows from the arithmetic: the kernel's normaliser is the fp32
+sum of the fp32 softmax weights (each exp2 within a few ulp), a tree of four adds
+per lane and tile and one add per tile, so for T tiles log of the sum is within
+about (T + 8) 2^-23 of the exact one (under 3e-6 for the <= 16 tiles of these
+lists), plus the fp32 rounding of the scaled maximum (|m| <= 100: 4e-6).
 """
 import math
 
@@ -21,7 +22,7 @@ from paper_2603_29494_amd import synth
 
 pytestmark = pytest.mark.gpu
 
-ATOL_MAX, ATOL_MEAN, LSE_TOL = 2e-2, 2e-3, 4e-3
+ATOL_MAX, ATOL_MEAN, LSE_TOL = 2e-2, 2e-3, 1e-4
 
 
 def dev(bits: np.ndarray) -> torch.Tensor:

@@ -4,7 +4,7 @@ taken in that order (vecattn_sparse_attn_ordered), through the C ABI.
 The order is integer work, compared bit for bit with its definition written
 out in numpy (count descending, then the sampled mean key, then the block
 index).  The ordered attention must meet the attention bar of test_attn_gpu
-(max-abs 2e-2, mean-abs 2e-3 and LSE 4e-3 against the fp64 oracle) whatever
+(max-abs 2e-2, mean-abs 2e-3 and LSE 1e-4 against the fp64 oracle) whatever
 the order, since Eq. 4 treats the query blocks independently."""
 import numpy as np
 import pytest
@@ -16,7 +16,7 @@ from paper_2603_29494_amd import synth
 
 pytestmark = pytest.mark.gpu
 
-ATOL_MAX, ATOL_MEAN, LSE_TOL = 2e-2, 2e-3, 4e-3
+ATOL_MAX, ATOL_MEAN, LSE_TOL = 2e-2, 2e-3, 1e-4
 
 
 def lists(seed, B, H, Np, N, P, causal, counts_from, cap):

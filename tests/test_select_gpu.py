@@ -329,7 +329,7 @@ def test_varlen_batch(gpu, causal, mode, param):
         l = lse[Hq * r0:Hq * r1].view(1, Hq, n).cpu().numpy()
         ok = np.isfinite(lse_ref)
         assert np.array_equal(np.isfinite(l), ok)
-        assert np.abs(l[ok] - lse_ref[ok]).max() <= 4e-3  # log(1 + 2^-8): bf16 weights in the sum
+        assert np.abs(l[ok] - lse_ref[ok]).max() <= 1e-4  # fp32 normaliser (see test_attn_gpu)
 
 
 @pytest.mark.parametrize("mode,param", [("topk", 0.1), ("topp", 0.9), ("mins", 0.7)])

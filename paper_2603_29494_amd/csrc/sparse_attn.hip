@@ -112,6 +112,7 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
   constexpr int DS = D / 16;                // MFMA K-steps over the head dimension
   constexpr int DB = D / 32;                // 32-wide blocks of the head dimension
   constexpr int RB = 2 * D;                 // bytes per LDS row
+  constexpr bool kPrio = ROWS == 64;         // raised priority for the MFMA bursts
   // Each pipeline stage is its own LDS object, so that the compiler can tell
   // that reads of one stage do not depend on the gathers in flight into the
   // other and does not make them wait for those.
@@ -324,16 +325,19 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
     // S^T = K_tile Q^T for this wave's 32 keys x 32 rows.
     f32x16 sacc = f32x16{};
     const char* kb = reinterpret_cast<const char*>(kbuf(st)) + krow * RB;
-    // The MFMA bursts run at raised wave priority, so that a wave issuing them
-    // is not held back by the other wave's softmax work on the same SIMD.
-    __builtin_amdgcn_s_setprio(2);
+    // In 64-row workgroups the MFMA bursts run at raised wave priority, so that
+    // a wave issuing them is not held back by the softmax work of the other
+    // wave on its SIMD (which belongs to the other workgroup, at another point
+    // of its step).  The two waves a SIMD holds of an 8-wave workgroup are at
+    // the same point of the same step, and run faster without it.
+    if (kPrio) __builtin_amdgcn_s_setprio(2);
 #pragma unroll
     for (int s2 = 0; s2 < DS; ++s2) {
       const u32x4 a = *reinterpret_cast<const u32x4*>(kb + 16 * ((2 * s2 + g) ^ ksw));
       sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), qf[s2], sacc,
                                                      0, 0, 0);
     }
-    __builtin_amdgcn_s_setprio(0);
+    if (kPrio) __builtin_amdgcn_s_setprio(0);
     // The V^T operands (transposing LDS reads) are fetched now, so that their
     // latency hides behind the score MFMAs and the softmax.
     const char* vb = reinterpret_cast<const char*>(vbuf(st));
@@ -419,14 +423,14 @@ __global__ __launch_bounds__(4 * ROWS) void k_sparse_attn(
     l_run += tsum;
 
     // O^T += V_tile^T P^T.
-    __builtin_amdgcn_s_setprio(2);
+    if (kPrio) __builtin_amdgcn_s_setprio(2);
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks)
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vfrag[db][ks]),
                                                            ks ? pb1 : pb0, oacc[db], 0, 0, 0);
-    __builtin_amdgcn_s_setprio(0);
+    if (kPrio) __builtin_amdgcn_s_setprio(0);
   };
   for (int t = 0; t < ntiles; t += 2) {
     step(t, 0);

@@ -9,7 +9,7 @@
 // that must contain its cut, one pass over the keys at a time:
 //   HIST     score tiles stay on chip; each key of the row is classified
 //            against the interval (above / inside / below); keys inside land
-//            in a 256-bin LDS histogram, keys above are counted (and their
+//            in a 128-bin LDS histogram, keys above are counted (and their
 //            softmax mass summed for topP).  A resolve kernel picks the bin
 //            range that must hold the cut, which becomes the next interval.
 //   COLLECT  once the interval holds at most kCand keys: a bit per key at or
